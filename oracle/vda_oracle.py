@@ -1,0 +1,229 @@
+"""Plain fp64 CPU oracle for the Video Delta Attention (VDA) forward pass.
+
+TEST INFRASTRUCTURE ONLY.  Nothing in the product path imports or calls this
+module; only the test-suite, the smoke check and the benchmark's CPU-baseline
+leg may.  It shares no code, constants or helpers with the HIP library.
+
+It computes the operator straight from its definition in the paper
+(arXiv 2609.20744, "Video DeltaNet"), in float64, one head problem at a time,
+with no blocking, fusion or reordering beyond what the equations state:
+
+* Frame statistics, Eq. 3b (Section 3.1):
+      A_t = K_t^T Diag(beta_t) K_t,   B_t = V_t^T Diag(beta_t) K_t.
+* Joint frame update, Eq. 4 -> Eq. 5 (Section 3.2): the unique minimiser
+      S_t = (Sbar_t + B_t)(I + A_t)^{-1},
+  evaluated with a Cholesky solve of the SPD key-space matrix I + A_t.
+* With no decay input, Sbar_t = S_{t-1} (alpha = 1), so each frame is the
+  affine map S_t = S_{t-1} M_t + J_t of Eq. A.1 (Appendix A.1), scanned in
+  both temporal directions (Algorithm 1, step 5) from a zero initial state
+  (Eq. 1b with no text state).
+* Boundary gather, Eq. A.4 (Appendix A.3), with the local window reduced to
+  the query's own frame and alpha = 1: frame t reads P_{t-1} + R_{t+1}, the
+  forward state through the previous frame plus the reverse state through
+  the next one (the two regions are disjoint, Section 2.2, Eq. 1a).
+* Readout o_{t,u} = S~_t q_{t,u}, then the branch epilogue of Eq. 1c:
+      y = g * RMSNorm(o),  RMSNorm(o) = o / sqrt(mean_j o_j^2 + eps),
+  over the d_v channels of one token of one head, no learnable weight.
+
+Index convention: the paper numbers frames 1..F; arrays here use 0..F-1, so
+array frame i is the paper's frame t = i + 1.
+
+Every function here is pinned by the CPU tests against values the paper's
+equations fix independently of this code (closed forms, invariants, a
+hand-derived worked example, library routines and brute force).
+"""
+from __future__ import annotations
+
+import numpy as np
+import scipy.linalg
+
+#: RMSNorm epsilon.  The paper does not state it; 1e-6 is the reading used.
+RMS_EPS = 1e-6
+
+
+# ----------------------------------------------------------------------------
+# One frame
+# ----------------------------------------------------------------------------
+
+def frame_statistics(K: np.ndarray, V: np.ndarray, beta: np.ndarray):
+    """Eq. 3b: A = K^T Diag(beta) K (d_k x d_k), B = V^T Diag(beta) K (d_v x d_k).
+
+    K [U, d_k], V [U, d_v], beta [U] (all float64).
+    """
+    KD = K * beta[:, None]          # Diag(beta) K
+    A = K.T @ KD
+    B = V.T @ KD
+    return A, B
+
+
+def joint_frame_update(S_bar: np.ndarray, A: np.ndarray, B: np.ndarray) -> np.ndarray:
+    """Eq. 5: the S solving S (I + A) = S_bar + B.
+
+    I + A is symmetric positive definite (A is a beta-weighted Gram matrix,
+    beta >= 0; Appendix A.1), so the right solve X C = Y is done as
+    C X^T = Y^T with a Cholesky factorisation.
+    """
+    C = np.eye(A.shape[0]) + A
+    Y = S_bar + B
+    factor = scipy.linalg.cho_factor(C, lower=True)
+    return scipy.linalg.cho_solve(factor, Y.T).T
+
+
+def frame_transition(A: np.ndarray, B: np.ndarray, alpha: np.ndarray | None = None):
+    """Eq. A.1: M = Diag(alpha) (I + A)^{-1}, J = B (I + A)^{-1}.
+
+    Used by the composition and contraction checks; the scan itself uses
+    joint_frame_update, which is the same map.
+    """
+    Cinv = np.linalg.inv(np.eye(A.shape[0]) + A)
+    M = Cinv if alpha is None else np.diag(alpha) @ Cinv
+    return M, B @ Cinv
+
+
+# ----------------------------------------------------------------------------
+# One head problem: scans, gather, readout, epilogue
+# ----------------------------------------------------------------------------
+
+def head_statistics(k: np.ndarray, v: np.ndarray, beta: np.ndarray):
+    """Eq. 3b for every frame of one head.  k [F,N,d_k], v [F,N,d_v], beta [F,N]."""
+    F = k.shape[0]
+    As = np.empty((F, k.shape[2], k.shape[2]))
+    Bs = np.empty((F, v.shape[2], k.shape[2]))
+    for t in range(F):
+        As[t], Bs[t] = frame_statistics(k[t], v[t], beta[t])
+    return As, Bs
+
+
+def scan_states(As: np.ndarray, Bs: np.ndarray, S0: np.ndarray) -> np.ndarray:
+    """Apply the frame map of Eq. 5 (alpha = 1) to frames 0..F-1 in order.
+
+    Returns [F+1, d_v, d_k]: element j is the state after the first j frames
+    (element 0 is the initial state S0).
+    """
+    F = As.shape[0]
+    out = np.empty((F + 1,) + S0.shape)
+    out[0] = S0
+    for t in range(F):
+        out[t + 1] = joint_frame_update(out[t], As[t], Bs[t])
+    return out
+
+
+def forward_states(As, Bs, S0=None):
+    """Forward scan (Algorithm 1, step 5).  P[j] = state through frames 1..j
+    (paper numbering), P[0] the virtual initial state."""
+    d_v, d_k = Bs.shape[1], Bs.shape[2]
+    S0 = np.zeros((d_v, d_k)) if S0 is None else S0
+    return scan_states(As, Bs, S0)
+
+
+def reverse_states(As, Bs, S0=None):
+    """Reverse scan (Algorithm 1, step 5), the same frame map applied from the
+    last frame down.  Returns R of length F+2 in paper numbering:
+    R[j] = state through frames F..j for j = 1..F, R[F+1] = initial state,
+    R[0] unused (zero)."""
+    F, d_v, d_k = Bs.shape
+    S0 = np.zeros((d_v, d_k)) if S0 is None else S0
+    rev = scan_states(As[::-1], Bs[::-1], S0)      # rev[m] = through last m frames
+    R = np.zeros((F + 2, d_v, d_k))
+    for j in range(1, F + 2):
+        R[j] = rev[F + 1 - j]
+    return R
+
+
+def gathered_states(As, Bs) -> np.ndarray:
+    """Eq. A.4 with window [t, t] and alpha = 1, no text state: the state read
+    by array frame i (paper frame t = i + 1) is P_{t-1} + R_{t+1}.
+    Returns [F, d_v, d_k]."""
+    F = As.shape[0]
+    P = forward_states(As, Bs)
+    R = reverse_states(As, Bs)
+    return np.stack([P[t - 1] + R[t + 1] for t in range(1, F + 1)])
+
+
+def readout(S_tilde: np.ndarray, q: np.ndarray) -> np.ndarray:
+    """Eq. A.4 last line / Eq. 1a: o_{t,u} = S~_t q_{t,u}.  q [U, d_k] -> [U, d_v]."""
+    return q @ S_tilde.T
+
+
+def rmsnorm_gate(o: np.ndarray, gate: float, eps: float = RMS_EPS) -> np.ndarray:
+    """Eq. 1c, linear branch: g * RMSNorm(o) over the last (d_v) axis."""
+    ms = np.mean(o * o, axis=-1, keepdims=True)
+    return gate * o / np.sqrt(ms + eps)
+
+
+def head_forward(q, k, v, beta, gate: float, eps: float = RMS_EPS) -> np.ndarray:
+    """Whole operator for one head problem.  q,k [F,N,d_k], v [F,N,d_v],
+    beta [F,N] (float64, beta >= 0) -> y [F,N,d_v]."""
+    if np.any(beta < 0):
+        raise ValueError("write strengths must be non-negative")
+    As, Bs = head_statistics(k, v, beta)
+    St = gathered_states(As, Bs)
+    y = np.empty(q.shape[:2] + (v.shape[2],))
+    for t in range(q.shape[0]):
+        y[t] = rmsnorm_gate(readout(St[t], q[t]), gate, eps)
+    return y
+
+
+def vda_forward(q, k, v, beta, gate, eps: float = RMS_EPS) -> np.ndarray:
+    """All head problems: q,k [H,F,N,d_k], v [H,F,N,d_v], beta [H,F,N],
+    gate [H] (float64) -> y [H,F,N,d_v]."""
+    return np.stack([head_forward(q[h], k[h], v[h], beta[h], float(gate[h]), eps)
+                     for h in range(q.shape[0])])
+
+
+def head_forward_sampled(q, k, v, beta, gate: float, frames, tokens,
+                         eps: float = RMS_EPS) -> np.ndarray:
+    """Outputs of one head at the listed (frame, token) positions only.
+
+    The states still come from every frame of the head (the scans need all of
+    them); only the readout is restricted.  Returns [len(frames), d_v].
+    """
+    As, Bs = head_statistics(k, v, beta)
+    St = gathered_states(As, Bs)
+    frames = np.asarray(frames)
+    tokens = np.asarray(tokens)
+    o = np.einsum("sjc,sc->sj", St[frames], q[frames, tokens])
+    return rmsnorm_gate(o, gate, eps)
+
+
+# ----------------------------------------------------------------------------
+# Other forms of the same rule, and neighbouring rules, for the checks
+# ----------------------------------------------------------------------------
+
+def objective(S, S_bar, K, V, beta) -> float:
+    """Eq. 4: 1/2 ||S - S_bar||_F^2 + 1/2 sum_u beta_u ||S k_u - v_u||^2."""
+    r = K @ S.T - V                       # rows: S k_u - v_u
+    return 0.5 * np.sum((S - S_bar) ** 2) + 0.5 * np.sum(beta * np.sum(r * r, axis=1))
+
+
+def joint_frame_update_token_space(S_bar, K, V, beta) -> np.ndarray:
+    """The same minimiser reached through a U x U solve in token space.
+
+    The first-order condition of Eq. 4 reads S = S_bar + W^T K with
+    W = Diag(beta)(V - K S^T) (Appendix A.2's rearranged form); substituting
+    S gives (I_U + Diag(beta) K K^T) W = Diag(beta)(V - K S_bar^T).
+    """
+    U = K.shape[0]
+    D = np.diag(beta)
+    W = np.linalg.solve(np.eye(U) + D @ K @ K.T, D @ (V - K @ S_bar.T))
+    return S_bar + W.T @ K
+
+
+def token_delta_rule(S0, keys, values, betas, alphas=None) -> np.ndarray:
+    """Eq. 2, one token per step: Sbar = S Diag(alpha); S = Sbar + beta (v - Sbar k) k^T.
+    keys [T,d_k], values [T,d_v], betas [T]; returns the final state."""
+    S = np.array(S0, dtype=np.float64)
+    for i in range(keys.shape[0]):
+        if alphas is not None:
+            S = S @ np.diag(alphas[i])
+        kk, vv = keys[i], values[i]
+        S = S + betas[i] * np.outer(vv - S @ kk, kk)
+    return S
+
+
+def frozen_state_update(S_bar, A, B, U: int | None = None) -> np.ndarray:
+    """Eq. 3c: S = S_bar (I - A) + B; with U given, the 1/sqrt(U) key scaling
+    of Appendix A.2 (A -> A/U, B -> B/sqrt(U))."""
+    if U is not None:
+        A, B = A / U, B / np.sqrt(U)
+    return S_bar @ (np.eye(A.shape[0]) - A) + B

@@ -1,0 +1,518 @@
+"""Pins of the fp64 oracle against what the paper and the mathematics fix.
+
+Each ``pin_*`` function checks the oracle against something other than its own
+code: a hand-derived worked example, a closed form printed in the paper, an
+invariant the paper proves, a library routine, or brute force on tiny inputs.
+``test_mutants_are_caught`` plants plausible mistakes in the oracle (on the CPU)
+and checks that at least one pin fails for each.
+"""
+import json
+import math
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+import oracle.vda_oracle as O
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _rng(seed):
+    return np.random.default_rng(seed)
+
+
+def _unit_rows(x):
+    return x / np.linalg.norm(x, axis=-1, keepdims=True)
+
+
+def _random_frame(rng, U=7, d_k=5, d_v=4):
+    K = _unit_rows(rng.standard_normal((U, d_k)))
+    V = rng.standard_normal((U, d_v))
+    beta = 1.0 / (1.0 + np.exp(-rng.standard_normal(U)))
+    return K, V, beta
+
+
+def _random_clip(rng, F=5, N=6, d_k=4, d_v=3):
+    q = _unit_rows(rng.standard_normal((F, N, d_k)))
+    k = _unit_rows(rng.standard_normal((F, N, d_k)))
+    v = rng.standard_normal((F, N, d_v))
+    beta = 1.0 / (1.0 + np.exp(-rng.standard_normal((F, N))))
+    return q, k, v, beta
+
+
+def _frac(a):
+    return np.vectorize(lambda s: float(Fraction(s)))(np.array(a, dtype=object)).astype(np.float64)
+
+
+# ----------------------------------------------------------------------------
+# Pins
+# ----------------------------------------------------------------------------
+
+def pin_golden_hand_example():
+    """Hand-derived exact example (tests/golden): Eq. 3b, 5, A.1, A.4, 1a, 1c."""
+    with open(os.path.join(GOLDEN, "hand_example_dk2_dv2_F3.json")) as f:
+        g = json.load(f)
+    k = np.stack([_frac(fr["k"]) for fr in g["frames"]])
+    v = np.stack([_frac(fr["v"]) for fr in g["frames"]])
+    q = np.stack([_frac(fr["q"]) for fr in g["frames"]])
+    beta = np.stack([_frac(fr["beta"]) for fr in g["frames"]])
+    gate = float(Fraction(g["gate"]))
+    As, Bs = O.head_statistics(k, v, beta)
+    np.testing.assert_allclose(np.eye(2)[None] + As, _frac(g["A"]), rtol=0, atol=1e-14)
+    np.testing.assert_allclose(Bs, _frac(g["B"]), rtol=0, atol=1e-14)
+    P = O.forward_states(As, Bs)
+    np.testing.assert_allclose(P, _frac(g["P"]), rtol=0, atol=1e-14)
+    R = O.reverse_states(As, Bs)
+    np.testing.assert_allclose(R[1:], _frac(g["R"]), rtol=0, atol=1e-14)
+    St = O.gathered_states(As, Bs)
+    np.testing.assert_allclose(St, _frac(g["S_tilde"]), rtol=0, atol=1e-14)
+    o_expect = _frac(g["o"])
+    ms = _frac(g["ms"])
+    for t in range(3):
+        o = O.readout(St[t], q[t])
+        np.testing.assert_allclose(o, o_expect[t], rtol=0, atol=1e-14)
+        y = O.rmsnorm_gate(o, gate, eps=0.0)
+        np.testing.assert_allclose(y, gate * o_expect[t] / np.sqrt(ms[t])[:, None],
+                                   rtol=1e-14, atol=1e-14)
+    y_all = O.head_forward(q, k, v, beta, gate, eps=0.0)
+    np.testing.assert_allclose(y_all, gate * o_expect / np.sqrt(ms)[..., None], rtol=1e-14)
+
+
+def pin_stats_outer_product_sum():
+    """Eq. 3b, left forms: A = sum_u beta k k^T, B = sum_u beta v k^T (token loop)."""
+    rng = _rng(1)
+    K, V, beta = _random_frame(rng, U=9, d_k=5, d_v=3)
+    A_loop = np.zeros((5, 5))
+    B_loop = np.zeros((3, 5))
+    for u in range(9):
+        for i in range(5):
+            for j in range(5):
+                A_loop[i, j] += beta[u] * K[u, i] * K[u, j]
+        for i in range(3):
+            for j in range(5):
+                B_loop[i, j] += beta[u] * V[u, i] * K[u, j]
+    A, B = O.frame_statistics(K, V, beta)
+    np.testing.assert_allclose(A, A_loop, rtol=1e-13, atol=1e-14)
+    np.testing.assert_allclose(B, B_loop, rtol=1e-13, atol=1e-14)
+
+
+def pin_solve_matches_dense_inverse():
+    """Eq. 5 against an explicit dense inverse (library routine)."""
+    rng = _rng(2)
+    for d_k, d_v, U in [(4, 3, 6), (8, 8, 20), (16, 8, 40)]:
+        K, V, beta = _random_frame(rng, U, d_k, d_v)
+        S_bar = rng.standard_normal((d_v, d_k))
+        A, B = O.frame_statistics(K, V, beta)
+        S = O.joint_frame_update(S_bar, A, B)
+        S_ref = (S_bar + B) @ np.linalg.inv(np.eye(d_k) + A)
+        np.testing.assert_allclose(S, S_ref, rtol=1e-12, atol=1e-13)
+
+
+def pin_solve_matches_token_space():
+    """The key-space solve equals the U x U token-space solve of the same
+    first-order condition (the N x N correction solve)."""
+    rng = _rng(3)
+    for d_k, d_v, U in [(4, 3, 2), (4, 3, 9), (6, 5, 30)]:
+        K, V, beta = _random_frame(rng, U, d_k, d_v)
+        S_bar = rng.standard_normal((d_v, d_k))
+        A, B = O.frame_statistics(K, V, beta)
+        S = O.joint_frame_update(S_bar, A, B)
+        S_tok = O.joint_frame_update_token_space(S_bar, K, V, beta)
+        np.testing.assert_allclose(S, S_tok, rtol=1e-12, atol=1e-13)
+
+
+def pin_solve_kronecker_bruteforce():
+    """Brute force: vec(S C) = (C^T kron I) vec(S) (row-major vec), solved densely."""
+    rng = _rng(4)
+    d_k, d_v, U = 4, 3, 5
+    K, V, beta = _random_frame(rng, U, d_k, d_v)
+    S_bar = rng.standard_normal((d_v, d_k))
+    C = np.eye(d_k)
+    for u in range(U):
+        C = C + beta[u] * np.outer(K[u], K[u])
+    rhs = S_bar.copy()
+    for u in range(U):
+        rhs = rhs + beta[u] * np.outer(V[u], K[u])
+    # row-major vec: vec(S C)[i*d_k + j] = sum_m S[i,m] C[m,j]
+    big = np.kron(np.eye(d_v), C.T)
+    S_bf = np.linalg.solve(big, rhs.reshape(-1)).reshape(d_v, d_k)
+    A, B = O.frame_statistics(K, V, beta)
+    np.testing.assert_allclose(O.joint_frame_update(S_bar, A, B), S_bf, rtol=1e-12, atol=1e-13)
+
+
+def _eq4(S, S_bar, K, V, beta):
+    """Eq. 4 written out token by token."""
+    val = 0.5 * float(np.sum((S - S_bar) ** 2))
+    for u in range(K.shape[0]):
+        r = S @ K[u] - V[u]
+        val += 0.5 * beta[u] * float(r @ r)
+    return val
+
+
+def pin_solve_minimises_eq4():
+    """Eq. 4: the update is a stationary point (central differences) and a
+    strict minimum against random perturbations."""
+    rng = _rng(5)
+    d_k, d_v, U = 4, 3, 6
+    K, V, beta = _random_frame(rng, U, d_k, d_v)
+    S_bar = rng.standard_normal((d_v, d_k))
+    A, B = O.frame_statistics(K, V, beta)
+    S = O.joint_frame_update(S_bar, A, B)
+    h = 1e-5
+    grad = np.zeros_like(S)
+    for i in range(d_v):
+        for j in range(d_k):
+            E = np.zeros_like(S)
+            E[i, j] = h
+            grad[i, j] = (_eq4(S + E, S_bar, K, V, beta) - _eq4(S - E, S_bar, K, V, beta)) / (2 * h)
+    assert np.max(np.abs(grad)) < 1e-8, grad
+    f0 = _eq4(S, S_bar, K, V, beta)
+    for _ in range(20):
+        D = rng.standard_normal(S.shape) * 1e-3
+        assert _eq4(S + D, S_bar, K, V, beta) > f0
+
+
+def pin_prop1_spectral_norm():
+    """Proposition 1 / Eq. A.2: ||Diag(alpha)(I + A)^-1||_2 <= 1 for beta >= 0,
+    alpha in [0, 1]; and ||(I+A)^-1||_2 = 1 / (1 + lambda_min(A))."""
+    rng = _rng(6)
+    for U in [1, 3, 50, 400]:
+        K, V, beta = _random_frame(rng, U, 8, 4)
+        A, Bm = O.frame_statistics(K, V, beta)
+        Cinv = np.linalg.inv(np.eye(8) + A)
+        lam_min = np.linalg.eigvalsh(A)[0]
+        np.testing.assert_allclose(np.linalg.norm(Cinv, 2), 1.0 / (1.0 + lam_min), rtol=1e-10)
+        assert np.linalg.norm(Cinv, 2) <= 1.0 + 1e-12
+        alpha = rng.random(8)
+        M, _ = O.frame_transition(A, Bm, alpha)
+        assert np.linalg.svd(M, compute_uv=False)[0] <= 1.0 + 1e-12
+
+
+def pin_beta_zero_keeps_state():
+    """beta = 0: the frame writes nothing (S_t = S_bar), and zero-strength
+    tokens can be deleted without changing the state (Eq. 3b sums)."""
+    rng = _rng(7)
+    K, V, beta = _random_frame(rng, 6, 5, 3)
+    S_bar = rng.standard_normal((3, 5))
+    A, B = O.frame_statistics(K, V, np.zeros(6))
+    np.testing.assert_array_equal(O.joint_frame_update(S_bar, A, B), S_bar)
+    beta2 = beta.copy()
+    beta2[[1, 4]] = 0.0
+    A2, B2 = O.frame_statistics(K, V, beta2)
+    keep = [0, 2, 3, 5]
+    A3, B3 = O.frame_statistics(K[keep], V[keep], beta2[keep])
+    np.testing.assert_allclose(O.joint_frame_update(S_bar, A2, B2),
+                               O.joint_frame_update(S_bar, A3, B3), rtol=1e-13, atol=1e-14)
+
+
+def pin_repeated_key_eqA3():
+    """Eq. A.3: U copies of one unit key with common beta give
+    S_t k = s / (1 + U beta) + U beta / (1 + U beta) * vbar, s = S_bar k."""
+    rng = _rng(8)
+    d_k, d_v = 6, 4
+    for U, b in [(1, 0.3), (5, 0.7), (64, 0.5)]:
+        k = _unit_rows(rng.standard_normal(d_k))
+        K = np.tile(k, (U, 1))
+        V = rng.standard_normal((U, d_v))
+        S_bar = rng.standard_normal((d_v, d_k))
+        A, B = O.frame_statistics(K, V, np.full(U, b))
+        S = O.joint_frame_update(S_bar, A, B)
+        s = S_bar @ k
+        vbar = V.mean(axis=0)
+        expect = s / (1 + U * b) + U * b / (1 + U * b) * vbar
+        np.testing.assert_allclose(S @ k, expect, rtol=1e-12, atol=1e-13)
+        # directions orthogonal to k are untouched
+        x = rng.standard_normal(d_k)
+        x -= (x @ k) * k
+        np.testing.assert_allclose(S @ x, S_bar @ x, rtol=1e-12, atol=1e-13)
+
+
+def pin_orthonormal_keys_weight():
+    """Appendix A.2: orthogonal keys each receive weight beta / (1 + beta):
+    S_t k_u = s_u + beta_u / (1 + beta_u) (v_u - s_u)."""
+    rng = _rng(9)
+    d_k, d_v, U = 8, 3, 5
+    Qm, _ = np.linalg.qr(rng.standard_normal((d_k, d_k)))
+    K = Qm[:U]
+    V = rng.standard_normal((U, d_v))
+    beta = rng.random(U) * 2
+    S_bar = rng.standard_normal((d_v, d_k))
+    A, B = O.frame_statistics(K, V, beta)
+    S = O.joint_frame_update(S_bar, A, B)
+    for u in range(U):
+        s = S_bar @ K[u]
+        np.testing.assert_allclose(S @ K[u], s + beta[u] / (1 + beta[u]) * (V[u] - s),
+                                   rtol=1e-12, atol=1e-13)
+
+
+def pin_token_permutation_invariance():
+    """The frame update imposes no patch order: permuting a frame's tokens
+    (k, v, beta together) leaves the state unchanged."""
+    rng = _rng(10)
+    K, V, beta = _random_frame(rng, 11, 6, 4)
+    S_bar = rng.standard_normal((4, 6))
+    perm = rng.permutation(11)
+    A, B = O.frame_statistics(K, V, beta)
+    Ap, Bp = O.frame_statistics(K[perm], V[perm], beta[perm])
+    np.testing.assert_allclose(O.joint_frame_update(S_bar, A, B),
+                               O.joint_frame_update(S_bar, Ap, Bp), rtol=1e-12, atol=1e-13)
+
+
+def pin_n1_reduces_to_token_delta_rule():
+    """One token per frame: the forward scan equals the token-wise delta rule
+    of Eq. 2 (alpha = 1) with write strength beta' = beta / (1 + beta ||k||^2)
+    (Sherman-Morrison), and differs from it with the same beta."""
+    rng = _rng(11)
+    F, d_k, d_v = 9, 5, 4
+    k = rng.standard_normal((F, 1, d_k))          # not unit: exercises ||k||^2
+    v = rng.standard_normal((F, 1, d_v))
+    beta = rng.random((F, 1)) * 1.5
+    As, Bs = O.head_statistics(k, v, beta)
+    P = O.forward_states(As, Bs)
+    kn2 = np.sum(k[:, 0] ** 2, axis=1)
+    beta_p = beta[:, 0] / (1 + beta[:, 0] * kn2)
+    S_tok = O.token_delta_rule(np.zeros((d_v, d_k)), k[:, 0], v[:, 0], beta_p)
+    np.testing.assert_allclose(P[F], S_tok, rtol=1e-12, atol=1e-13)
+    S_same = O.token_delta_rule(np.zeros((d_v, d_k)), k[:, 0], v[:, 0], beta[:, 0])
+    assert np.max(np.abs(P[F] - S_same)) > 1e-3
+    # a non-zero entering state as well
+    S0 = rng.standard_normal((d_v, d_k))
+    P2 = O.forward_states(As, Bs, S0)
+    np.testing.assert_allclose(P2[F], O.token_delta_rule(S0, k[:, 0], v[:, 0], beta_p),
+                               rtol=1e-12, atol=1e-13)
+
+
+def pin_reverse_is_forward_on_reversed_frames():
+    """Algorithm 1 step 5: the reverse scan is the forward scan run on the
+    time-reversed frames, reversed back; and it matches an explicit
+    descending loop of Eq. A.1."""
+    rng = _rng(12)
+    q, k, v, beta = _random_clip(rng, F=6)
+    As, Bs = O.head_statistics(k, v, beta)
+    R = O.reverse_states(As, Bs)
+    Pr = O.forward_states(As[::-1], Bs[::-1])
+    F = 6
+    for j in range(1, F + 2):
+        np.testing.assert_allclose(R[j], Pr[F + 1 - j], rtol=1e-13, atol=1e-14)
+    S = np.zeros_like(Bs[0])
+    for t in range(F, 0, -1):
+        M, J = O.frame_transition(As[t - 1], Bs[t - 1])
+        S = S @ M + J
+        np.testing.assert_allclose(R[t], S, rtol=1e-12, atol=1e-13)
+
+
+def pin_perturbation_contracts():
+    """Eq. A.2: changing the entering state by dS changes the frame's result
+    by at most ||dS||_F."""
+    rng = _rng(13)
+    for U in [1, 4, 100]:
+        K, V, beta = _random_frame(rng, U, 6, 5)
+        A, B = O.frame_statistics(K, V, beta)
+        for _ in range(10):
+            S1 = rng.standard_normal((5, 6))
+            dS = rng.standard_normal((5, 6))
+            d_out = O.joint_frame_update(S1 + dS, A, B) - O.joint_frame_update(S1, A, B)
+            assert np.linalg.norm(d_out) <= np.linalg.norm(dS) * (1 + 1e-12)
+
+
+def pin_affine_composition():
+    """Eq. A.1: frames a..b compose into one affine map S -> S M + J with
+    M = M_a ... M_b, J = (...(J_a M_{a+1} + J_{a+1}) M_{a+2} ...) + J_b."""
+    rng = _rng(14)
+    q, k, v, beta = _random_clip(rng, F=7)
+    As, Bs = O.head_statistics(k, v, beta)
+    S0 = rng.standard_normal(Bs[0].shape)
+    P = O.forward_states(As, Bs, S0)
+    M_tot = np.eye(As.shape[1])
+    J_tot = np.zeros_like(Bs[0])
+    for t in range(2, 6):          # frames 3..6 in paper numbering
+        M, J = O.frame_transition(As[t], Bs[t])
+        M_tot = M_tot @ M
+        J_tot = J_tot @ M + J
+    np.testing.assert_allclose(P[2] @ M_tot + J_tot, P[6], rtol=1e-12, atol=1e-13)
+
+
+def pin_whole_operator_orthonormal_keys():
+    """Whole operator, before the epilogue: with every key of the clip
+    mutually orthonormal, each frame write stays in its own key directions, so
+    o_{t,u} = sum_{j != t} sum_w beta/(1+beta) (k_{j,w} . q_{t,u}) v_{j,w}."""
+    rng = _rng(15)
+    F, N, d_k, d_v = 4, 3, 16, 5
+    Qm, _ = np.linalg.qr(rng.standard_normal((d_k, d_k)))
+    k = Qm[: F * N].reshape(F, N, d_k)
+    v = rng.standard_normal((F, N, d_v))
+    beta = rng.random((F, N)) * 3
+    q = _unit_rows(rng.standard_normal((F, N, d_k)))
+    As, Bs = O.head_statistics(k, v, beta)
+    St = O.gathered_states(As, Bs)
+    for t in range(F):
+        for u in range(N):
+            expect = np.zeros(d_v)
+            for j in range(F):
+                if j == t:
+                    continue
+                for w in range(N):
+                    expect += beta[j, w] / (1 + beta[j, w]) * (k[j, w] @ q[t, u]) * v[j, w]
+            np.testing.assert_allclose(O.readout(St[t], q[t])[u], expect, rtol=1e-12, atol=1e-13)
+
+
+def pin_single_frame_and_lone_writer():
+    """Eq. A.4 edge cases: a one-frame clip reads no distant video (y = 0);
+    when only frame j writes, frame j reads nothing and every other frame
+    reads exactly frame j's single-frame state B_j (I + A_j)^-1."""
+    rng = _rng(16)
+    q, k, v, beta = _random_clip(rng, F=1)
+    y = O.head_forward(q, k, v, beta, 0.7)
+    assert np.all(y == 0.0)
+    q, k, v, beta = _random_clip(rng, F=5)
+    beta[[0, 1, 3, 4]] = 0.0
+    As, Bs = O.head_statistics(k, v, beta)
+    St = O.gathered_states(As, Bs)
+    lone = Bs[2] @ np.linalg.inv(np.eye(As.shape[1]) + As[2])
+    assert np.all(St[2] == 0.0)
+    for t in [0, 1, 3, 4]:
+        np.testing.assert_allclose(St[t], lone, rtol=1e-12, atol=1e-13)
+
+
+def pin_rmsnorm_library_and_invariances():
+    """Eq. 1c: matches torch's RMSNorm (library routine) times the gate; y is
+    invariant to v -> c v (c > 0; o is linear in v from a zero state) up to
+    eps, and linear in the gate."""
+    import torch
+    rng = _rng(17)
+    o = rng.standard_normal((10, 7))
+    y = O.rmsnorm_gate(o, 0.3, eps=1e-6)
+    ref = 0.3 * torch.nn.functional.rms_norm(torch.from_numpy(o), (7,), eps=1e-6).numpy()
+    np.testing.assert_allclose(y, ref, rtol=1e-12, atol=1e-14)
+    q, k, v, beta = _random_clip(rng, F=4)
+    y1 = O.head_forward(q, k, v, beta, 0.5, eps=0.0)
+    y2 = O.head_forward(q, k, 3.0 * v, beta, 0.5, eps=0.0)
+    np.testing.assert_allclose(y1, y2, rtol=1e-11, atol=1e-12)
+    y3 = O.head_forward(q, k, v, beta, 0.25, eps=0.0)
+    np.testing.assert_allclose(y3, 0.5 * y1, rtol=1e-13, atol=1e-15)
+    # per-token mean square of the normalised output is gate^2 (eps = 0)
+    np.testing.assert_allclose(np.mean(y1 ** 2, axis=-1), 0.25, rtol=1e-12)
+
+
+def pin_sampled_matches_full():
+    """The sampled readout used at full sizes equals the full operator."""
+    rng = _rng(18)
+    q, k, v, beta = _random_clip(rng, F=5, N=9, d_k=6, d_v=4)
+    y = O.head_forward(q, k, v, beta, 0.8)
+    frames = [0, 2, 4, 4, 1]
+    toks = [3, 8, 0, 5, 1]
+    ys = O.head_forward_sampled(q, k, v, beta, 0.8, frames, toks)
+    np.testing.assert_allclose(ys, y[frames, toks], rtol=1e-13, atol=1e-14)
+
+
+PINS = [f for name, f in sorted(globals().items()) if name.startswith("pin_")]
+
+
+@pytest.mark.parametrize("pin", PINS, ids=[p.__name__ for p in PINS])
+def test_pin(pin):
+    pin()
+
+
+# ----------------------------------------------------------------------------
+# Planted mistakes: each must be caught by at least one pin
+# ----------------------------------------------------------------------------
+
+def _mut_stats_no_beta(K, V, beta):
+    return K.T @ K, V.T @ K
+
+
+def _mut_stats_beta_squared(K, V, beta):
+    KD = K * (beta ** 2)[:, None]
+    return K.T @ KD, V.T @ KD
+
+
+def _mut_update_no_identity(S_bar, A, B):
+    return (S_bar + B) @ np.linalg.pinv(A)
+
+
+def _mut_update_frozen_state(S_bar, A, B):
+    return S_bar @ (np.eye(A.shape[0]) - A) + B
+
+
+def _mut_update_drop_inherited(S_bar, A, B):
+    return B @ np.linalg.inv(np.eye(A.shape[0]) + A)
+
+
+def _mut_update_wrong_sign(S_bar, A, B):
+    return (S_bar - B) @ np.linalg.inv(np.eye(A.shape[0]) + A)
+
+
+def _mut_gather_inclusive(As, Bs):
+    F = As.shape[0]
+    P = O.forward_states(As, Bs)
+    R = O.reverse_states(As, Bs)
+    return np.stack([P[t] + R[t] for t in range(1, F + 1)])
+
+
+def _mut_gather_forward_only(As, Bs):
+    F = As.shape[0]
+    P = O.forward_states(As, Bs)
+    return np.stack([P[t - 1] for t in range(1, F + 1)])
+
+
+def _mut_gather_swapped(As, Bs):
+    F = As.shape[0]
+    P = O.forward_states(As, Bs)
+    R = O.reverse_states(As, Bs)
+    zero = np.zeros_like(P[0])
+    return np.stack([(R[t - 1] if t >= 2 else zero) + (P[t + 1] if t + 1 <= F else zero)
+                     for t in range(1, F + 1)])
+
+
+def _mut_reverse_not_reversed(As, Bs, S0=None):
+    F, d_v, d_k = Bs.shape
+    fwd = O.scan_states(As, Bs, np.zeros((d_v, d_k)) if S0 is None else S0)
+    R = np.zeros((F + 2, d_v, d_k))
+    for j in range(1, F + 2):
+        R[j] = fwd[F + 1 - j]
+    return R
+
+
+def _mut_readout_transposed(S_tilde, q):
+    return q @ S_tilde
+
+
+def _mut_rms_sum_not_mean(o, gate, eps=O.RMS_EPS):
+    return gate * o / np.sqrt(np.sum(o * o, axis=-1, keepdims=True) + eps)
+
+
+def _mut_rms_gate_inside(o, gate, eps=O.RMS_EPS):
+    og = gate * o
+    return og / np.sqrt(np.mean(og * og, axis=-1, keepdims=True) + eps)
+
+
+MUTANTS = [
+    ("frame_statistics", _mut_stats_no_beta),
+    ("frame_statistics", _mut_stats_beta_squared),
+    ("joint_frame_update", _mut_update_no_identity),
+    ("joint_frame_update", _mut_update_frozen_state),
+    ("joint_frame_update", _mut_update_drop_inherited),
+    ("joint_frame_update", _mut_update_wrong_sign),
+    ("gathered_states", _mut_gather_inclusive),
+    ("gathered_states", _mut_gather_forward_only),
+    ("gathered_states", _mut_gather_swapped),
+    ("reverse_states", _mut_reverse_not_reversed),
+    ("readout", _mut_readout_transposed),
+    ("rmsnorm_gate", _mut_rms_sum_not_mean),
+    ("rmsnorm_gate", _mut_rms_gate_inside),
+]
+
+
+@pytest.mark.parametrize("target,mutant", MUTANTS, ids=[m.__name__ for _, m in MUTANTS])
+def test_mutants_are_caught(monkeypatch, target, mutant):
+    monkeypatch.setattr(O, target, mutant)
+    caught = []
+    for pin in PINS:
+        try:
+            with np.errstate(all="ignore"):
+                pin()
+        except Exception:
+            caught.append(pin.__name__)
+    assert caught, f"no pin detects the planted mistake {mutant.__name__}"
