@@ -1,0 +1,226 @@
+#!/usr/bin/env python3
+"""Throughput of the VDA forward pass on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--workload 768p_bf16] [--no-cpu-baseline]
+
+A step is one whole forward pass (frame statistics, inverse, both scans,
+readout + RMSNorm + gate) over the workload's synthetic inputs, which are
+resident in HBM before timing starts.  The timed region runs K steps through
+the library's stage entry points (the same kernels and launch configuration
+as vda_forward) with HIP events between the stages on the launch stream, so
+each kernel's average duration is measured live; vda_forward itself is timed
+in a second region as a cross-check.  Prints one JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import platform
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "VDA fwd tokens/s and TFLOP/s (% bf16 MFMA peak) on one MI355X, 768p-shaped"
+PEAK_BF16_TFLOPS = 2500.0   # dense bf16 MFMA, MI355X
+PEAK_HBM_GBS = 8000.0       # HBM3E, MI355X
+
+
+def flops_alg(w) -> float:
+    """FLOPs of the method per call: A_t (2 N d_k^2), B_t and the readout
+    (4 N d_k d_v), the SPD inverse (d_k^3) and two scan products (4 d_v d_k^2)
+    per frame and head."""
+    dk, dv, N = w.d_k, w.d_v, w.N
+    return w.frame_heads * (2 * N * dk * dk + 4 * N * dk * dv + dk ** 3 + 4 * dv * dk * dk)
+
+
+def bytes_alg(w) -> float:
+    """Bytes the operator must move: q, k, v, out (storage type), fp32 beta and gate."""
+    e = 4 if w.dtype == "f32" else 2
+    return w.heads * w.F * w.N * (e * (2 * w.d_k + w.d_v) + e * w.d_v + 4) + 4 * w.heads
+
+
+def kernel_bytes(w):
+    """Algorithmic bytes per launch of each kernel: what it must read and
+    write once (its inputs and its outputs), without split partials."""
+    e = 4 if w.dtype == "f32" else 2
+    fh, N, dk, dv = w.frame_heads, w.N, w.d_k, w.d_v
+    return {
+        "frame_stats": fh * (N * (e * (dk + dv) + 4) + 4 * (dk * dk + dv * dk)),
+        "frame_inverse": fh * 8 * dk * dk,
+        "state_scan": fh * 2 * (4 * dk * dk + 4 * dv * dk + 4 * dv * dk),
+        "readout": fh * (N * e * (dk + dv) + 8 * dv * dk) + 4 * w.heads,
+    }
+
+
+def cpu_baseline(w, budget_s: float = 20.0) -> dict:
+    """Time the fp64 oracle on whole heads of the same workload until about
+    budget_s of CPU work, and scale to the full job's tokens/s."""
+    import numpy as np
+
+    import oracle.vda_oracle as O
+    from paper_2609_20744_amd import inputs as I
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()
+                       if p.get("user_api") == "blas"] or [1])
+    except Exception:
+        threads = int(os.environ.get("OMP_NUM_THREADS", "1"))
+    spent, heads = 0.0, 0
+    for hb in range(w.heads):
+        x = I.make_inputs(w, heads=[hb])
+        f = {k: I.as_float64(x[k], w.dtype)[0] for k in ("q", "k", "v")}
+        b = x["beta"][0].astype(np.float64)
+        g = float(x["gate"][0])
+        t0 = time.perf_counter()
+        O.head_forward(f["q"], f["k"], f["v"], b, g)
+        spent += time.perf_counter() - t0
+        heads += 1
+        if spent >= budget_s:
+            break
+    per_head = spent / heads
+    value = w.tokens / (per_head * w.heads)
+    return {"value": value, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"{heads} of {w.heads} heads of the {w.name} workload (all {w.F} frames x "
+                      f"{w.N} tokens, fp64 NumPy oracle, {spent:.1f} s), scaled to all heads",
+            "host": platform.processor() or platform.machine(), "nproc": os.cpu_count()}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="768p_bf16")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=20.0)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (the operator is one GPU's head shard); "
+              f"--gpus {args.gpus} is not supported", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    from paper_2609_20744_amd import inputs as I
+    from paper_2609_20744_amd import vda
+
+    w = I.WORKLOADS[args.workload]
+    torch.cuda.set_device(0)
+    print(f"[bench] generating {w.name} inputs", file=sys.stderr, flush=True)
+    x = I.make_inputs(w)
+
+    def dev(a, dt):
+        if dt == "bf16":
+            return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+        return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+    q, k, v = dev(x["q"], w.dtype), dev(x["k"], w.dtype), dev(x["v"], w.dtype)
+    beta, gate = dev(x["beta"], "f32"), dev(x["gate"], "f32")
+    del x
+    H, F, N, dk, dv = w.heads, w.F, w.N, w.d_k, w.d_v
+    splits = vda.default_splits(F, N, H)
+    A_part = torch.empty((splits, H, F, dk, dk), dtype=torch.float32, device="cuda")
+    B_part = torch.empty((splits, H, F, dv, dk), dtype=torch.float32, device="cuda")
+    S_fwd = torch.empty((H, F, dv, dk), dtype=torch.float32, device="cuda")
+    S_rev = torch.empty((H, F, dv, dk), dtype=torch.float32, device="cuda")
+    out = torch.empty((H, F, N, dv), dtype=q.dtype, device="cuda")
+    Inv = A_part[0]
+
+    names = ["frame_stats", "frame_inverse", "state_scan", "readout"]
+
+    def step(evs=None):
+        vda.frame_stats(k, v, beta, splits=splits, A_part=A_part, B_part=B_part)
+        if evs is not None:
+            evs[1].record()
+        vda.frame_inverse(A_part, Inv=Inv)
+        if evs is not None:
+            evs[2].record()
+        vda.state_scan(Inv, B_part, S_fwd, S_rev)
+        if evs is not None:
+            evs[3].record()
+        vda.readout(q, S_fwd, S_rev, gate, out=out)
+        if evs is not None:
+            evs[4].record()
+
+    print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    K = args.steps
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(K)]
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    t_start.record()
+    for i in range(K):
+        evs[i][0].record()
+        step(evs[i])
+    t_end.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    total_ms = t_start.elapsed_time(t_end)
+    ms = total_ms / K
+    per_kernel = {n: sum(evs[i][j].elapsed_time(evs[i][j + 1]) for i in range(K)) / K
+                  for j, n in enumerate(names)}
+    print(f"[bench] timed {K} steps: {ms:.4f} ms/step", file=sys.stderr, flush=True)
+
+    # Cross-check: the all-in-one entry point over the same number of steps.
+    for _ in range(2):
+        vda.forward(q, k, v, beta, gate, out=out)
+    torch.cuda.synchronize()
+    f0 = torch.cuda.Event(enable_timing=True)
+    f1 = torch.cuda.Event(enable_timing=True)
+    f0.record()
+    for _ in range(K):
+        vda.forward(q, k, v, beta, gate, out=out)
+    f1.record()
+    torch.cuda.synchronize()
+    fused_ms = f0.elapsed_time(f1) / K
+
+    t = ms / 1e3
+    tflops = flops_alg(w) / t / 1e12
+    gbs = bytes_alg(w) / t / 1e9
+    kb = kernel_bytes(w)
+    dominant = max(("frame_stats", "readout"), key=lambda n: per_kernel[n])
+    ach = kb[dominant] / (per_kernel[dominant] / 1e3) / 1e9
+    result = {
+        "metric": METRIC,
+        "value": w.tokens / t,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if w.dtype == "bf16" else "f32",
+        "data": "synthetic (seeded; L2-normalised q,k; sigmoid write strengths and gates)",
+        "config": {"workload": w.name, "B": w.B, "H": w.H, "F": F, "N": N, "d_k": dk, "d_v": dv,
+                   "storage": w.dtype, "state": "fp32", "splits": splits},
+        "tflops": tflops,
+        "pct_bf16_mfma_peak": 100.0 * tflops / PEAK_BF16_TFLOPS,
+        "hbm_gbs_alg": gbs,
+        "pct_hbm_peak": 100.0 * gbs / PEAK_HBM_GBS,
+        "token_heads_per_s": w.tokens * w.H / t,
+        "kernel_ms": per_kernel,
+        "forward_entry_ms_per_step": fused_ms,
+        "wall_s_timed_region": wall,
+        "roofline": {"bound": "hbm", "kernel": dominant, "achieved": ach, "peak": PEAK_HBM_GBS,
+                     "unit": "GB/s", "frac": ach / PEAK_HBM_GBS, "traffic": None},
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
+        result["cpu_baseline"] = cpu_baseline(w, args.cpu_budget)
+    print(json.dumps(result), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,158 @@
+/*
+ * vda.h -- Video Delta Attention (VDA) forward pass on AMD Instinct MI355X (gfx950).
+ *
+ * VDA is the linear branch of Video DeltaNet (arXiv 2609.20744).  For every
+ * independent head problem h and every frame t (U = N tokens per frame) it
+ * forms the frame statistics (Eq. 3b)
+ *     A_t = K_t^T Diag(beta_t) K_t            (d_k x d_k)
+ *     B_t = V_t^T Diag(beta_t) K_t            (d_v x d_k)
+ * and updates a d_v x d_k state once per frame with the joint solve (Eq. 5,
+ * no decay, so Sbar_t = S_{t-1})
+ *     S_t = (S_{t-1} + B_t) (I + A_t)^{-1},
+ * scanned forward (P) and backward (R) over the frames from a zero state
+ * (Eq. A.1; Algorithm 1, step 5).  Frame t reads the states outside itself
+ * (Eq. A.4 with the local window reduced to the own frame, Eq. 1a)
+ *     o_{t,u} = (P_{t-1} + R_{t+1}) q_{t,u}
+ * and the branch epilogue (Eq. 1c) gives
+ *     y_{t,u} = gate_h * o_{t,u} / sqrt(mean_j o_{t,u,j}^2 + 1e-6).
+ * Frame 1 reads only R_2, frame F only P_{F-1}; a one-frame clip gives y = 0.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - All tensor pointers are DEVICE pointers owned by the caller; the library
+ *    never frees or retains them.  Tensors are dense, row-major, frame-major:
+ *        q, k      [H][F][N][d_k]
+ *        v, out    [H][F][N][d_v]
+ *        beta      [H][F][N]     fp32, per-token write strength, >= 0
+ *                                 (0 allowed; negative values are not checked
+ *                                 and give undefined results)
+ *        gate      [H]           fp32, per-head output gate (already squashed)
+ *    H counts independent head problems (batch folded in: H = B * heads).
+ *  - Supported head dimensions: d_k, d_v in {32, 64, 128}.  F, N, H >= 1.
+ *  - q, k, v, out and the fp32 work buffers must be 16-byte aligned; beta and
+ *    gate 4-byte aligned.  out must not overlap any input.
+ *  - Every call is asynchronous on `stream` (0 = the null stream): it
+ *    validates its arguments on the host, enqueues kernels and returns.  It
+ *    never synchronises.  Invalid arguments are reported before anything is
+ *    enqueued.  A device fault surfaces at the caller's next synchronisation.
+ *  - Calls keep no state between them except per-device cached properties
+ *    and the workspace memory pool; they may be issued concurrently from
+ *    several threads on different streams.
+ *  - Results are deterministic: no floating-point atomics are used.
+ *  - No C++ exception crosses this interface.
+ */
+#ifndef VDA_H
+#define VDA_H
+
+#include <stddef.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes returned by every entry point. */
+typedef enum {
+  VDA_OK = 0,
+  VDA_ERR_NULL = 1,        /* a required pointer is NULL                      */
+  VDA_ERR_SIZE = 2,        /* F, N, H or splits < 1, or sizes overflow limits */
+  VDA_ERR_UNSUPPORTED = 3, /* d_k or d_v not in {32, 64, 128}                 */
+  VDA_ERR_ALIGN = 4,       /* a pointer is not aligned as required            */
+  VDA_ERR_OVERLAP = 5,     /* the output overlaps an input                    */
+  VDA_ERR_HIP = 6,         /* the HIP runtime reported an error               */
+  VDA_ERR_NOMEM = 7        /* workspace allocation failed                     */
+} vda_status;
+
+/* Human-readable name of a status code (static storage; never NULL). */
+const char* vda_status_string(int status);
+
+/* ------------------------------------------------------------------------- */
+/* Whole operator                                                             */
+/* ------------------------------------------------------------------------- */
+
+/*
+ * vda_forward -- the whole forward pass (Eq. 3b, 5, A.1, A.4, 1a, 1c) with
+ * bf16 storage for q, k, v (inputs) and out (output, round-to-nearest-even).
+ * Frame statistics and the readout run on bf16 matrix cores with fp32
+ * accumulation; (I + A_t)^{-1}, the recurrent states and the epilogue are
+ * fp32.  Workspace (about H*F*(3*d_k*d_k + 4*d_v*d_k)*4 bytes) is taken from a
+ * library-owned stream-ordered memory pool and released on `stream`.
+ */
+int vda_forward(const void* q, const void* k, const void* v,
+                const float* beta, const float* gate,
+                int F, int N, int H, int d_k, int d_v,
+                void* out, hipStream_t stream);
+
+/*
+ * vda_forward_f32 -- identical semantics and arguments with fp32 storage for
+ * q, k, v and out; every product and sum is computed in fp32.
+ */
+int vda_forward_f32(const float* q, const float* k, const float* v,
+                    const float* beta, const float* gate,
+                    int F, int N, int H, int d_k, int d_v,
+                    float* out, hipStream_t stream);
+
+/* ------------------------------------------------------------------------- */
+/* Stage interface: the same kernels as vda_forward, one step per call, with  */
+/* caller-owned fp32 work buffers (all device pointers, 16-byte aligned).     */
+/* ------------------------------------------------------------------------- */
+
+/*
+ * vda_default_splits -- number of token ranges the frame-statistics step
+ * splits each frame into on the current device (>= 1).  Each range yields one
+ * partial A and B; the later steps add the partials in index order.
+ */
+int vda_default_splits(int F, int N, int H);
+
+/*
+ * vda_frame_stats -- step a1, Eq. 3b.  For split s covering tokens
+ * [s*T, min(N, (s+1)*T)) with T = 64 * ceil(ceil(N / splits) / 64):
+ *     A_part[s][h][t] = sum_u beta k k^T   (d_k x d_k, fp32)
+ *     B_part[s][h][t] = sum_u beta v k^T   (d_v x d_k, fp32)
+ * A_part is [splits][H][F][d_k][d_k], B_part is [splits][H][F][d_v][d_k].
+ * k, v are bf16 (is_f32 == 0) or fp32 (is_f32 != 0).  With bf16 storage the
+ * products beta * k are rounded to bf16 before the fp32-accumulated matrix
+ * product; with fp32 storage everything is fp32.  splits must not exceed
+ * ceil(N / 64).
+ */
+int vda_frame_stats(const void* k, const void* v, const float* beta,
+                    int F, int N, int H, int d_k, int d_v, int splits, int is_f32,
+                    float* A_part, float* B_part, hipStream_t stream);
+
+/*
+ * vda_frame_inverse -- step a2, Eq. 5: Inv[i] = (I + sum_s A_part[s][i])^{-1}
+ * for i < count, in fp32 by Gauss-Jordan elimination without pivoting
+ * (I + A is symmetric positive definite with eigenvalues >= 1 when beta >= 0).
+ * Inv is [count][d_k][d_k].  Inv may alias A_part (in-place when splits == 1,
+ * or onto the first partial); it must not overlap any other partial.
+ */
+int vda_frame_inverse(const float* A_part, int splits, int count, int d_k,
+                      float* Inv, hipStream_t stream);
+
+/*
+ * vda_state_scan -- steps a3 and a4, Eq. A.1 and Algorithm 1 step 5 with a
+ * zero initial state.  With B_t = sum_s B_part[s][h][t]:
+ *     forward  P_0 = 0,     P_t = (P_{t-1} + B_t) Inv_t,  S_fwd[h][t] = P_{t-1}
+ *     reverse  R_{F+1} = 0, R_t = (R_{t+1} + B_t) Inv_t,  S_rev[h][t] = R_{t+1}
+ * (frames numbered 1..F here; array index t-1).  S_fwd, S_rev are
+ * [H][F][d_v][d_k] fp32; Inv is [H][F][d_k][d_k].
+ */
+int vda_state_scan(const float* Inv, const float* B_part, int splits,
+                   int F, int H, int d_k, int d_v,
+                   float* S_fwd, float* S_rev, hipStream_t stream);
+
+/*
+ * vda_readout -- steps a5-a7, Eq. A.4 (own-frame window), Eq. 1a and Eq. 1c:
+ *     out[h][t][u] = gate[h] * RMSNorm((S_fwd[h][t] + S_rev[h][t]) q[h][t][u]).
+ * q and out are bf16 (is_f32 == 0; the summed state is rounded to bf16 for
+ * the fp32-accumulated matrix product) or fp32 (is_f32 != 0).
+ */
+int vda_readout(const void* q, const float* S_fwd, const float* S_rev,
+                const float* gate, int F, int N, int H, int d_k, int d_v,
+                int is_f32, void* out, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* VDA_H */

@@ -1,0 +1,267 @@
+// C ABI of the VDA library: argument validation, workspace, launch order.
+// Declarations and contracts are in include/vda.h.
+#include <stdint.h>
+#include <string.h>
+
+#include <mutex>
+
+#include "../../include/vda.h"
+#include "vda_common.h"
+#include "vda_launch.h"
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+
+bool supported_dim(int d) { return d == 32 || d == 64 || d == 128; }
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+struct Range {
+  uintptr_t lo, hi;  // [lo, hi)
+};
+
+Range range_of(const void* p, size_t bytes) {
+  const uintptr_t lo = reinterpret_cast<uintptr_t>(p);
+  return Range{lo, lo + bytes};
+}
+
+bool overlaps(Range a, Range b) { return a.lo < b.hi && b.lo < a.hi; }
+
+// Shape checks shared by every entry point.  Grids are one-dimensional with
+// one workgroup per (frame, head, split/chunk), so H*F*64 must fit 31 bits.
+int check_shape(int F, int N, int H, int d_k, int d_v) {
+  if (F < 1 || N < 1 || H < 1) return VDA_ERR_SIZE;
+  if (!supported_dim(d_k) || !supported_dim(d_v)) return VDA_ERR_UNSUPPORTED;
+  if ((long long)H * F * 64 > 0x7fffffffLL) return VDA_ERR_SIZE;
+  if ((long long)N > (1LL << 30)) return VDA_ERR_SIZE;
+  return VDA_OK;
+}
+
+int hip_status(hipError_t e) { return e == hipSuccess ? VDA_OK : VDA_ERR_HIP; }
+
+int current_device_cus() {
+  static int cus[kMaxDevices] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return 256;
+  if (cus[dev] == 0) {
+    int c = 0;
+    if (hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || c <= 0)
+      c = 256;
+    cus[dev] = c;
+  }
+  return cus[dev];
+}
+
+// Library-owned stream-ordered pool per device.  Freed blocks stay in the
+// pool (release threshold = max), so repeated calls do not remap memory.
+hipMemPool_t device_pool(int dev) {
+  static std::mutex mu;
+  static hipMemPool_t pools[kMaxDevices] = {nullptr};
+  if (dev < 0 || dev >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(mu);
+  if (pools[dev] == nullptr) {
+    hipMemPoolProps props;
+    memset(&props, 0, sizeof(props));
+    props.allocType = hipMemAllocationTypePinned;
+    props.handleTypes = hipMemHandleTypeNone;
+    props.location.type = hipMemLocationTypeDevice;
+    props.location.id = dev;
+    hipMemPool_t pool = nullptr;
+    if (hipMemPoolCreate(&pool, &props) != hipSuccess) return nullptr;
+    uint64_t threshold = UINT64_MAX;
+    (void)hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &threshold);
+    pools[dev] = pool;
+  }
+  return pools[dev];
+}
+
+int default_splits(int F, int N, int H) {
+  // Aim for about four statistics workgroups per compute unit, never fewer
+  // than 256 tokens per split.
+  const long long fh = (long long)H * F;
+  const long long target = 4LL * current_device_cus();
+  long long s = (target + fh - 1) / fh;
+  long long cap = N / 256;
+  if (cap < 1) cap = 1;
+  if (s > cap) s = cap;
+  if (s < 1) s = 1;
+  return (int)s;
+}
+
+struct Workspace {
+  size_t a_part, b_part, s_fwd, s_rev, total;  // byte offsets / total
+};
+
+Workspace workspace_layout(int F, int H, int d_k, int d_v, int splits) {
+  const size_t fh = (size_t)H * F;
+  const size_t a = (size_t)splits * fh * d_k * d_k * sizeof(float);
+  const size_t b = (size_t)splits * fh * d_v * d_k * sizeof(float);
+  const size_t s = fh * d_v * d_k * sizeof(float);
+  Workspace w;
+  w.a_part = 0;
+  w.b_part = a;
+  w.s_fwd = a + b;
+  w.s_rev = a + b + s;
+  w.total = a + b + 2 * s;
+  return w;
+}
+
+int forward_impl(bool is_f32, const void* q, const void* k, const void* v, const float* beta,
+                 const float* gate, int F, int N, int H, int d_k, int d_v, void* out,
+                 hipStream_t stream) {
+  if (!q || !k || !v || !beta || !gate || !out) return VDA_ERR_NULL;
+  int st = check_shape(F, N, H, d_k, d_v);
+  if (st != VDA_OK) return st;
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 16) ||
+      !aligned(beta, 4) || !aligned(gate, 4))
+    return VDA_ERR_ALIGN;
+  const size_t es = is_f32 ? 4 : 2;
+  const size_t tok = (size_t)H * F * N;
+  const Range ro = range_of(out, tok * d_v * es);
+  if (overlaps(ro, range_of(q, tok * d_k * es)) || overlaps(ro, range_of(k, tok * d_k * es)) ||
+      overlaps(ro, range_of(v, tok * d_v * es)) || overlaps(ro, range_of(beta, tok * 4)) ||
+      overlaps(ro, range_of(gate, (size_t)H * 4)))
+    return VDA_ERR_OVERLAP;
+
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return VDA_ERR_HIP;
+  hipMemPool_t pool = device_pool(dev);
+  if (!pool) return VDA_ERR_HIP;
+  const int splits = default_splits(F, N, H);
+  const Workspace w = workspace_layout(F, H, d_k, d_v, splits);
+  void* ws = nullptr;
+  if (hipMallocFromPoolAsync(&ws, w.total, pool, stream) != hipSuccess || !ws) return VDA_ERR_NOMEM;
+  char* base = static_cast<char*>(ws);
+  float* A_part = reinterpret_cast<float*>(base + w.a_part);
+  float* B_part = reinterpret_cast<float*>(base + w.b_part);
+  float* S_fwd = reinterpret_cast<float*>(base + w.s_fwd);
+  float* S_rev = reinterpret_cast<float*>(base + w.s_rev);
+  float* Inv = A_part;  // the inverse overwrites the first partial
+
+  hipError_t e = vda::launch_frame_stats(is_f32, k, v, beta, F, N, H, d_k, d_v, splits, A_part,
+                                         B_part, stream);
+  if (e == hipSuccess)
+    e = vda::launch_frame_inverse(A_part, splits, (long long)H * F, d_k, Inv, stream);
+  if (e == hipSuccess)
+    e = vda::launch_state_scan(Inv, B_part, splits, F, H, d_k, d_v, S_fwd, S_rev, stream);
+  if (e == hipSuccess)
+    e = vda::launch_readout(is_f32, q, S_fwd, S_rev, gate, F, N, H, d_k, d_v, out, stream);
+  const hipError_t ef = hipFreeAsync(ws, stream);
+  if (e != hipSuccess) return VDA_ERR_HIP;
+  return hip_status(ef);
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* vda_status_string(int status) {
+  switch (status) {
+    case VDA_OK: return "VDA_OK";
+    case VDA_ERR_NULL: return "VDA_ERR_NULL: a required pointer is NULL";
+    case VDA_ERR_SIZE: return "VDA_ERR_SIZE: a size is out of range";
+    case VDA_ERR_UNSUPPORTED: return "VDA_ERR_UNSUPPORTED: d_k and d_v must be 32, 64 or 128";
+    case VDA_ERR_ALIGN: return "VDA_ERR_ALIGN: a pointer is misaligned";
+    case VDA_ERR_OVERLAP: return "VDA_ERR_OVERLAP: the output overlaps an input";
+    case VDA_ERR_HIP: return "VDA_ERR_HIP: the HIP runtime reported an error";
+    case VDA_ERR_NOMEM: return "VDA_ERR_NOMEM: workspace allocation failed";
+    default: return "VDA: unknown status";
+  }
+}
+
+int vda_forward(const void* q, const void* k, const void* v, const float* beta, const float* gate,
+                int F, int N, int H, int d_k, int d_v, void* out, hipStream_t stream) {
+  return forward_impl(false, q, k, v, beta, gate, F, N, H, d_k, d_v, out, stream);
+}
+
+int vda_forward_f32(const float* q, const float* k, const float* v, const float* beta,
+                    const float* gate, int F, int N, int H, int d_k, int d_v, float* out,
+                    hipStream_t stream) {
+  return forward_impl(true, q, k, v, beta, gate, F, N, H, d_k, d_v, out, stream);
+}
+
+int vda_default_splits(int F, int N, int H) {
+  if (F < 1 || N < 1 || H < 1) return 1;
+  return default_splits(F, N, H);
+}
+
+int vda_frame_stats(const void* k, const void* v, const float* beta, int F, int N, int H,
+                    int d_k, int d_v, int splits, int is_f32, float* A_part, float* B_part,
+                    hipStream_t stream) {
+  if (!k || !v || !beta || !A_part || !B_part) return VDA_ERR_NULL;
+  int st = check_shape(F, N, H, d_k, d_v);
+  if (st != VDA_OK) return st;
+  if (splits < 1 || splits > (N + 63) / 64 || (long long)H * F * splits > 0x7fffffffLL)
+    return VDA_ERR_SIZE;
+  if (!aligned(k, 16) || !aligned(v, 16) || !aligned(beta, 4) || !aligned(A_part, 16) ||
+      !aligned(B_part, 16))
+    return VDA_ERR_ALIGN;
+  const size_t fh = (size_t)H * F;
+  const Range ra = range_of(A_part, (size_t)splits * fh * d_k * d_k * 4);
+  const Range rb = range_of(B_part, (size_t)splits * fh * d_v * d_k * 4);
+  const size_t es = is_f32 ? 4 : 2;
+  const Range rk = range_of(k, fh * N * d_k * es), rv = range_of(v, fh * N * d_v * es),
+              rbeta = range_of(beta, fh * N * 4);
+  if (overlaps(ra, rb) || overlaps(ra, rk) || overlaps(ra, rv) || overlaps(ra, rbeta) ||
+      overlaps(rb, rk) || overlaps(rb, rv) || overlaps(rb, rbeta))
+    return VDA_ERR_OVERLAP;
+  return hip_status(vda::launch_frame_stats(is_f32 != 0, k, v, beta, F, N, H, d_k, d_v, splits,
+                                            A_part, B_part, stream));
+}
+
+int vda_frame_inverse(const float* A_part, int splits, int count, int d_k, float* Inv,
+                      hipStream_t stream) {
+  if (!A_part || !Inv) return VDA_ERR_NULL;
+  if (splits < 1 || count < 1) return VDA_ERR_SIZE;
+  if (!supported_dim(d_k)) return VDA_ERR_UNSUPPORTED;
+  if (!aligned(A_part, 16) || !aligned(Inv, 16)) return VDA_ERR_ALIGN;
+  const size_t mat = (size_t)count * d_k * d_k * 4;
+  const Range ri = range_of(Inv, mat);
+  for (int s = 0; s < splits; ++s) {
+    const Range rs = range_of(reinterpret_cast<const char*>(A_part) + s * mat, mat);
+    const bool same = rs.lo == ri.lo;
+    if (overlaps(ri, rs) && !(same && s == 0)) return VDA_ERR_OVERLAP;
+  }
+  return hip_status(vda::launch_frame_inverse(A_part, splits, count, d_k, Inv, stream));
+}
+
+int vda_state_scan(const float* Inv, const float* B_part, int splits, int F, int H, int d_k,
+                   int d_v, float* S_fwd, float* S_rev, hipStream_t stream) {
+  if (!Inv || !B_part || !S_fwd || !S_rev) return VDA_ERR_NULL;
+  int st = check_shape(F, 1, H, d_k, d_v);
+  if (st != VDA_OK) return st;
+  if (splits < 1) return VDA_ERR_SIZE;
+  if (!aligned(Inv, 16) || !aligned(B_part, 16) || !aligned(S_fwd, 16) || !aligned(S_rev, 16))
+    return VDA_ERR_ALIGN;
+  const size_t fh = (size_t)H * F;
+  const Range rf = range_of(S_fwd, fh * d_v * d_k * 4), rr = range_of(S_rev, fh * d_v * d_k * 4);
+  const Range ri = range_of(Inv, fh * d_k * d_k * 4);
+  const Range rb = range_of(B_part, (size_t)splits * fh * d_v * d_k * 4);
+  if (overlaps(rf, rr) || overlaps(rf, ri) || overlaps(rf, rb) || overlaps(rr, ri) ||
+      overlaps(rr, rb))
+    return VDA_ERR_OVERLAP;
+  return hip_status(
+      vda::launch_state_scan(Inv, B_part, splits, F, H, d_k, d_v, S_fwd, S_rev, stream));
+}
+
+int vda_readout(const void* q, const float* S_fwd, const float* S_rev, const float* gate, int F,
+                int N, int H, int d_k, int d_v, int is_f32, void* out, hipStream_t stream) {
+  if (!q || !S_fwd || !S_rev || !gate || !out) return VDA_ERR_NULL;
+  int st = check_shape(F, N, H, d_k, d_v);
+  if (st != VDA_OK) return st;
+  if (!aligned(q, 16) || !aligned(S_fwd, 16) || !aligned(S_rev, 16) || !aligned(gate, 4) ||
+      !aligned(out, 16))
+    return VDA_ERR_ALIGN;
+  const size_t es = is_f32 ? 4 : 2;
+  const size_t fh = (size_t)H * F;
+  const Range ro = range_of(out, fh * N * d_v * es);
+  if (overlaps(ro, range_of(q, fh * N * d_k * es)) ||
+      overlaps(ro, range_of(S_fwd, fh * d_v * d_k * 4)) ||
+      overlaps(ro, range_of(S_rev, fh * d_v * d_k * 4)) || overlaps(ro, range_of(gate, H * 4)))
+    return VDA_ERR_OVERLAP;
+  return hip_status(vda::launch_readout(is_f32 != 0, q, S_fwd, S_rev, gate, F, N, H, d_k, d_v,
+                                        out, stream));
+}
+
+}  // extern "C"

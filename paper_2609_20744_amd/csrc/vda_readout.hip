@@ -1,0 +1,213 @@
+// Steps a5-a7: gather, readout, RMSNorm and gate.
+//   S~_t = P_{t-1} + R_{t+1}            (Eq. A.4 with the window [t, t], alpha = 1)
+//   o_{t,u} = S~_t q_{t,u}               (Eq. 1a)
+//   y_{t,u} = gate * o / sqrt(mean(o^2) + eps)   (Eq. 1c)
+//
+// bf16 path: a workgroup owns one frame of one head and a range of its
+// tokens.  It sums the two fp32 states, rounds S~ to bf16 once into LDS, and
+// each wavefront keeps all of S~ as MFMA A-operands in registers.  It then
+// streams 16-token groups: the group's queries are the B-operand (16-byte
+// loads straight from HBM, prefetched one group ahead), O^T = S~ Q^T is
+// accumulated in fp32 by v_mfma_f32_16x16x32_bf16, and the RMSNorm over the
+// d_v outputs of a token is a lane-local sum plus two cross-lane exchanges.
+// The normalised, gated values are rounded to bf16 and stored.
+#include "vda_common.h"
+#include "vda_launch.h"
+
+namespace vda {
+namespace {
+
+template <int DK, int DV>
+__global__ __launch_bounds__(kThreads, 2)
+void readout_bf16_kernel(const uint16_t* __restrict__ Q, const float* __restrict__ S_fwd,
+                         const float* __restrict__ S_rev, const float* __restrict__ gate,
+                         int F, int N, int chunks, int tokens_per_chunk,
+                         uint16_t* __restrict__ out) {
+  constexpr int SLD = DK + 8;  // bf16 row stride of S~ in LDS
+  constexpr int MB = DV / 16;  // 16-row blocks of S~ (output channels)
+  constexpr int KB = DK / 32;  // 32-wide k steps
+  __shared__ __align__(16) uint16_t st[DV * SLD];
+
+  const unsigned fh = blockIdx.x / chunks;
+  const int chunk = blockIdx.x % chunks;
+  const int n_begin = chunk * tokens_per_chunk;
+  const int n_end = min(N, n_begin + tokens_per_chunk);
+  const float g = gate[fh / F];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int li = lane & 15;
+  const int lg = lane >> 4;
+
+  {
+    const float* sf = S_fwd + (size_t)fh * (DV * DK);
+    const float* sr = S_rev + (size_t)fh * (DV * DK);
+    for (int idx = tid * 4; idx < DV * DK; idx += kThreads * 4) {
+      const float4 a = *reinterpret_cast<const float4*>(sf + idx);
+      const float4 b = *reinterpret_cast<const float4*>(sr + idx);
+      const int i = idx / DK, j = idx % DK;
+      *reinterpret_cast<uint2*>(&st[i * SLD + j]) =
+          make_uint2(pack_bf16x2(a.x + b.x, a.y + b.y), pack_bf16x2(a.z + b.z, a.w + b.w));
+    }
+  }
+  __syncthreads();
+
+  bf16x8 sop[MB][KB];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb)
+      sop[mb][kb] = *reinterpret_cast<const bf16x8*>(&st[(mb * 16 + li) * SLD + kb * 32 + lg * 8]);
+
+  const uint16_t* qbase = Q + (size_t)fh * N * DK;
+  uint16_t* obase = out + (size_t)fh * N * DV;
+
+  uint4 qc[KB], qn[KB];
+  auto load_q = [&](int n0, uint4 (&qv)[KB]) {
+    const int row = n0 + li;
+    const bool ok = row < n_end;
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb)
+      qv[kb] = ok ? *reinterpret_cast<const uint4*>(qbase + (size_t)row * DK + kb * 32 + lg * 8)
+                  : make_uint4(0, 0, 0, 0);
+  };
+
+  int n0 = n_begin + wave * 16;
+  if (n0 < n_end) load_q(n0, qc);
+  for (; n0 < n_end; n0 += 64) {
+    if (n0 + 64 < n_end) load_q(n0 + 64, qn);
+    floatx4 acc[MB];
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) acc[mb] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) {
+      const bf16x8 qop = __builtin_bit_cast(bf16x8, qc[kb]);
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb)
+        acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sop[mb][kb], qop, acc[mb], 0, 0, 0);
+    }
+    // lane holds o[token n0 + li][mb*16 + 4*lg + i]
+    float ss = 0.f;
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) ss = fmaf(acc[mb][i], acc[mb][i], ss);
+    ss += __shfl_xor(ss, 16);
+    ss += __shfl_xor(ss, 32);
+    const float scale = g / sqrtf(ss * (1.0f / DV) + kRmsEps);
+    const int row = n0 + li;
+    if (row < n_end) {
+      uint16_t* dst = obase + (size_t)row * DV + lg * 4;
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb)
+        *reinterpret_cast<uint2*>(dst + mb * 16) =
+            make_uint2(pack_bf16x2(acc[mb][0] * scale, acc[mb][1] * scale),
+                       pack_bf16x2(acc[mb][2] * scale, acc[mb][3] * scale));
+    }
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) qc[kb] = qn[kb];
+  }
+}
+
+// fp32 storage: fp32 products and sums.  16 threads per token, each owning
+// d_v/16 output channels; S~ in LDS (fp32), queries staged per 16 tokens.
+template <int DK, int DV>
+__global__ __launch_bounds__(kThreads)
+void readout_f32_kernel(const float* __restrict__ Q, const float* __restrict__ S_fwd,
+                        const float* __restrict__ S_rev, const float* __restrict__ gate,
+                        int F, int N, int chunks, int tokens_per_chunk, float* __restrict__ out) {
+  constexpr int SLD = DK + 1;
+  constexpr int VPT = DV / 16;  // output channels per thread
+  __shared__ float st[DV * SLD];
+  __shared__ float qs[16][DK];
+
+  const unsigned fh = blockIdx.x / chunks;
+  const int chunk = blockIdx.x % chunks;
+  const int n_begin = chunk * tokens_per_chunk;
+  const int n_end = min(N, n_begin + tokens_per_chunk);
+  const float g = gate[fh / F];
+  const int tid = threadIdx.x;
+
+  const float* sf = S_fwd + (size_t)fh * (DV * DK);
+  const float* sr = S_rev + (size_t)fh * (DV * DK);
+  for (int idx = tid; idx < DV * DK; idx += kThreads)
+    st[(idx / DK) * SLD + idx % DK] = sf[idx] + sr[idx];
+
+  const int tok = tid >> 4;  // token within the group of 16
+  const int part = tid & 15;
+  for (int n0 = n_begin; n0 < n_end; n0 += 16) {
+    __syncthreads();
+    for (int idx = tid; idx < 16 * DK; idx += kThreads) {
+      const int e = idx / DK, c = idx % DK;
+      const int n = n0 + e;
+      qs[e][c] = n < n_end ? Q[((size_t)fh * N + n) * DK + c] : 0.f;
+    }
+    __syncthreads();
+    float o[VPT];
+#pragma unroll
+    for (int m = 0; m < VPT; ++m) o[m] = 0.f;
+    for (int c = 0; c < DK; ++c) {
+      const float qv = qs[tok][c];
+#pragma unroll
+      for (int m = 0; m < VPT; ++m) o[m] = fmaf(st[(part + 16 * m) * SLD + c], qv, o[m]);
+    }
+    float ss = 0.f;
+#pragma unroll
+    for (int m = 0; m < VPT; ++m) ss = fmaf(o[m], o[m], ss);
+#pragma unroll
+    for (int off = 1; off < 16; off <<= 1) ss += __shfl_xor(ss, off);
+    const float scale = g / sqrtf(ss * (1.0f / DV) + kRmsEps);
+    const int n = n0 + tok;
+    if (n < n_end) {
+#pragma unroll
+      for (int m = 0; m < VPT; ++m) out[((size_t)fh * N + n) * DV + part + 16 * m] = o[m] * scale;
+    }
+  }
+}
+
+inline int readout_chunks(long long fh_count, int N) {
+  // Enough workgroups to cover the chip a few times, each with >= 512 tokens.
+  const long long target = 2048;
+  long long c = (target + fh_count - 1) / fh_count;
+  const long long cap = (N + 511) / 512;
+  if (c > cap) c = cap;
+  return c < 1 ? 1 : (int)c;
+}
+
+template <int DK, int DV>
+hipError_t launch_readout_t(bool is_f32, const void* q, const float* S_fwd, const float* S_rev,
+                            const float* gate, int F, int N, int H, void* out,
+                            hipStream_t stream) {
+  const long long fh_count = (long long)H * F;
+  const int chunks = readout_chunks(fh_count, N);
+  int tpc = (N + chunks - 1) / chunks;
+  tpc = ((tpc + 63) / 64) * 64;
+  const dim3 grid((unsigned)(fh_count * chunks));
+  if (is_f32)
+    hipLaunchKernelGGL((readout_f32_kernel<DK, DV>), grid, dim3(kThreads), 0, stream,
+                       static_cast<const float*>(q), S_fwd, S_rev, gate, F, N, chunks, tpc,
+                       static_cast<float*>(out));
+  else
+    hipLaunchKernelGGL((readout_bf16_kernel<DK, DV>), grid, dim3(kThreads), 0, stream,
+                       static_cast<const uint16_t*>(q), S_fwd, S_rev, gate, F, N, chunks, tpc,
+                       static_cast<uint16_t*>(out));
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_readout(bool is_f32, const void* q, const float* S_fwd, const float* S_rev,
+                          const float* gate, int F, int N, int H, int d_k, int d_v, void* out,
+                          hipStream_t stream) {
+#define VDA_READOUT_CASE(DKV, DVV) \
+  if (d_k == DKV && d_v == DVV)    \
+    return launch_readout_t<DKV, DVV>(is_f32, q, S_fwd, S_rev, gate, F, N, H, out, stream);
+  VDA_READOUT_CASE(32, 32) VDA_READOUT_CASE(32, 64) VDA_READOUT_CASE(32, 128)
+  VDA_READOUT_CASE(64, 32) VDA_READOUT_CASE(64, 64) VDA_READOUT_CASE(64, 128)
+  VDA_READOUT_CASE(128, 32) VDA_READOUT_CASE(128, 64) VDA_READOUT_CASE(128, 128)
+#undef VDA_READOUT_CASE
+  return hipErrorInvalidValue;
+}
+
+}  // namespace vda

@@ -1,0 +1,236 @@
+"""Thin Python binding of libvda.so (the C ABI in include/vda.h).
+
+Argument marshalling only: every step of the operator runs in the HIP
+kernels of libvda.so.  PyTorch supplies device memory and the stream.
+Importing this module raises ImportError if the library is not built.
+
+Tensor layout (batch and heads folded into one leading axis, or kept as any
+number of leading axes, which are flattened):
+    q, k  [..., F, N, d_k]   v, out [..., F, N, d_v]
+    beta  [..., F, N] fp32   gate   [...] fp32
+q, k, v, out are torch.bfloat16 (vda_forward) or torch.float32
+(vda_forward_f32), contiguous, on one GPU.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+import re
+
+# torch is imported before libvda.so is loaded: torch bundles its own HIP
+# runtime (soname libamdhip64.so.7), and loading it first makes libvda.so's
+# dependency resolve to that same runtime, so torch's streams and memory are
+# valid in the library's calls.  Loading libvda.so first would bring in a
+# second runtime instance whose streams are unrelated to torch's.
+import torch  # noqa: F401  (load order matters, see above)
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libvda.so")
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "vda.h")
+
+VDA_OK = 0
+STATUS_NAMES = {0: "VDA_OK", 1: "VDA_ERR_NULL", 2: "VDA_ERR_SIZE", 3: "VDA_ERR_UNSUPPORTED",
+                4: "VDA_ERR_ALIGN", 5: "VDA_ERR_OVERLAP", 6: "VDA_ERR_HIP", 7: "VDA_ERR_NOMEM"}
+
+_P = ctypes.c_void_p
+_I = ctypes.c_int
+
+_SIGNATURES = {
+    "vda_status_string": (ctypes.c_char_p, [_I]),
+    "vda_forward": (_I, [_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _P, _P]),
+    "vda_forward_f32": (_I, [_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _P, _P]),
+    "vda_default_splits": (_I, [_I, _I, _I]),
+    "vda_frame_stats": (_I, [_P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _P, _P, _P]),
+    "vda_frame_inverse": (_I, [_P, _I, _I, _I, _P, _P]),
+    "vda_state_scan": (_I, [_P, _P, _I, _I, _I, _I, _I, _P, _P, _P]),
+    "vda_readout": (_I, [_P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _P, _P]),
+}
+
+
+def _load() -> ctypes.CDLL:
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(
+            f"{LIB_PATH} is not built; run `python -m paper_2609_20744_amd.build` "
+            "(the VDA operator has no fallback path)")
+    lib = ctypes.CDLL(LIB_PATH)
+    for name, (res, args) in _SIGNATURES.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    return lib
+
+
+lib = _load()
+
+
+class VDAError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {status_string(status)}")
+
+
+def status_string(status: int) -> str:
+    return lib.vda_status_string(int(status)).decode()
+
+
+def header_functions() -> list[str]:
+    """Names of the entry points declared in include/vda.h."""
+    with open(HEADER) as f:
+        text = f.read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\*?\s+\*?(vda_\w+)\s*\(", text, flags=re.M)))
+
+
+def _check(status: int, where: str) -> None:
+    if status != VDA_OK:
+        if status == 1:
+            raise ValueError(f"{where}: {status_string(status)}")
+        if status in (2, 3, 4, 5):
+            raise ValueError(f"{where}: {status_string(status)}")
+        raise VDAError(status, where)
+
+
+# ----------------------------------------------------------------------------
+# torch-facing wrappers
+# ----------------------------------------------------------------------------
+
+def _torch():
+    import torch
+    return torch
+
+
+def _stream_ptr(device, stream=None) -> int:
+    torch = _torch()
+    s = stream if stream is not None else torch.cuda.current_stream(device)
+    return int(s.cuda_stream)
+
+
+def _require(t, name, dtype, device):
+    torch = _torch()
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device != device:
+        raise ValueError(f"{name} is on {t.device}, expected {device}")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} has dtype {t.dtype}, expected {dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def _shape(q, k, v, beta, gate=None):
+    if q.dim() < 3:
+        raise ValueError("q must be [..., F, N, d_k]")
+    lead = tuple(q.shape[:-3])
+    F, N, d_k = q.shape[-3:]
+    d_v = v.shape[-1]
+    H = math.prod(lead) if lead else 1
+    if tuple(k.shape) != tuple(q.shape):
+        raise ValueError(f"k shape {tuple(k.shape)} != q shape {tuple(q.shape)}")
+    if tuple(v.shape) != lead + (F, N, d_v):
+        raise ValueError(f"v shape {tuple(v.shape)} does not match q")
+    if tuple(beta.shape) != lead + (F, N):
+        raise ValueError(f"beta shape {tuple(beta.shape)} must be {lead + (F, N)}")
+    if gate is not None and gate.numel() != H:
+        raise ValueError(f"gate must have {H} elements (one per head problem)")
+    return lead, F, N, H, d_k, d_v
+
+
+def forward(q, k, v, beta, gate, out=None, stream=None):
+    """VDA forward (vda_forward for bf16 tensors, vda_forward_f32 for fp32)."""
+    torch = _torch()
+    dt = q.dtype
+    if dt not in (torch.bfloat16, torch.float32):
+        raise ValueError(f"q dtype {dt} must be bfloat16 or float32")
+    dev = q.device
+    if dev.type != "cuda":
+        raise ValueError("VDA runs on the GPU only; tensors must be on a cuda device")
+    for t, n in ((q, "q"), (k, "k"), (v, "v")):
+        _require(t, n, dt, dev)
+    _require(beta, "beta", torch.float32, dev)
+    _require(gate, "gate", torch.float32, dev)
+    lead, F, N, H, d_k, d_v = _shape(q, k, v, beta, gate)
+    if out is None:
+        out = torch.empty(lead + (F, N, d_v), dtype=dt, device=dev)
+    else:
+        _require(out, "out", dt, dev)
+        if tuple(out.shape) != lead + (F, N, d_v):
+            raise ValueError(f"out shape {tuple(out.shape)} must be {lead + (F, N, d_v)}")
+    fn = lib.vda_forward if dt == torch.bfloat16 else lib.vda_forward_f32
+    with torch.cuda.device(dev):
+        st = fn(q.data_ptr(), k.data_ptr(), v.data_ptr(), beta.data_ptr(), gate.data_ptr(),
+                F, N, H, d_k, d_v, out.data_ptr(), _stream_ptr(dev, stream))
+    _check(st, fn.__name__)
+    return out
+
+
+def default_splits(F: int, N: int, H: int) -> int:
+    return int(lib.vda_default_splits(F, N, H))
+
+
+def frame_stats(k, v, beta, splits=None, A_part=None, B_part=None, stream=None):
+    """Step a1 (vda_frame_stats): partial A, B per token split, fp32."""
+    torch = _torch()
+    dev, dt = k.device, k.dtype
+    for t, n in ((k, "k"), (v, "v")):
+        _require(t, n, dt, dev)
+    _require(beta, "beta", torch.float32, dev)
+    lead, F, N, H, d_k, d_v = _shape(k, k, v, beta)
+    splits = default_splits(F, N, H) if splits is None else int(splits)
+    if A_part is None:
+        A_part = torch.empty((splits, H, F, d_k, d_k), dtype=torch.float32, device=dev)
+    if B_part is None:
+        B_part = torch.empty((splits, H, F, d_v, d_k), dtype=torch.float32, device=dev)
+    with torch.cuda.device(dev):
+        st = lib.vda_frame_stats(k.data_ptr(), v.data_ptr(), beta.data_ptr(), F, N, H, d_k, d_v,
+                                 splits, int(dt == torch.float32), A_part.data_ptr(),
+                                 B_part.data_ptr(), _stream_ptr(dev, stream))
+    _check(st, "vda_frame_stats")
+    return A_part, B_part
+
+
+def frame_inverse(A_part, Inv=None, stream=None):
+    """Step a2 (vda_frame_inverse): (I + sum of partials)^-1, fp32.
+    A_part is [splits, count..., d_k, d_k]."""
+    torch = _torch()
+    splits = A_part.shape[0]
+    d_k = A_part.shape[-1]
+    count = math.prod(A_part.shape[1:-2])
+    if Inv is None:
+        Inv = torch.empty(A_part.shape[1:], dtype=torch.float32, device=A_part.device)
+    with torch.cuda.device(A_part.device):
+        st = lib.vda_frame_inverse(A_part.data_ptr(), splits, count, d_k, Inv.data_ptr(),
+                                   _stream_ptr(A_part.device, stream))
+    _check(st, "vda_frame_inverse")
+    return Inv
+
+
+def state_scan(Inv, B_part, S_fwd=None, S_rev=None, stream=None):
+    """Steps a3/a4 (vda_state_scan).  Inv [H, F, d_k, d_k], B_part [splits, H, F, d_v, d_k]."""
+    torch = _torch()
+    splits, H, F, d_v, d_k = B_part.shape
+    dev = B_part.device
+    if S_fwd is None:
+        S_fwd = torch.empty((H, F, d_v, d_k), dtype=torch.float32, device=dev)
+    if S_rev is None:
+        S_rev = torch.empty((H, F, d_v, d_k), dtype=torch.float32, device=dev)
+    with torch.cuda.device(dev):
+        st = lib.vda_state_scan(Inv.data_ptr(), B_part.data_ptr(), splits, F, H, d_k, d_v,
+                                S_fwd.data_ptr(), S_rev.data_ptr(), _stream_ptr(dev, stream))
+    _check(st, "vda_state_scan")
+    return S_fwd, S_rev
+
+
+def readout(q, S_fwd, S_rev, gate, d_v=None, out=None, stream=None):
+    """Steps a5-a7 (vda_readout).  q [H, F, N, d_k], S_* [H, F, d_v, d_k], gate [H]."""
+    torch = _torch()
+    H, F, N, d_k = q.shape
+    d_v = S_fwd.shape[-2] if d_v is None else d_v
+    dev = q.device
+    if out is None:
+        out = torch.empty((H, F, N, d_v), dtype=q.dtype, device=dev)
+    with torch.cuda.device(dev):
+        st = lib.vda_readout(q.data_ptr(), S_fwd.data_ptr(), S_rev.data_ptr(), gate.data_ptr(),
+                             F, N, H, d_k, d_v, int(q.dtype == torch.float32), out.data_ptr(),
+                             _stream_ptr(dev, stream))
+    _check(st, "vda_readout")
+    return out

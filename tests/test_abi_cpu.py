@@ -1,0 +1,84 @@
+"""Host-side checks of the C ABI (no GPU): the library loads, exports every
+entry point that include/vda.h declares, and rejects invalid arguments
+before anything is enqueued (these calls never reach the HIP runtime)."""
+import ctypes
+
+import pytest
+
+vda = pytest.importorskip("paper_2609_20744_amd.vda", reason="libvda.so not built")
+
+P = 0x10000  # a 64 KiB-aligned fake device address; validation never dereferences it
+
+
+def test_exports_every_declared_symbol():
+    names = vda.header_functions()
+    assert set(names) >= {"vda_forward", "vda_forward_f32", "vda_status_string", "vda_frame_stats",
+                          "vda_frame_inverse", "vda_state_scan", "vda_readout",
+                          "vda_default_splits"}
+    for n in names:
+        assert hasattr(vda.lib, n), n
+    assert set(names) == set(vda._SIGNATURES)
+
+
+def test_status_strings():
+    for code, name in vda.STATUS_NAMES.items():
+        assert vda.status_string(code).startswith(name)
+    assert "unknown" in vda.status_string(99)
+
+
+def _fwd(**kw):
+    a = dict(q=P, k=P * 2, v=P * 3, beta=P * 4, gate=P * 5, F=4, N=64, H=2, d_k=64, d_v=64,
+             out=P * 16, stream=None)
+    a.update(kw)
+    return vda.lib.vda_forward(a["q"], a["k"], a["v"], a["beta"], a["gate"], a["F"], a["N"],
+                               a["H"], a["d_k"], a["d_v"], a["out"], a["stream"])
+
+
+def test_forward_validation():
+    # distinct far-apart fake buffers: out = 16 * 64 KiB, inputs below it
+    big = 1 << 32
+    ok = dict(q=big, k=2 * big, v=3 * big, beta=4 * big, gate=5 * big, out=6 * big)
+    assert _fwd(q=None, **{k: v for k, v in ok.items() if k != "q"}) == 1
+    assert _fwd(**{**ok, "out": None}) == 1
+    assert _fwd(**ok, F=0) == 2
+    assert _fwd(**ok, N=0) == 2
+    assert _fwd(**ok, H=-1) == 2
+    assert _fwd(**ok, d_k=48) == 3
+    assert _fwd(**ok, d_v=256) == 3
+    assert _fwd(**ok, d_k=16) == 3
+    assert _fwd(**{**ok, "q": big + 8}) == 4
+    assert _fwd(**{**ok, "beta": 4 * big + 2}) == 4
+    # out overlapping v
+    assert _fwd(**{**ok, "out": 3 * big + 64}) == 5
+    # out overlapping beta
+    assert _fwd(**{**ok, "out": 4 * big - 16}) == 5
+    # H * F too large for the launch grid
+    assert _fwd(**ok, H=1 << 20, F=1 << 10) == 2
+
+
+def test_stage_validation():
+    big = 1 << 32
+    L = vda.lib
+    assert L.vda_frame_stats(None, big, 2 * big, 4, 64, 2, 64, 64, 1, 0, 3 * big, 4 * big, None) == 1
+    assert L.vda_frame_stats(big, 2 * big, 3 * big, 4, 64, 2, 64, 64, 0, 0, 4 * big, 5 * big, None) == 2
+    assert L.vda_frame_stats(big, 2 * big, 3 * big, 4, 64, 2, 64, 64, 2, 0, 4 * big, 5 * big, None) == 2
+    assert L.vda_frame_stats(big, 2 * big, 3 * big, 4, 64, 2, 64, 64, 1, 0, 4 * big + 4, 5 * big, None) == 4
+    assert L.vda_frame_stats(big, 2 * big, 3 * big, 4, 64, 2, 64, 64, 1, 0, big, 5 * big, None) == 5
+    assert L.vda_frame_inverse(None, 1, 8, 64, big, None) == 1
+    assert L.vda_frame_inverse(big, 1, 8, 96, 2 * big, None) == 3
+    assert L.vda_frame_inverse(big, 0, 8, 64, 2 * big, None) == 2
+    # in place onto the first partial is allowed (would launch), onto the second is not
+    assert L.vda_frame_inverse(big, 2, 8, 64, big + 8 * 64 * 64 * 4, None) == 5
+    assert L.vda_state_scan(big, 2 * big, 1, 4, 2, 64, 64, 3 * big, 3 * big, None) == 5
+    assert L.vda_state_scan(big, 2 * big, 1, 4, 2, 64, 48, 3 * big, 4 * big, None) == 3
+    assert L.vda_readout(big, 2 * big, 3 * big, 4 * big, 4, 64, 2, 64, 64, 0, big, None) == 5
+    assert L.vda_readout(big, 2 * big, 3 * big, None, 4, 64, 2, 64, 64, 0, 5 * big, None) == 1
+
+
+def test_single_hip_runtime_loaded():
+    """The binding and torch must share one HIP runtime instance, or torch's
+    streams would be unknown to the library."""
+    import os
+    maps = open(f"/proc/{os.getpid()}/maps").read()
+    libs = {l.split()[-1] for l in maps.splitlines() if "libamdhip64" in l}
+    assert len(libs) == 1, libs

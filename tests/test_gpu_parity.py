@@ -1,0 +1,306 @@
+"""GPU parity of the HIP path against the fp64 oracle, through the C ABI.
+
+Stage tests feed oracle-computed inputs into one kernel and compare with the
+oracle's result for that step; whole-operator tests run vda_forward on the
+seeded workloads and compare element by element (small sizes) or at sampled
+positions (full sizes, in the launch configuration the benchmark times).
+The bar: rel. max-norm error <= 1e-4 (fp32 storage) and <= 2e-2 (bf16
+storage, fp32 state).
+"""
+import numpy as np
+import pytest
+
+import oracle.vda_oracle as O
+from paper_2609_20744_amd import inputs as I
+from vda_testutil import (TOL_BF16, TOL_F32, device_inputs, from_device, oracle_inputs,
+                          oracle_sampled, rel_max_err, sample_positions, to_device, tol_for)
+
+pytestmark = pytest.mark.gpu
+
+DIMS = [(32, 32), (32, 64), (32, 128), (64, 32), (64, 64), (64, 128), (128, 32), (128, 64),
+        (128, 128)]
+
+
+@pytest.fixture(scope="module")
+def V():
+    import torch
+    assert torch.cuda.is_available(), "the gpu tests need an MI355X"
+    from paper_2609_20744_amd import vda
+    return vda
+
+
+def _log(msg):
+    print(msg, flush=True)
+
+
+def _forward(V, w, x):
+    import torch
+    d = device_inputs(w, x)
+    y = V.forward(d["q"], d["k"], d["v"], d["beta"], d["gate"])
+    torch.cuda.synchronize()
+    return y
+
+
+# ----------------------------------------------------------------------------
+# Stage parity (oracle-fed)
+# ----------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("dk,dv", DIMS)
+def test_stats_stage(V, dtype, dk, dv):
+    import torch
+    w = I.custom("stats", 1, 2, 3, 200, dk, dv, dtype, seed=11)
+    x = I.make_inputs(w)
+    xo = oracle_inputs(w, x)
+    d = device_inputs(w, x)
+    for splits in (1, 3):
+        _log(f"stats dtype={dtype} dk={dk} dv={dv} splits={splits}")
+        A_part, B_part = V.frame_stats(d["k"], d["v"], d["beta"], splits=splits)
+        torch.cuda.synchronize()
+        A = A_part.double().sum(0).cpu().numpy()
+        B = B_part.double().sum(0).cpu().numpy()
+        for h in range(2):
+            As, Bs = O.head_statistics(xo["k"][h], xo["v"][h], xo["beta"][h])
+            tol = 1e-5 if dtype == "f32" else 1e-2
+            assert rel_max_err(A[h], As) < tol
+            assert rel_max_err(B[h], Bs) < tol
+
+
+@pytest.mark.parametrize("dk", [32, 64, 128])
+def test_inverse_stage(V, dk):
+    import torch
+    rng = np.random.default_rng(dk)
+    count, U = 6, 3 * dk
+    K = rng.standard_normal((count, U, dk))
+    K /= np.linalg.norm(K, axis=-1, keepdims=True)
+    beta = rng.random((count, U))
+    beta[0] = 0.0                        # A = 0: inverse is the identity
+    beta[1] *= 10.0                      # stronger writes, larger condition number
+    A = np.stack([O.frame_statistics(K[i], K[i][:, :1], beta[i])[0] for i in range(count)])
+    expect = np.stack([O.frame_transition(A[i], np.zeros((1, dk)))[0] for i in range(count)])
+    for splits in (1, 2):
+        _log(f"inverse dk={dk} splits={splits}")
+        parts = np.stack([A / splits] * splits).astype(np.float32)
+        A_dev = to_device(parts, "f32")
+        Inv = V.frame_inverse(A_dev)
+        torch.cuda.synchronize()
+        got = Inv.double().cpu().numpy()
+        np.testing.assert_array_equal(got[0], np.eye(dk))
+        for i in range(count):
+            cond = np.linalg.cond(np.eye(dk) + A[i])
+            assert rel_max_err(got[i], expect[i]) < 2e-6 * cond, (i, cond)
+    # in place onto the partial buffer
+    A_dev = to_device(A[None].astype(np.float32), "f32")
+    V.frame_inverse(A_dev, Inv=A_dev[0])
+    torch.cuda.synchronize()
+    assert rel_max_err(A_dev[0].double().cpu().numpy()[3], expect[3]) < 1e-4
+
+
+@pytest.mark.parametrize("dk,dv", DIMS)
+def test_scan_stage(V, dk, dv):
+    import torch
+    _log(f"scan dk={dk} dv={dv}")
+    w = I.custom("scan", 1, 3, 7, 40, dk, dv, "f32", seed=21)
+    x = I.make_inputs(w)
+    xo = oracle_inputs(w, x)
+    Inv = np.empty((3, 7, dk, dk))
+    Bm = np.empty((3, 7, dv, dk))
+    P_exp = np.empty((3, 7, dv, dk))
+    R_exp = np.empty((3, 7, dv, dk))
+    for h in range(3):
+        As, Bs = O.head_statistics(xo["k"][h], xo["v"][h], xo["beta"][h])
+        for t in range(7):
+            Inv[h, t] = np.linalg.inv(np.eye(dk) + As[t])
+        Bm[h] = Bs
+        P = O.forward_states(As, Bs)
+        R = O.reverse_states(As, Bs)
+        for t in range(1, 8):
+            P_exp[h, t - 1] = P[t - 1]
+            R_exp[h, t - 1] = R[t + 1]
+    for splits in (1, 2):
+        Bp = np.stack([Bm / splits] * splits)
+        Sf, Sr = V.state_scan(to_device(Inv.astype(np.float32), "f32"),
+                              to_device(Bp.astype(np.float32), "f32"))
+        torch.cuda.synchronize()
+        assert rel_max_err(Sf.double().cpu().numpy(), P_exp) < 1e-5
+        assert rel_max_err(Sr.double().cpu().numpy(), R_exp) < 1e-5
+        assert np.all(Sf[:, 0].cpu().numpy() == 0) and np.all(Sr[:, -1].cpu().numpy() == 0)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("dk,dv", DIMS)
+def test_readout_stage(V, dtype, dk, dv):
+    import torch
+    _log(f"readout dtype={dtype} dk={dk} dv={dv}")
+    w = I.custom("readout", 1, 2, 3, 77, dk, dv, dtype, seed=31)
+    x = I.make_inputs(w)
+    xo = oracle_inputs(w, x)
+    rng = np.random.default_rng(5)
+    Sf = rng.standard_normal((2, 3, dv, dk)) * 0.3
+    Sr = rng.standard_normal((2, 3, dv, dk)) * 0.3
+    y = V.readout(to_device(x["q"], dtype), to_device(Sf.astype(np.float32), "f32"),
+                  to_device(Sr.astype(np.float32), "f32"), to_device(x["gate"], "f32"))
+    torch.cuda.synchronize()
+    got = from_device(y)
+    Sf32 = Sf.astype(np.float32).astype(np.float64)
+    Sr32 = Sr.astype(np.float32).astype(np.float64)
+    exp = np.empty_like(got)
+    for h in range(2):
+        for t in range(3):
+            o = O.readout(Sf32[h, t] + Sr32[h, t], xo["q"][h, t])
+            exp[h, t] = O.rmsnorm_gate(o, xo["gate"][h])
+    tol = 1e-5 if dtype == "f32" else 1e-2
+    assert rel_max_err(got, exp) < tol
+
+
+# ----------------------------------------------------------------------------
+# Whole operator on the five workloads
+# ----------------------------------------------------------------------------
+
+@pytest.mark.parametrize("name", ["tiny_f32", "small_bf16"])
+def test_forward_full_oracle(V, name):
+    w = I.WORKLOADS[name]
+    _log(f"forward {name} (every output against the oracle)")
+    x = I.make_inputs(w)
+    got = from_device(_forward(V, w, x))
+    xo = oracle_inputs(w, x)
+    exp = O.vda_forward(xo["q"], xo["k"], xo["v"], xo["beta"], xo["gate"])
+    err = rel_max_err(got, exp)
+    _log(f"  rel max-norm error {err:.3e}")
+    assert err <= tol_for(w)
+
+
+@pytest.mark.parametrize("name", ["480p_bf16", "768p_bf16", "ragged_bf16"])
+def test_forward_full_size_sampled(V, name):
+    """Full-size workloads in the benchmark's launch configuration; the oracle
+    evaluates every frame of two heads at sampled tokens."""
+    w = I.WORKLOADS[name]
+    _log(f"forward {name} (sampled outputs against the oracle)")
+    x = I.make_inputs(w)
+    y = _forward(V, w, x)
+    rng = np.random.default_rng(w.seed)
+    heads = [0, w.heads - 1]
+    xs = I.make_inputs(w, heads=heads)
+    xo = oracle_inputs(w, xs)
+    ys = []
+    refs = []
+    for i, h in enumerate(heads):
+        toks = sample_positions(w, rng, 24)
+        ref, frames, tk = oracle_sampled(w, xo, i, toks)
+        got = from_device(y[h][frames, tk])
+        ys.append(got)
+        refs.append(ref)
+    err = rel_max_err(np.concatenate(ys), np.concatenate(refs))
+    _log(f"  rel max-norm error {err:.3e}")
+    assert err <= TOL_BF16
+    assert np.isfinite(from_device(y)).all()
+
+
+# ----------------------------------------------------------------------------
+# Edge cases
+# ----------------------------------------------------------------------------
+
+def _check_small(V, w, x=None):
+    x = I.make_inputs(w) if x is None else x
+    got = from_device(_forward(V, w, x))
+    xo = oracle_inputs(w, x)
+    exp = O.vda_forward(xo["q"], xo["k"], xo["v"], xo["beta"], xo["gate"])
+    err = rel_max_err(got, exp)
+    assert err <= tol_for(w), err
+    return got, exp
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("dk,dv", DIMS)
+def test_head_dims(V, dtype, dk, dv):
+    _log(f"dims dtype={dtype} dk={dk} dv={dv}")
+    _check_small(V, I.custom("dims", 2, 1, 5, 150, dk, dv, dtype, seed=dk + dv))
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("N", [1, 2, 15, 16, 17, 63, 64, 65, 129, 300])
+def test_ragged_tokens(V, dtype, N):
+    _log(f"ragged N={N} dtype={dtype}")
+    _check_small(V, I.custom("ragged", 1, 2, 4, N, 64, 128, dtype, seed=N))
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_single_frame_is_zero(V, dtype):
+    w = I.custom("f1", 1, 3, 1, 100, 64, 64, dtype, seed=3)
+    got, _ = _check_small(V, w)
+    assert np.all(got == 0.0)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_zero_writes(V, dtype):
+    w = I.custom("zero", 1, 2, 5, 70, 64, 64, dtype, seed=4)
+    x = I.make_inputs(w)
+    x["beta"][:] = 0.0
+    got, _ = _check_small(V, w, x)
+    assert np.all(got == 0.0)
+    x = I.make_inputs(w)
+    x["beta"][:, [0, 1, 3, 4]] = 0.0     # only frame 3 (index 2) writes
+    got, _ = _check_small(V, w, x)
+    assert np.all(got[:, 2] == 0.0)
+    assert np.all(np.abs(got[:, [0, 1, 3, 4]]).max(axis=-1) > 0)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_duplicate_and_strong_writes(V, dtype):
+    w = I.custom("dup", 1, 2, 6, 90, 64, 64, dtype, seed=9, dup_frac=0.3, beta_sigma=3.0,
+                 beta_zero_frac=0.2)
+    x = I.make_inputs(w)
+    x["k"][:, :, 10:20] = x["k"][:, :, 5:6]   # exact duplicates
+    x["beta"][:, :, 10:20] = 1.0
+    _check_small(V, w, x)
+
+
+def test_deterministic_and_guarded(V):
+    import torch
+    w = I.custom("det", 1, 4, 6, 333, 128, 128, "bf16", seed=12)
+    x = I.make_inputs(w)
+    d = device_inputs(w, x)
+    pad = 4096
+    buf = torch.full((2 * pad + w.heads * w.F * w.N * w.d_v,), -7, dtype=torch.int16, device="cuda")
+    out = buf[pad:pad + w.heads * w.F * w.N * w.d_v].view(torch.bfloat16).view(w.heads, w.F, w.N, w.d_v)
+    V.forward(d["q"], d["k"], d["v"], d["beta"], d["gate"], out=out)
+    y1 = V.forward(d["q"], d["k"], d["v"], d["beta"], d["gate"])
+    torch.cuda.synchronize()
+    assert torch.equal(out.view(torch.int16), y1.view(torch.int16))
+    assert torch.all(buf[:pad] == -7) and torch.all(buf[-pad:] == -7)
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        y2 = V.forward(d["q"], d["k"], d["v"], d["beta"], d["gate"])
+    s.synchronize()
+    assert torch.equal(y1.view(torch.int16), y2.view(torch.int16))
+
+
+def test_stages_compose_to_forward(V):
+    import torch
+    w = I.custom("compose", 1, 3, 5, 700, 128, 128, "bf16", seed=13)
+    x = I.make_inputs(w)
+    d = device_inputs(w, x)
+    y = V.forward(d["q"], d["k"], d["v"], d["beta"], d["gate"])
+    A_part, B_part = V.frame_stats(d["k"], d["v"], d["beta"])
+    Inv = V.frame_inverse(A_part, Inv=A_part[0])
+    Sf, Sr = V.state_scan(Inv, B_part)
+    y2 = V.readout(d["q"], Sf, Sr, d["gate"])
+    torch.cuda.synchronize()
+    assert torch.equal(y.view(torch.int16), y2.view(torch.int16))
+
+
+def test_invalid_arguments_raise(V):
+    import torch
+    w = I.custom("bad", 1, 2, 3, 64, 64, 64, "bf16", seed=1)
+    d = device_inputs(w, I.make_inputs(w))
+    with pytest.raises(ValueError):
+        V.forward(d["q"], d["k"], d["v"], d["beta"][..., :10].contiguous(), d["gate"])
+    q48 = torch.zeros((2, 3, 64, 48), dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(ValueError, match="UNSUPPORTED"):
+        V.forward(q48, q48, d["v"], d["beta"], d["gate"])
+    flat = torch.zeros(2 * 3 * 64 * 64 + 1, dtype=torch.bfloat16, device="cuda")
+    q_mis = flat[1:].view(2, 3, 64, 64)
+    with pytest.raises(ValueError, match="ALIGN"):
+        V.forward(q_mis, d["k"], d["v"], d["beta"], d["gate"])
+    with pytest.raises(ValueError, match="OVERLAP"):
+        V.forward(d["q"], d["k"], d["v"], d["beta"], d["gate"], out=d["v"])

@@ -1,0 +1,72 @@
+"""Helpers shared by the GPU parity tests: host <-> device transfer of the
+seeded inputs, the error metric, and oracle evaluation at sampled positions."""
+from __future__ import annotations
+
+import numpy as np
+
+import oracle.vda_oracle as O
+from paper_2609_20744_amd import inputs as I
+
+# Rel. max-norm tolerances of the parity bar: fp32 storage path, bf16 storage path.
+TOL_F32 = 1e-4
+TOL_BF16 = 2e-2
+
+
+def tol_for(w) -> float:
+    return TOL_F32 if w.dtype == "f32" else TOL_BF16
+
+
+def to_device(x: np.ndarray, dtype: str):
+    import torch
+    if dtype == "bf16":
+        return torch.from_numpy(np.ascontiguousarray(x).view(np.int16)).view(torch.bfloat16).cuda()
+    return torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).cuda()
+
+
+def from_device(t) -> np.ndarray:
+    """Device tensor -> float64 numpy array of the exact stored values."""
+    import torch
+    if t.dtype == torch.bfloat16:
+        return I.bf16_bits_to_f32(t.view(torch.int16).cpu().numpy().view(np.uint16)).astype(np.float64)
+    return t.double().cpu().numpy()
+
+
+def device_inputs(w, x: dict) -> dict:
+    return {"q": to_device(x["q"], w.dtype), "k": to_device(x["k"], w.dtype),
+            "v": to_device(x["v"], w.dtype), "beta": to_device(x["beta"], "f32"),
+            "gate": to_device(x["gate"], "f32")}
+
+
+def oracle_inputs(w, x: dict) -> dict:
+    return {"q": I.as_float64(x["q"], w.dtype), "k": I.as_float64(x["k"], w.dtype),
+            "v": I.as_float64(x["v"], w.dtype), "beta": x["beta"].astype(np.float64),
+            "gate": x["gate"].astype(np.float64)}
+
+
+def rel_max_err(y: np.ndarray, ref: np.ndarray) -> float:
+    """||y - ref||_inf / ||ref||_inf (0 when both are zero)."""
+    den = float(np.max(np.abs(ref))) if ref.size else 0.0
+    num = float(np.max(np.abs(y - ref))) if ref.size else 0.0
+    if den == 0.0:
+        return num
+    return num / den
+
+
+def sample_positions(w, rng, per_frame: int):
+    """Token indices per frame: the first, the last, the last full 16-token
+    group boundary and random ones."""
+    N = w.N
+    base = {0, N - 1, max(0, (N // 16) * 16 - 1), min(N - 1, (N // 16) * 16)}
+    extra = rng.choice(N, size=min(N, per_frame), replace=False)
+    toks = sorted(base | set(int(t) for t in extra))
+    return toks
+
+
+def oracle_sampled(w, xo: dict, h_local: int, toks) -> tuple[np.ndarray, np.ndarray, np.ndarray]:
+    """Oracle outputs of head ``h_local`` (index into xo) at every frame x toks."""
+    F = w.F
+    frames = np.repeat(np.arange(F), len(toks))
+    tk = np.tile(np.asarray(toks), F)
+    y = O.head_forward_sampled(xo["q"][h_local], xo["k"][h_local], xo["v"][h_local],
+                               xo["beta"][h_local], float(xo["gate"][h_local]), frames, tk)
+    return y, frames, tk
