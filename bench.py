@@ -96,6 +96,9 @@ def main() -> int:
     ap.add_argument("--workload", default="768p_bf16")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
+    ap.add_argument("--calibrate-copy", type=float, default=0.0, metavar="GIB",
+                    help="instead of the operator, run a plain elementwise copy (torch.neg) "
+                         "reading and writing GIB GiB, to calibrate HBM byte counters")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (the operator is one GPU's head shard); "
@@ -108,8 +111,26 @@ def main() -> int:
     from paper_2609_20744_amd import inputs as I
     from paper_2609_20744_amd import vda
 
-    w = I.WORKLOADS[args.workload]
     torch.cuda.set_device(0)
+    if args.calibrate_copy > 0:
+        n = int(args.calibrate_copy * (1 << 30)) // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(args.warmup):
+            torch.neg(src, out=dst)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(args.steps):
+            torch.neg(src, out=dst)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / args.steps
+        print(json.dumps({"calibration": "torch.neg fp32 copy", "bytes_read": 4 * n,
+                          "bytes_written": 4 * n, "ms": ms,
+                          "gbs_read_plus_write": 8 * n / ms / 1e6}), flush=True)
+        return 0
+    w = I.WORKLOADS[args.workload]
     print(f"[bench] generating {w.name} inputs", file=sys.stderr, flush=True)
     x = I.make_inputs(w)
 
