@@ -157,10 +157,10 @@ def main() -> int:
         vda.frame_stats(k, v, beta, splits=splits, A_part=A_part, B_part=B_part)
         if evs is not None:
             evs[1].record()
-        vda.frame_inverse(A_part, Inv=Inv)
+        vda.frame_inverse(A_part, B_part, Inv=Inv)
         if evs is not None:
             evs[2].record()
-        vda.state_scan(Inv, B_part, S_fwd, S_rev)
+        vda.state_scan(Inv, B_part[0], S_fwd, S_rev, exact_f32=(w.dtype == "f32"))
         if evs is not None:
             evs[3].record()
         vda.readout(q, S_fwd, S_rev, gate, out=out)

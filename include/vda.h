@@ -75,7 +75,8 @@ const char* vda_status_string(int status);
  * bf16 storage for q, k, v (inputs) and out (output, round-to-nearest-even).
  * Frame statistics and the readout run on bf16 matrix cores with fp32
  * accumulation; (I + A_t)^{-1}, the recurrent states and the epilogue are
- * fp32.  Workspace (about H*F*(3*d_k*d_k + 4*d_v*d_k)*4 bytes) is taken from a
+ * fp32, and the state products use split-bf16 operands (see vda_state_scan).
+ * Workspace (about H*F*(3*d_k*d_k + 4*d_v*d_k)*4 bytes) is taken from a
  * library-owned stream-ordered memory pool and released on `stream`.
  */
 int vda_forward(const void* q, const void* k, const void* v,
@@ -121,24 +122,33 @@ int vda_frame_stats(const void* k, const void* v, const float* beta,
 
 /*
  * vda_frame_inverse -- step a2, Eq. 5: Inv[i] = (I + sum_s A_part[s][i])^{-1}
- * for i < count, in fp32 by Gauss-Jordan elimination without pivoting
- * (I + A is symmetric positive definite with eigenvalues >= 1 when beta >= 0).
- * Inv is [count][d_k][d_k].  Inv may alias A_part (in-place when splits == 1,
- * or onto the first partial); it must not overlap any other partial.
+ * for i < count, in fp32 by blocked Gauss-Jordan elimination without
+ * pivoting (I + A is symmetric positive definite with eigenvalues >= 1 when
+ * beta >= 0).  Inv is [count][d_k][d_k].  Inv may alias A_part (in-place when
+ * splits == 1, or onto the first partial); it must not overlap any other
+ * partial.  When splits > 1 the call also folds the split partials of B in
+ * place: B_part[0][i] = sum_s B_part[s][i] (B_part is [splits][count][d_v][d_k];
+ * d_v and B_part are ignored when splits == 1), so the state scan reads one B.
  */
-int vda_frame_inverse(const float* A_part, int splits, int count, int d_k,
-                      float* Inv, hipStream_t stream);
+int vda_frame_inverse(const float* A_part, float* B_part, int splits, int count,
+                      int d_k, int d_v, float* Inv, hipStream_t stream);
 
 /*
  * vda_state_scan -- steps a3 and a4, Eq. A.1 and Algorithm 1 step 5 with a
- * zero initial state.  With B_t = sum_s B_part[s][h][t]:
+ * zero initial state.  With B_t = B[h][t] ([H][F][d_v][d_k] fp32, the reduced
+ * frame statistic; after vda_frame_inverse it is B_part[0]):
  *     forward  P_0 = 0,     P_t = (P_{t-1} + B_t) Inv_t,  S_fwd[h][t] = P_{t-1}
  *     reverse  R_{F+1} = 0, R_t = (R_{t+1} + B_t) Inv_t,  S_rev[h][t] = R_{t+1}
  * (frames numbered 1..F here; array index t-1).  S_fwd, S_rev are
- * [H][F][d_v][d_k] fp32; Inv is [H][F][d_k][d_k].
+ * [H][F][d_v][d_k] fp32; Inv is [H][F][d_k][d_k] and must be symmetric (as
+ * (I + A_t)^{-1} is): element Inv[k][j] is read from Inv[j][k].
+ * The state is fp32.  is_f32 != 0: fp32 matrix products.  is_f32 == 0 (the
+ * bf16 storage path): each product operand is split into two bf16 parts
+ * (hi + lo) and three bf16 matrix products are accumulated in fp32, about
+ * 16 mantissa bits per operand.
  */
-int vda_state_scan(const float* Inv, const float* B_part, int splits,
-                   int F, int H, int d_k, int d_v,
+int vda_state_scan(const float* Inv, const float* B,
+                   int F, int H, int d_k, int d_v, int is_f32,
                    float* S_fwd, float* S_rev, hipStream_t stream);
 
 /*

@@ -34,7 +34,8 @@ int check_shape(int F, int N, int H, int d_k, int d_v) {
   if (F < 1 || N < 1 || H < 1) return VDA_ERR_SIZE;
   if (!supported_dim(d_k) || !supported_dim(d_v)) return VDA_ERR_UNSUPPORTED;
   if ((long long)H * F * 64 > 0x7fffffffLL) return VDA_ERR_SIZE;
-  if ((long long)N > (1LL << 30)) return VDA_ERR_SIZE;
+  // Byte offsets within one frame of one head are 32-bit.
+  if ((long long)N * (d_k > d_v ? d_k : d_v) * 4 > 0x7fffffffLL) return VDA_ERR_SIZE;
   return VDA_OK;
 }
 
@@ -77,11 +78,13 @@ hipMemPool_t device_pool(int dev) {
 }
 
 int default_splits(int F, int N, int H) {
-  // Aim for about four statistics workgroups per compute unit, never fewer
-  // than 256 tokens per split.
-  const long long fh = (long long)H * F;
-  const long long target = 4LL * current_device_cus();
-  long long s = (target + fh - 1) / fh;
+  // The statistics step runs two workgroups (row halves) per frame and split;
+  // split the tokens only when that leaves fewer than about three workgroups
+  // per compute unit, and never below 256 tokens per split.  Splits cost a
+  // partial sum per split and a fold in the inverse step.
+  const long long wg_per_split = 2LL * H * F;
+  const long long target = 3LL * current_device_cus();
+  long long s = (target + wg_per_split - 1) / wg_per_split;
   long long cap = N / 256;
   if (cap < 1) cap = 1;
   if (s > cap) s = cap;
@@ -142,9 +145,9 @@ int forward_impl(bool is_f32, const void* q, const void* k, const void* v, const
   hipError_t e = vda::launch_frame_stats(is_f32, k, v, beta, F, N, H, d_k, d_v, splits, A_part,
                                          B_part, stream);
   if (e == hipSuccess)
-    e = vda::launch_frame_inverse(A_part, splits, (long long)H * F, d_k, Inv, stream);
+    e = vda::launch_frame_inverse(A_part, B_part, splits, (long long)H * F, d_k, d_v, Inv, stream);
   if (e == hipSuccess)
-    e = vda::launch_state_scan(Inv, B_part, splits, F, H, d_k, d_v, S_fwd, S_rev, stream);
+    e = vda::launch_state_scan(is_f32, Inv, B_part, F, H, d_k, d_v, S_fwd, S_rev, stream);
   if (e == hipSuccess)
     e = vda::launch_readout(is_f32, q, S_fwd, S_rev, gate, F, N, H, d_k, d_v, out, stream);
   const hipError_t ef = hipFreeAsync(ws, stream);
@@ -210,12 +213,12 @@ int vda_frame_stats(const void* k, const void* v, const float* beta, int F, int 
                                             A_part, B_part, stream));
 }
 
-int vda_frame_inverse(const float* A_part, int splits, int count, int d_k, float* Inv,
-                      hipStream_t stream) {
-  if (!A_part || !Inv) return VDA_ERR_NULL;
-  if (splits < 1 || count < 1) return VDA_ERR_SIZE;
-  if (!supported_dim(d_k)) return VDA_ERR_UNSUPPORTED;
-  if (!aligned(A_part, 16) || !aligned(Inv, 16)) return VDA_ERR_ALIGN;
+int vda_frame_inverse(const float* A_part, float* B_part, int splits, int count, int d_k,
+                      int d_v, float* Inv, hipStream_t stream) {
+  if (!A_part || !Inv || (splits > 1 && !B_part)) return VDA_ERR_NULL;
+  if (splits < 1 || count < 1 || (long long)count * 64 > 0x7fffffffLL) return VDA_ERR_SIZE;
+  if (!supported_dim(d_k) || (splits > 1 && !supported_dim(d_v))) return VDA_ERR_UNSUPPORTED;
+  if (!aligned(A_part, 16) || !aligned(Inv, 16) || !aligned(B_part, 16)) return VDA_ERR_ALIGN;
   const size_t mat = (size_t)count * d_k * d_k * 4;
   const Range ri = range_of(Inv, mat);
   for (int s = 0; s < splits; ++s) {
@@ -223,26 +226,31 @@ int vda_frame_inverse(const float* A_part, int splits, int count, int d_k, float
     const bool same = rs.lo == ri.lo;
     if (overlaps(ri, rs) && !(same && s == 0)) return VDA_ERR_OVERLAP;
   }
-  return hip_status(vda::launch_frame_inverse(A_part, splits, count, d_k, Inv, stream));
+  if (splits > 1) {
+    const size_t bmat = (size_t)count * d_v * d_k * 4;
+    const Range rb = range_of(B_part, splits * bmat);
+    if (overlaps(rb, ri) || overlaps(rb, range_of(A_part, splits * mat))) return VDA_ERR_OVERLAP;
+  }
+  return hip_status(
+      vda::launch_frame_inverse(A_part, B_part, splits, count, d_k, d_v, Inv, stream));
 }
 
-int vda_state_scan(const float* Inv, const float* B_part, int splits, int F, int H, int d_k,
-                   int d_v, float* S_fwd, float* S_rev, hipStream_t stream) {
-  if (!Inv || !B_part || !S_fwd || !S_rev) return VDA_ERR_NULL;
+int vda_state_scan(const float* Inv, const float* B, int F, int H, int d_k, int d_v, int is_f32,
+                   float* S_fwd, float* S_rev, hipStream_t stream) {
+  if (!Inv || !B || !S_fwd || !S_rev) return VDA_ERR_NULL;
   int st = check_shape(F, 1, H, d_k, d_v);
   if (st != VDA_OK) return st;
-  if (splits < 1) return VDA_ERR_SIZE;
-  if (!aligned(Inv, 16) || !aligned(B_part, 16) || !aligned(S_fwd, 16) || !aligned(S_rev, 16))
+  if (!aligned(Inv, 16) || !aligned(B, 16) || !aligned(S_fwd, 16) || !aligned(S_rev, 16))
     return VDA_ERR_ALIGN;
   const size_t fh = (size_t)H * F;
   const Range rf = range_of(S_fwd, fh * d_v * d_k * 4), rr = range_of(S_rev, fh * d_v * d_k * 4);
   const Range ri = range_of(Inv, fh * d_k * d_k * 4);
-  const Range rb = range_of(B_part, (size_t)splits * fh * d_v * d_k * 4);
+  const Range rb = range_of(B, fh * d_v * d_k * 4);
   if (overlaps(rf, rr) || overlaps(rf, ri) || overlaps(rf, rb) || overlaps(rr, ri) ||
       overlaps(rr, rb))
     return VDA_ERR_OVERLAP;
   return hip_status(
-      vda::launch_state_scan(Inv, B_part, splits, F, H, d_k, d_v, S_fwd, S_rev, stream));
+      vda::launch_state_scan(is_f32 != 0, Inv, B, F, H, d_k, d_v, S_fwd, S_rev, stream));
 }
 
 int vda_readout(const void* q, const float* S_fwd, const float* S_rev, const float* gate, int F,

@@ -34,6 +34,47 @@ __device__ __forceinline__ uint32_t perm_b32(uint32_t hi, uint32_t lo, uint32_t 
   return __builtin_amdgcn_perm(hi, lo, sel);
 }
 
+// Buffer resource over [base, base + bytes): buffer loads outside the range
+// return zero and buffer stores outside it are dropped, with no branch, so
+// the compiler can keep counting outstanding memory operations precisely.
+// The last word is the gfx9-family raw-buffer configuration.
+// The base and size must be workgroup-uniform; they are passed through
+// readfirstlane so the descriptor lives in scalar registers even when the
+// address arithmetic ran on the vector ALU.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  const uint64_t b = reinterpret_cast<uint64_t>(base);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)b);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(b >> 32));
+  void* p = reinterpret_cast<void*>(((uint64_t)hi << 32) | lo);
+  return __builtin_amdgcn_make_buffer_rsrc(p, (short)0, (int)__builtin_amdgcn_readfirstlane(bytes),
+                                           0x00020000);
+}
+
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+// Any offset at or past this is outside every buffer range used here.
+constexpr uint32_t kOutOfRange = 0xfffffff0u;
+
+__device__ __forceinline__ uint4 load_b128(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
+  const u32x4 v = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)byte_off, 0, 0));
+  return make_uint4(v[0], v[1], v[2], v[3]);
+}
+
+__device__ __forceinline__ float load_f32(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, (int)byte_off, 0, 0));
+}
+
+__device__ __forceinline__ void store_b64(__amdgpu_buffer_rsrc_t r, uint32_t byte_off, uint2 v) {
+  __builtin_amdgcn_raw_buffer_store_b64(u32x2{v.x, v.y}, r, (int)byte_off, 0, 0);
+}
+
+// Workgroup-uniform integer kept in a scalar register.  Integer division by
+// a runtime value is expanded on the vector ALU; without this the compiler
+// may treat values derived from it (such as buffer descriptors) as varying
+// per lane.
+__device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
+
 // Map a linear workgroup id onto a logical id so that consecutive logical
 // ids land on the same XCD.  Workgroups are dispatched round-robin over the
 // 8 XCDs (id % 8), each with its own L2; grouping logically adjacent work

@@ -10,14 +10,15 @@ hipError_t launch_frame_stats(bool is_f32, const void* k, const void* v, const f
                               int F, int N, int H, int d_k, int d_v, int splits,
                               float* A_part, float* B_part, hipStream_t stream);
 
-// Step a2, Eq. 5: Inv = (I + sum of A partials)^{-1}.
-hipError_t launch_frame_inverse(const float* A_part, int splits, long long count, int d_k,
-                                float* Inv, hipStream_t stream);
+// Step a2, Eq. 5: Inv = (I + sum of A partials)^{-1}; also folds the B
+// partials into B_part[0].
+hipError_t launch_frame_inverse(const float* A_part, float* B_part, int splits, long long count,
+                                int d_k, int d_v, float* Inv, hipStream_t stream);
 
-// Steps a3/a4, Eq. A.1: forward and reverse state scans.
-hipError_t launch_state_scan(const float* Inv, const float* B_part, int splits,
-                             int F, int H, int d_k, int d_v,
-                             float* S_fwd, float* S_rev, hipStream_t stream);
+// Steps a3/a4, Eq. A.1: forward and reverse state scans (exact fp32 products,
+// or split-bf16 products with fp32 accumulation).
+hipError_t launch_state_scan(bool exact_f32, const float* Inv, const float* Bm, int F, int H,
+                             int d_k, int d_v, float* S_fwd, float* S_rev, hipStream_t stream);
 
 // Steps a5-a7, Eq. A.4 / 1a / 1c: gather, readout, RMSNorm and gate.
 hipError_t launch_readout(bool is_f32, const void* q, const float* S_fwd, const float* S_rev,

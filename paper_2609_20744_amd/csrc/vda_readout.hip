@@ -7,7 +7,7 @@
 // tokens.  It sums the two fp32 states, rounds S~ to bf16 once into LDS, and
 // each wavefront keeps all of S~ as MFMA A-operands in registers.  It then
 // streams 16-token groups: the group's queries are the B-operand (16-byte
-// loads straight from HBM, prefetched one group ahead), O^T = S~ Q^T is
+// loads straight from HBM, three groups in flight per wave), O^T = S~ Q^T is
 // accumulated in fp32 by v_mfma_f32_16x16x32_bf16, and the RMSNorm over the
 // d_v outputs of a token is a lane-local sum plus two cross-lane exchanges.
 // The normalised, gated values are rounded to bf16 and stored.
@@ -21,22 +21,24 @@ template <int DK, int DV>
 __global__ __launch_bounds__(kThreads, 2)
 void readout_bf16_kernel(const uint16_t* __restrict__ Q, const float* __restrict__ S_fwd,
                          const float* __restrict__ S_rev, const float* __restrict__ gate,
-                         int F, int N, int chunks, int tokens_per_chunk,
+                         int F, int N, int chunks, int tokens_per_chunk, unsigned nwg,
                          uint16_t* __restrict__ out) {
   constexpr int SLD = DK + 8;  // bf16 row stride of S~ in LDS
   constexpr int MB = DV / 16;  // 16-row blocks of S~ (output channels)
   constexpr int KB = DK / 32;  // 32-wide k steps
   __shared__ __align__(16) uint16_t st[DV * SLD];
 
-  const unsigned fh = blockIdx.x / chunks;
-  const int chunk = blockIdx.x % chunks;
+  // The chunks of one frame read the same two states: keep them on one XCD.
+  const unsigned L = xcd_grouped_id(blockIdx.x, nwg);
+  const unsigned fh = L / chunks;
+  const int chunk = L % chunks;
   const int n_begin = chunk * tokens_per_chunk;
   const int n_end = min(N, n_begin + tokens_per_chunk);
   const float g = gate[fh / F];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (scalar)
   const int li = lane & 15;
   const int lg = lane >> 4;
 
@@ -63,50 +65,63 @@ void readout_bf16_kernel(const uint16_t* __restrict__ Q, const float* __restrict
   const uint16_t* qbase = Q + (size_t)fh * N * DK;
   uint16_t* obase = out + (size_t)fh * N * DV;
 
-  uint4 qc[KB], qn[KB];
-  auto load_q = [&](int n0, uint4 (&qv)[KB]) {
-    const int row = n0 + li;
-    const bool ok = row < n_end;
+  // Each wave owns every fourth 16-token group; the queries of its next
+  // kQ groups are in flight in a register ring (slot d: group n0 + 64*d).
+  // Rows past the range are clamped onto its last row (always valid memory);
+  // their outputs are dropped by the range-checked stores, so loads and
+  // stores need no branches.
+  constexpr int kQ = 3;
+  uint4 qr[kQ][KB];
+  auto load_q = [&](int nq, uint4 (&qv)[KB]) {
+    const int row = min(nq + li, n_end - 1);
 #pragma unroll
     for (int kb = 0; kb < KB; ++kb)
-      qv[kb] = ok ? *reinterpret_cast<const uint4*>(qbase + (size_t)row * DK + kb * 32 + lg * 8)
-                  : make_uint4(0, 0, 0, 0);
+      qv[kb] = *reinterpret_cast<const uint4*>(qbase + (size_t)row * DK + kb * 32 + lg * 8);
   };
+  const __amdgpu_buffer_rsrc_t orsrc = make_rsrc(obase, (uint32_t)n_end * DV * 2u);
 
-  int n0 = n_begin + wave * 16;
-  if (n0 < n_end) load_q(n0, qc);
-  for (; n0 < n_end; n0 += 64) {
-    if (n0 + 64 < n_end) load_q(n0 + 64, qn);
-    floatx4 acc[MB];
+  const int n_first = n_begin + wave * 16;
+  if (n_first >= n_end) return;
+  // Issue the ring in slot order (the scheduler must not reorder it), so on
+  // loop entry slot 0 is the oldest load and waits stay partial.
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb) acc[mb] = floatx4{0.f, 0.f, 0.f, 0.f};
+  for (int d = 0; d < kQ; ++d) {
+    load_q(n_first + 64 * d, qr[d]);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  for (int n0 = n_first; n0 < n_end; n0 += 64 * kQ) {
 #pragma unroll
-    for (int kb = 0; kb < KB; ++kb) {
-      const bf16x8 qop = __builtin_bit_cast(bf16x8, qc[kb]);
+    for (int d = 0; d < kQ; ++d) {
+      // Groups past the range (at most kQ-1 per wave) run on clamped rows;
+      // their stores fall outside the buffer range and are dropped.
+      const int ng = n0 + 64 * d;
+      floatx4 acc[MB];
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) acc[mb] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) {
+        const bf16x8 qop = __builtin_bit_cast(bf16x8, qr[d][kb]);
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb)
+          acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sop[mb][kb], qop, acc[mb], 0, 0, 0);
+      }
+      load_q(ng + 64 * kQ, qr[d]);
+      // lane holds o[token ng + li][mb*16 + 4*lg + i]
+      float ss = 0.f;
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb)
-        acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sop[mb][kb], qop, acc[mb], 0, 0, 0);
-    }
-    // lane holds o[token n0 + li][mb*16 + 4*lg + i]
-    float ss = 0.f;
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) ss = fmaf(acc[mb][i], acc[mb][i], ss);
-    ss += __shfl_xor(ss, 16);
-    ss += __shfl_xor(ss, 32);
-    const float scale = g / sqrtf(ss * (1.0f / DV) + kRmsEps);
-    const int row = n0 + li;
-    if (row < n_end) {
-      uint16_t* dst = obase + (size_t)row * DV + lg * 4;
+        for (int i = 0; i < 4; ++i) ss = fmaf(acc[mb][i], acc[mb][i], ss);
+      ss += __shfl_xor(ss, 16);
+      ss += __shfl_xor(ss, 32);
+      const float scale = g / sqrtf(ss * (1.0f / DV) + kRmsEps);
+      const uint32_t off = ((uint32_t)(ng + li) * DV + lg * 4) * 2u;
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb)
-        *reinterpret_cast<uint2*>(dst + mb * 16) =
-            make_uint2(pack_bf16x2(acc[mb][0] * scale, acc[mb][1] * scale),
-                       pack_bf16x2(acc[mb][2] * scale, acc[mb][3] * scale));
+        store_b64(orsrc, off + mb * 32u,
+                  make_uint2(pack_bf16x2(acc[mb][0] * scale, acc[mb][1] * scale),
+                             pack_bf16x2(acc[mb][2] * scale, acc[mb][3] * scale)));
     }
-#pragma unroll
-    for (int kb = 0; kb < KB; ++kb) qc[kb] = qn[kb];
   }
 }
 
@@ -191,7 +206,7 @@ hipError_t launch_readout_t(bool is_f32, const void* q, const float* S_fwd, cons
   else
     hipLaunchKernelGGL((readout_bf16_kernel<DK, DV>), grid, dim3(kThreads), 0, stream,
                        static_cast<const uint16_t*>(q), S_fwd, S_rev, gate, F, N, chunks, tpc,
-                       static_cast<uint16_t*>(out));
+                       (unsigned)(fh_count * chunks), static_cast<uint16_t*>(out));
   return hipGetLastError();
 }
 

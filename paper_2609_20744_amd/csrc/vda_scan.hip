@@ -8,26 +8,43 @@
 // times Inv_t), so a chain (head, direction) is split into 16-row blocks,
 // one workgroup each, and the frame loop runs inside the workgroup with the
 // 16 x d_k block resident in LDS (double-buffered, fp32).  Per frame the four
-// wavefronts multiply the block by Inv_t with v_mfma_f32_16x16x4_f32, each
-// producing d_k/64 16-column slices.  The next frame's Inv_t and B_t are
-// loaded into registers one step ahead, so only the matrix product and two
-// barriers sit on the serial path.  Workgroups of one chain are placed on one
-// XCD so they share Inv_t in its L2.
+// wavefronts multiply the block by Inv_t, each producing d_k/64 16-column
+// slices.  Inv_t is symmetric ((I + A_t)^{-1} of a symmetric A_t), so the
+// k-th column slice a lane needs is read as a contiguous piece of row j of
+// Inv_t with 16-byte loads.  Inv_t and B_t of the next three frames are in
+// flight in a register ring, so memory latency stays off the serial path,
+// which holds only the matrix product and two barriers.  Workgroups of one
+// chain are placed on one XCD so they share Inv_t in its L2.
+//
+// Products: with fp32 storage, v_mfma_f32_16x16x4_f32 (exact fp32 products).
+// With bf16 storage, each fp32 operand x is split into bf16 hi = bf16(x) and
+// lo = bf16(x - hi), and the product is hi*hi + hi*lo + lo*hi on
+// v_mfma_f32_16x16x32_bf16 with fp32 accumulation (about 16 mantissa bits per
+// operand, relative error ~1e-5), several times the fp32 matrix rate.
 #include "vda_common.h"
 #include "vda_launch.h"
 
 namespace vda {
 namespace {
 
-template <int DK>
+__device__ __forceinline__ void split_bf16x8(const float (&x)[8], bf16x8& hi, bf16x8& lo) {
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const __bf16 h = (__bf16)x[e];
+    hi[e] = h;
+    lo[e] = (__bf16)(x[e] - (float)h);
+  }
+}
+
+template <int DK, bool EXACT_F32>
 __global__ __launch_bounds__(kThreads)
-void scan_kernel(const float* __restrict__ Inv, const float* __restrict__ B_part, int splits,
-                 size_t part_stride, int F, int DV, unsigned nwg,
+void scan_kernel(const float* __restrict__ Inv, const float* __restrict__ Bm,
+                 int F, int DV, unsigned nwg,
                  float* __restrict__ S_fwd, float* __restrict__ S_rev) {
   constexpr int XLD = DK + 4;        // LDS row stride (floats)
   constexpr int NB = DK / 16;        // 16-column output slices
   constexpr int NBW = (NB + 3) / 4;  // slices per wave
-  constexpr int KS = DK / 4;         // k values per lane group
+  constexpr int KL = DK / 4;         // k values per lane and slice
   constexpr int E = DK / 16;         // state elements per thread in the row-wise phase
   static_assert(E % 2 == 0, "float2 granularity");
   __shared__ __align__(16) float xs[2][16 * XLD];
@@ -41,7 +58,7 @@ void scan_kernel(const float* __restrict__ Inv, const float* __restrict__ B_part
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (scalar)
   const int li = lane & 15;
   const int lg = lane >> 4;
 
@@ -54,107 +71,173 @@ void scan_kernel(const float* __restrict__ Inv, const float* __restrict__ B_part
   float* Sout = dir == 0 ? S_fwd : S_rev;
   const size_t mat_b = (size_t)DV * DK;  // one B / state matrix
   const size_t row_off = (size_t)(rb * 16 + pr) * DK + pc;
+  // Entering states of this head, [F][d_v][d_k]: a range-checked buffer, so
+  // the padded steps past the last frame store nothing.
+  const __amdgpu_buffer_rsrc_t srsrc =
+      make_rsrc(Sout + (size_t)hb * F * mat_b, (uint32_t)(F * mat_b * sizeof(float)));
 
   auto frame_of = [&](int step) { return dir == 0 ? step : F - 1 - step; };
 
-  // B-operand of the MFMA: Inv_t[lg*KS + s][nb*16 + li].
-  float opc[NBW][KS], opn[NBW][KS];
-  float bc[E], bn[E];
-  auto load_ops = [&](int step, float (&op)[NBW][KS], float (&bb)[E]) {
+  // k indices held by this lane for the MFMA, in order:
+  //   exact fp32 (16x16x4, k = lg*KL + s):           lg*KL .. lg*KL + KL-1
+  //   split bf16 (16x16x32, k = ks*32 + 8*lg + e):   ks*32 + 8*lg .. +7, ks = 0..DK/32-1
+  auto kidx = [&](int s) {
+    return EXACT_F32 ? lg * KL + s : (s / 8) * 32 + 8 * lg + (s % 8);
+  };
+
+  // Operands of the next kPrefetch frames are in flight in a register ring
+  // (one workgroup per CU, so registers are plentiful): slot d holds frame
+  // step0 + d, refilled with frame step0 + d + kPrefetch once consumed.
+  constexpr int kPrefetch = 3;
+  float ops[kPrefetch][NBW][KL];
+  float bs[kPrefetch][E];
+  auto load_ops = [&](int step, float (&op)[NBW][KL], float (&bb)[E]) {
     const size_t fh = (size_t)hb * F + frame_of(step);
     const float* inv = Inv + fh * (DK * DK);
 #pragma unroll
     for (int m = 0; m < NBW; ++m) {
       const int nb = wave + 4 * m;
-      if (nb < NB) {
+      if (NB >= 4 || nb < NB) {  // compile-time true unless d_k = 32
+        // Inv[k][nb*16 + li] == Inv[nb*16 + li][k]
+        const float* row = inv + (size_t)(nb * 16 + li) * DK;
 #pragma unroll
-        for (int s = 0; s < KS; ++s) op[m][s] = inv[(lg * KS + s) * DK + nb * 16 + li];
-      }
-    }
-#pragma unroll
-    for (int e = 0; e < E; ++e) bb[e] = 0.f;
-    for (int sp = 0; sp < splits; ++sp) {
-      const float* src = B_part + sp * part_stride + fh * mat_b + row_off;
-#pragma unroll
-      for (int e = 0; e < E; e += 2) {
-        const float2 x = *reinterpret_cast<const float2*>(src + e);
-        bb[e] += x.x;
-        bb[e + 1] += x.y;
-      }
-    }
-  };
-
-  load_ops(0, opc, bc);
-  int cur = 0;
-  for (int step = 0; step < F; ++step) {
-    const size_t fh = (size_t)hb * F + frame_of(step);
-    if (step + 1 < F) load_ops(step + 1, opn, bn);
-    __syncthreads();  // xs[cur] holds the entering state
-    {
-      float* x = &xs[cur][pr * XLD + pc];
-      float* dst = Sout + fh * mat_b + row_off;
-#pragma unroll
-      for (int e = 0; e < E; e += 2) {
-        float2 v = *reinterpret_cast<float2*>(x + e);
-        *reinterpret_cast<float2*>(dst + e) = v;
-        v.x += bc[e];
-        v.y += bc[e + 1];
-        *reinterpret_cast<float2*>(x + e) = v;
-      }
-    }
-    __syncthreads();
-    if (wave < NB) {
-      float a[KS];
-      const float* xr = &xs[cur][li * XLD + lg * KS];
-#pragma unroll
-      for (int s = 0; s < KS; s += 4) {
-        const float4 v = *reinterpret_cast<const float4*>(xr + s);
-        a[s] = v.x;
-        a[s + 1] = v.y;
-        a[s + 2] = v.z;
-        a[s + 3] = v.w;
-      }
-#pragma unroll
-      for (int m = 0; m < NBW; ++m) {
-        const int nb = wave + 4 * m;
-        if (nb < NB) {
-          floatx4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-          for (int s = 0; s < KS; ++s)
-            acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[s], opc[m][s], acc, 0, 0, 0);
-#pragma unroll
-          for (int i = 0; i < 4; ++i) xs[cur ^ 1][(lg * 4 + i) * XLD + nb * 16 + li] = acc[i];
+        for (int s = 0; s < KL; s += 4) {
+          const float4 v = *reinterpret_cast<const float4*>(row + kidx(s));
+          op[m][s] = v.x;
+          op[m][s + 1] = v.y;
+          op[m][s + 2] = v.z;
+          op[m][s + 3] = v.w;
         }
       }
     }
-    cur ^= 1;
+    const float* src = Bm + fh * mat_b + row_off;
 #pragma unroll
-    for (int m = 0; m < NBW; ++m)
+    for (int e = 0; e < E; e += 2) {
+      const float2 x = *reinterpret_cast<const float2*>(src + e);
+      bb[e] = x.x;
+      bb[e + 1] = x.y;
+    }
+  };
+
+  // Issue the ring in slot order (pinned against rescheduling) so slot 0 is
+  // the oldest load on loop entry.
 #pragma unroll
-      for (int s = 0; s < KS; ++s) opc[m][s] = opn[m][s];
+  for (int d = 0; d < kPrefetch; ++d) {
+    load_ops(min(d, F - 1), ops[d], bs[d]);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+
+  // The step count is padded to a multiple of the ring depth; padded steps
+  // (step >= F) read a clamped frame and their stores are dropped, so the
+  // loop body has no early exit.
+  int cur = 0;
+  for (int step0 = 0; step0 < F; step0 += kPrefetch) {
 #pragma unroll
-    for (int e = 0; e < E; ++e) bc[e] = bn[e];
+    for (int d = 0; d < kPrefetch; ++d) {
+      const int step = step0 + d;
+      // Frame index within the head; past the end it is out of the buffer
+      // range (>= F forward, negative and so huge as unsigned in reverse).
+      const int frame = dir == 0 ? step : F - 1 - step;
+      __syncthreads();  // xs[cur] holds the entering state
+      {
+        float* x = &xs[cur][pr * XLD + pc];
+        const uint32_t off = (uint32_t)((size_t)(unsigned)frame * mat_b + row_off) * 4u;
+#pragma unroll
+        for (int e = 0; e < E; e += 2) {
+          float2 v = *reinterpret_cast<float2*>(x + e);
+          store_b64(srsrc, off + e * 4u, make_uint2(__float_as_uint(v.x), __float_as_uint(v.y)));
+          v.x += bs[d][e];
+          v.y += bs[d][e + 1];
+          *reinterpret_cast<float2*>(x + e) = v;
+        }
+      }
+      __syncthreads();
+      if (NB >= 4 || wave < NB) {
+        // A-operand: row li of the block at this lane's k indices.
+        float a[KL];
+        const float* xr = &xs[cur][li * XLD];
+#pragma unroll
+        for (int s = 0; s < KL; s += 4) {
+          const float4 v = *reinterpret_cast<const float4*>(xr + kidx(s));
+          a[s] = v.x;
+          a[s + 1] = v.y;
+          a[s + 2] = v.z;
+          a[s + 3] = v.w;
+        }
+        if constexpr (EXACT_F32) {
+#pragma unroll
+          for (int m = 0; m < NBW; ++m) {
+            const int nb = wave + 4 * m;
+            if (NB >= 4 || nb < NB) {
+              floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+              for (int s = 0; s < KL; ++s)
+                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[s], ops[d][m][s], acc, 0, 0, 0);
+#pragma unroll
+              for (int i = 0; i < 4; ++i) xs[cur ^ 1][(lg * 4 + i) * XLD + nb * 16 + li] = acc[i];
+            }
+          }
+        } else {
+          constexpr int KB = DK / 32;
+          bf16x8 ahi[KB], alo[KB];
+#pragma unroll
+          for (int kb = 0; kb < KB; ++kb) {
+            float t[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) t[e] = a[kb * 8 + e];
+            split_bf16x8(t, ahi[kb], alo[kb]);
+          }
+#pragma unroll
+          for (int m = 0; m < NBW; ++m) {
+            const int nb = wave + 4 * m;
+            if (NB >= 4 || nb < NB) {
+              floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+              for (int kb = 0; kb < KB; ++kb) {
+                float t[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) t[e] = ops[d][m][kb * 8 + e];
+                bf16x8 bhi, blo;
+                split_bf16x8(t, bhi, blo);
+                acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(alo[kb], bhi, acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi[kb], blo, acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi[kb], bhi, acc, 0, 0, 0);
+              }
+#pragma unroll
+              for (int i = 0; i < 4; ++i) xs[cur ^ 1][(lg * 4 + i) * XLD + nb * 16 + li] = acc[i];
+            }
+          }
+        }
+      }
+      // Always refill (past the end: a clamped, unused frame) so no branch
+      // hides the loads from the wait-count bookkeeping.
+      load_ops(min(step + kPrefetch, F - 1), ops[d], bs[d]);
+      cur ^= 1;
+    }
   }
 }
 
 template <int DK>
-hipError_t launch_scan_t(const float* Inv, const float* B_part, int splits, int F, int H, int d_v,
+hipError_t launch_scan_t(bool exact_f32, const float* Inv, const float* Bm, int F, int H, int d_v,
                          float* S_fwd, float* S_rev, hipStream_t stream) {
   const unsigned nwg = (unsigned)H * 2u * (unsigned)(d_v / 16);
-  const size_t part_stride = (size_t)H * F * d_v * DK;
-  hipLaunchKernelGGL(scan_kernel<DK>, dim3(nwg), dim3(kThreads), 0, stream, Inv, B_part, splits,
-                     part_stride, F, d_v, nwg, S_fwd, S_rev);
+  if (exact_f32)
+    hipLaunchKernelGGL((scan_kernel<DK, true>), dim3(nwg), dim3(kThreads), 0, stream, Inv, Bm, F,
+                       d_v, nwg, S_fwd, S_rev);
+  else
+    hipLaunchKernelGGL((scan_kernel<DK, false>), dim3(nwg), dim3(kThreads), 0, stream, Inv, Bm,
+                       F, d_v, nwg, S_fwd, S_rev);
   return hipGetLastError();
 }
 
 }  // namespace
 
-hipError_t launch_state_scan(const float* Inv, const float* B_part, int splits, int F, int H,
+hipError_t launch_state_scan(bool exact_f32, const float* Inv, const float* Bm, int F, int H,
                              int d_k, int d_v, float* S_fwd, float* S_rev, hipStream_t stream) {
   switch (d_k) {
-    case 32: return launch_scan_t<32>(Inv, B_part, splits, F, H, d_v, S_fwd, S_rev, stream);
-    case 64: return launch_scan_t<64>(Inv, B_part, splits, F, H, d_v, S_fwd, S_rev, stream);
-    case 128: return launch_scan_t<128>(Inv, B_part, splits, F, H, d_v, S_fwd, S_rev, stream);
+    case 32: return launch_scan_t<32>(exact_f32, Inv, Bm, F, H, d_v, S_fwd, S_rev, stream);
+    case 64: return launch_scan_t<64>(exact_f32, Inv, Bm, F, H, d_v, S_fwd, S_rev, stream);
+    case 128: return launch_scan_t<128>(exact_f32, Inv, Bm, F, H, d_v, S_fwd, S_rev, stream);
     default: return hipErrorInvalidValue;
   }
 }

@@ -41,7 +41,7 @@ _SIGNATURES = {
     "vda_forward_f32": (_I, [_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _P, _P]),
     "vda_default_splits": (_I, [_I, _I, _I]),
     "vda_frame_stats": (_I, [_P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _P, _P, _P]),
-    "vda_frame_inverse": (_I, [_P, _I, _I, _I, _P, _P]),
+    "vda_frame_inverse": (_I, [_P, _P, _I, _I, _I, _I, _P, _P]),
     "vda_state_scan": (_I, [_P, _P, _I, _I, _I, _I, _I, _P, _P, _P]),
     "vda_readout": (_I, [_P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _P, _P]),
 }
@@ -188,34 +188,44 @@ def frame_stats(k, v, beta, splits=None, A_part=None, B_part=None, stream=None):
     return A_part, B_part
 
 
-def frame_inverse(A_part, Inv=None, stream=None):
-    """Step a2 (vda_frame_inverse): (I + sum of partials)^-1, fp32.
-    A_part is [splits, count..., d_k, d_k]."""
+def frame_inverse(A_part, B_part=None, Inv=None, stream=None):
+    """Step a2 (vda_frame_inverse): Inv = (I + sum of A partials)^-1, fp32.
+    A_part is [splits, count..., d_k, d_k].  With splits > 1, B_part
+    ([splits, count..., d_v, d_k]) is folded in place into B_part[0]."""
     torch = _torch()
     splits = A_part.shape[0]
     d_k = A_part.shape[-1]
     count = math.prod(A_part.shape[1:-2])
+    d_v = B_part.shape[-2] if B_part is not None else d_k
+    if splits > 1 and B_part is None:
+        raise ValueError("B_part is required when there is more than one split")
     if Inv is None:
         Inv = torch.empty(A_part.shape[1:], dtype=torch.float32, device=A_part.device)
     with torch.cuda.device(A_part.device):
-        st = lib.vda_frame_inverse(A_part.data_ptr(), splits, count, d_k, Inv.data_ptr(),
+        st = lib.vda_frame_inverse(A_part.data_ptr(),
+                                   B_part.data_ptr() if B_part is not None else None,
+                                   splits, count, d_k, d_v, Inv.data_ptr(),
                                    _stream_ptr(A_part.device, stream))
     _check(st, "vda_frame_inverse")
     return Inv
 
 
-def state_scan(Inv, B_part, S_fwd=None, S_rev=None, stream=None):
-    """Steps a3/a4 (vda_state_scan).  Inv [H, F, d_k, d_k], B_part [splits, H, F, d_v, d_k]."""
+def state_scan(Inv, B, S_fwd=None, S_rev=None, exact_f32=False, stream=None):
+    """Steps a3/a4 (vda_state_scan).  Inv [H, F, d_k, d_k], B [H, F, d_v, d_k]
+    (the reduced statistic, e.g. B_part[0] after frame_inverse).
+    exact_f32 selects fp32 matrix products (the fp32 storage path); otherwise
+    split-bf16 products with fp32 accumulation (the bf16 storage path)."""
     torch = _torch()
-    splits, H, F, d_v, d_k = B_part.shape
-    dev = B_part.device
+    H, F, d_v, d_k = B.shape
+    dev = B.device
     if S_fwd is None:
         S_fwd = torch.empty((H, F, d_v, d_k), dtype=torch.float32, device=dev)
     if S_rev is None:
         S_rev = torch.empty((H, F, d_v, d_k), dtype=torch.float32, device=dev)
     with torch.cuda.device(dev):
-        st = lib.vda_state_scan(Inv.data_ptr(), B_part.data_ptr(), splits, F, H, d_k, d_v,
-                                S_fwd.data_ptr(), S_rev.data_ptr(), _stream_ptr(dev, stream))
+        st = lib.vda_state_scan(Inv.data_ptr(), B.data_ptr(), F, H, d_k, d_v,
+                                int(bool(exact_f32)), S_fwd.data_ptr(), S_rev.data_ptr(),
+                                _stream_ptr(dev, stream))
     _check(st, "vda_state_scan")
     return S_fwd, S_rev
 

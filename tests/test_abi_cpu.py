@@ -64,13 +64,16 @@ def test_stage_validation():
     assert L.vda_frame_stats(big, 2 * big, 3 * big, 4, 64, 2, 64, 64, 2, 0, 4 * big, 5 * big, None) == 2
     assert L.vda_frame_stats(big, 2 * big, 3 * big, 4, 64, 2, 64, 64, 1, 0, 4 * big + 4, 5 * big, None) == 4
     assert L.vda_frame_stats(big, 2 * big, 3 * big, 4, 64, 2, 64, 64, 1, 0, big, 5 * big, None) == 5
-    assert L.vda_frame_inverse(None, 1, 8, 64, big, None) == 1
-    assert L.vda_frame_inverse(big, 1, 8, 96, 2 * big, None) == 3
-    assert L.vda_frame_inverse(big, 0, 8, 64, 2 * big, None) == 2
+    assert L.vda_frame_inverse(None, None, 1, 8, 64, 64, big, None) == 1
+    assert L.vda_frame_inverse(big, None, 2, 8, 64, 64, 2 * big, None) == 1
+    assert L.vda_frame_inverse(big, None, 1, 8, 96, 64, 2 * big, None) == 3
+    assert L.vda_frame_inverse(big, None, 0, 8, 64, 64, 2 * big, None) == 2
     # in place onto the first partial is allowed (would launch), onto the second is not
-    assert L.vda_frame_inverse(big, 2, 8, 64, big + 8 * 64 * 64 * 4, None) == 5
-    assert L.vda_state_scan(big, 2 * big, 1, 4, 2, 64, 64, 3 * big, 3 * big, None) == 5
-    assert L.vda_state_scan(big, 2 * big, 1, 4, 2, 64, 48, 3 * big, 4 * big, None) == 3
+    assert L.vda_frame_inverse(big, 3 * big, 2, 8, 64, 64, big + 8 * 64 * 64 * 4, None) == 5
+    # B partials may not overlap the A partials or Inv
+    assert L.vda_frame_inverse(big, big + 4096, 2, 8, 64, 64, 2 * big, None) == 5
+    assert L.vda_state_scan(big, 2 * big, 4, 2, 64, 64, 0, 3 * big, 3 * big, None) == 5
+    assert L.vda_state_scan(big, 2 * big, 4, 2, 64, 48, 0, 3 * big, 4 * big, None) == 3
     assert L.vda_readout(big, 2 * big, 3 * big, 4 * big, 4, 64, 2, 64, 64, 0, big, None) == 5
     assert L.vda_readout(big, 2 * big, 3 * big, None, 4, 64, 2, 64, 64, 0, 5 * big, None) == 1
 
