@@ -55,6 +55,86 @@ def kernel_bytes(w):
     }
 
 
+# Kernel of each stage, and the sources whose change makes counters taken
+# on it stale.
+KERNEL_OF = {"frame_stats": "stats_bf16_kernel", "frame_inverse": "inverse_kernel",
+             "state_scan": "scan_kernel", "readout": "readout_bf16_kernel"}
+SOURCE_OF = {"frame_stats": "vda_stats.hip", "frame_inverse": "vda_inverse.hip",
+             "state_scan": "vda_scan.hip", "readout": "vda_readout.hip"}
+
+
+def source_hash(stage: str) -> str:
+    """SHA-256 over the kernel's source file and the shared device header."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in (SOURCE_OF[stage], "vda_common.h"):
+        with open(os.path.join(ROOT, "paper_2609_20744_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def traffic_file(workload: str) -> str:
+    return os.path.join(ROOT, "profiles", f"hbm_traffic_{workload}.json")
+
+
+def measured_traffic(workload: str, stage: str):
+    """HBM bytes per launch of `stage` from the committed counter summary, or
+    None when there is none or the kernel's source has changed since."""
+    path = traffic_file(workload)
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        summ = json.load(f)
+    k = summ.get("kernels", {}).get(stage)
+    if not k or k.get("source_sha256") != source_hash(stage):
+        return None
+    return k["hbm_bytes_per_launch"]
+
+
+def pmc_summary(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, copy_gib, workload):
+    """Turn four rocprofv3 --pmc runs (FETCH_SIZE and WRITE_SIZE of the bench,
+    and of the --calibrate-copy run) into HBM bytes per launch per kernel.
+    Each counter (KiB per dispatch) is scaled by the factor that makes it
+    match the bytes a plain copy of known size reads or writes."""
+    import csv
+    import re
+
+    def load(d):
+        """Average bytes per dispatch, by kernel: the library's kernels by
+        their function name, the calibration copy (torch's neg) as "copy"."""
+        out = {}
+        with open(os.path.join(d, "run_counter_collection.csv")) as f:
+            for r in csv.DictReader(f):
+                full = r["Kernel_Name"]
+                if "neg_kernel" in full:
+                    name = "copy"
+                else:
+                    m = re.search(r"::(\w+)(<[^()]*>)?\(", full)
+                    name = m.group(1) if m else full
+                out.setdefault(name, []).append(float(r["Counter_Value"]) * 1024.0)
+        return {n: sum(v) / len(v) for n, v in out.items()}
+
+    copy_bytes = copy_gib * (1 << 30)
+    f_fetch = copy_bytes / load(copy_fetch_dir)["copy"]
+    f_write = copy_bytes / load(copy_write_dir)["copy"]
+    fetch, write = load(fetch_dir), load(write_dir)
+    w = __import__("paper_2609_20744_amd.inputs", fromlist=["WORKLOADS"]).WORKLOADS[workload]
+    kb = kernel_bytes(w)
+    kernels = {}
+    for stage, kname in KERNEL_OF.items():
+        if kname not in fetch or kname not in write:
+            continue
+        rd, wr = fetch[kname] * f_fetch, write[kname] * f_write
+        kernels[stage] = {"kernel": kname, "fetch_size_bytes_raw": fetch[kname],
+                          "write_size_bytes_raw": write[kname], "hbm_read_bytes": rd,
+                          "hbm_write_bytes": wr, "hbm_bytes_per_launch": rd + wr,
+                          "algorithmic_bytes_per_launch": kb[stage],
+                          "traffic_over_algorithmic": (rd + wr) / kb[stage],
+                          "source_sha256": source_hash(stage)}
+    return {"workload": workload, "copy_gib": copy_gib, "fetch_factor": f_fetch,
+            "write_factor": f_write, "kernels": kernels}
+
+
 def cpu_baseline(w, budget_s: float = 20.0) -> dict:
     """Time the fp64 oracle on whole heads of the same workload until about
     budget_s of CPU work, and scale to the full job's tokens/s."""
@@ -99,7 +179,16 @@ def main() -> int:
     ap.add_argument("--calibrate-copy", type=float, default=0.0, metavar="GIB",
                     help="instead of the operator, run a plain elementwise copy (torch.neg) "
                          "reading and writing GIB GiB, to calibrate HBM byte counters")
+    ap.add_argument("--pmc-summary", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR",
+                                                       "COPY_WRITE_DIR"),
+                    help="summarise rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE runs of this "
+                         "benchmark and of --calibrate-copy into HBM bytes per launch (no GPU)")
+    ap.add_argument("--copy-gib", type=float, default=1.0,
+                    help="size given to --calibrate-copy in the counter runs")
     args = ap.parse_args()
+    if args.pmc_summary:
+        print(json.dumps(pmc_summary(*args.pmc_summary, args.copy_gib, args.workload), indent=1))
+        return 0
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (the operator is one GPU's head shard); "
               f"--gpus {args.gpus} is not supported", file=sys.stderr)
@@ -189,6 +278,8 @@ def main() -> int:
     ms = total_ms / K
     per_kernel = {n: sum(evs[i][j].elapsed_time(evs[i][j + 1]) for i in range(K)) / K
                   for j, n in enumerate(names)}
+    step_ms = sorted(evs[i][0].elapsed_time(evs[i][4]) for i in range(K))
+    pct = lambda p: step_ms[min(K - 1, int(p * (K - 1) + 0.5))]
     print(f"[bench] timed {K} steps: {ms:.4f} ms/step", file=sys.stderr, flush=True)
 
     # Cross-check: the all-in-one entry point over the same number of steps.
@@ -230,11 +321,13 @@ def main() -> int:
         "hbm_gbs_alg": gbs,
         "pct_hbm_peak": 100.0 * gbs / PEAK_HBM_GBS,
         "token_heads_per_s": w.tokens * w.H / t,
+        "step_ms_p10_p50_p90": [pct(0.1), pct(0.5), pct(0.9)],
         "kernel_ms": per_kernel,
         "forward_entry_ms_per_step": fused_ms,
         "wall_s_timed_region": wall,
         "roofline": {"bound": "hbm", "kernel": dominant, "achieved": ach, "peak": PEAK_HBM_GBS,
-                     "unit": "GB/s", "frac": ach / PEAK_HBM_GBS, "traffic": None},
+                     "unit": "GB/s", "frac": ach / PEAK_HBM_GBS,
+                     "traffic": measured_traffic(w.name, dominant)},
     }
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
