@@ -69,6 +69,10 @@ __device__ __forceinline__ void store_b64(__amdgpu_buffer_rsrc_t r, uint32_t byt
   __builtin_amdgcn_raw_buffer_store_b64(u32x2{v.x, v.y}, r, (int)byte_off, 0, 0);
 }
 
+__device__ __forceinline__ void store_b128(__amdgpu_buffer_rsrc_t r, uint32_t byte_off, u32x4 v) {
+  __builtin_amdgcn_raw_buffer_store_b128(v, r, (int)byte_off, 0, 0);
+}
+
 // Workgroup-uniform integer kept in a scalar register.  Integer division by
 // a runtime value is expanded on the vector ALU; without this the compiler
 // may treat values derived from it (such as buffer descriptors) as varying

@@ -10,7 +10,8 @@
 // loads straight from HBM, three groups in flight per wave), O^T = S~ Q^T is
 // accumulated in fp32 by v_mfma_f32_16x16x32_bf16, and the RMSNorm over the
 // d_v outputs of a token is a lane-local sum plus two cross-lane exchanges.
-// The normalised, gated values are rounded to bf16 and stored.
+// The normalised, gated values are rounded to bf16 and stored 16 bytes per
+// lane (a cross-lane swap first gathers 8 consecutive channels in a lane).
 #include "vda_common.h"
 #include "vda_launch.h"
 
@@ -45,6 +46,8 @@ void readout_bf16_kernel(const uint16_t* __restrict__ Q, const float* __restrict
   {
     const float* sf = S_fwd + (size_t)fh * (DV * DK);
     const float* sr = S_rev + (size_t)fh * (DV * DK);
+    // Fully unrolled, so all of a thread's loads are in flight together.
+#pragma unroll
     for (int idx = tid * 4; idx < DV * DK; idx += kThreads * 4) {
       const float4 a = *reinterpret_cast<const float4*>(sf + idx);
       const float4 b = *reinterpret_cast<const float4*>(sr + idx);
@@ -115,12 +118,24 @@ void readout_bf16_kernel(const uint16_t* __restrict__ Q, const float* __restrict
       ss += __shfl_xor(ss, 16);
       ss += __shfl_xor(ss, 32);
       const float scale = g / sqrtf(ss * (1.0f / DV) + kRmsEps);
-      const uint32_t off = ((uint32_t)(ng + li) * DV + lg * 4) * 2u;
+      // 16-byte stores: for each pair of row blocks (2m, 2m+1), lane groups
+      // 2p and 2p+1 (lanes l and l ^ 16) swap one 4-channel piece with
+      // v_permlane16_swap, after which lane group 2p holds channels
+      // 32m + 8p .. +7 of block 2m's rows and lane group 2p+1 the same
+      // channels of block 2m+1 (+16).  Each store then writes 64 contiguous
+      // bytes of each of 16 token rows.
+      const uint32_t off =
+          ((uint32_t)(ng + li) * DV + (lg & 1) * 16 + (lg >> 1) * 8) * 2u;
 #pragma unroll
-      for (int mb = 0; mb < MB; ++mb)
-        store_b64(orsrc, off + mb * 32u,
-                  make_uint2(pack_bf16x2(acc[mb][0] * scale, acc[mb][1] * scale),
-                             pack_bf16x2(acc[mb][2] * scale, acc[mb][3] * scale)));
+      for (int m = 0; m < MB / 2; ++m) {
+        const uint32_t a0 = pack_bf16x2(acc[2 * m][0] * scale, acc[2 * m][1] * scale);
+        const uint32_t a1 = pack_bf16x2(acc[2 * m][2] * scale, acc[2 * m][3] * scale);
+        const uint32_t b0 = pack_bf16x2(acc[2 * m + 1][0] * scale, acc[2 * m + 1][1] * scale);
+        const uint32_t b1 = pack_bf16x2(acc[2 * m + 1][2] * scale, acc[2 * m + 1][3] * scale);
+        const auto s0 = __builtin_amdgcn_permlane16_swap(a0, b0, false, false);
+        const auto s1 = __builtin_amdgcn_permlane16_swap(a1, b1, false, false);
+        store_b128(orsrc, off + m * 64u, u32x4{s0[0], s1[0], s0[1], s1[1]});
+      }
     }
   }
 }
