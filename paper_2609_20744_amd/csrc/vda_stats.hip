@@ -66,7 +66,11 @@ void stats_bf16_kernel(const uint16_t* __restrict__ K, const uint16_t* __restric
   constexpr int LDY = tile_ld(DK);
   constexpr int RB = XC / 16;         // 16-row output blocks
   constexpr int CB = DK / 16;         // 16-column output blocks
-  constexpr int RPW = (RB + 3) / 4;   // output row blocks per wave
+  // The four waves split the workgroup's XC x DK output 2 x 2: wave (wr, wc)
+  // owns row blocks wr*RPW .. and column blocks wc*CPW .. .  Per token a wave
+  // reads RPW + CPW operand blocks from LDS, fewer than a 4 x 1 split.
+  constexpr int RPW = (RB + 1) / 2;   // output row blocks per wave
+  constexpr int CPW = CB / 2;         // output column blocks per wave
   constexpr int KCH = DK / 8;         // 16-byte chunks per K row
   constexpr int VCH = VH / 8;         // 16-byte chunks per V-half row
   constexpr int NKC = kStatsTile * KCH / kThreads;                // K chunks per thread
@@ -90,6 +94,8 @@ void stats_bf16_kernel(const uint16_t* __restrict__ K, const uint16_t* __restric
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (scalar)
+  const int wr = wave & 1;
+  const int wc = wave >> 1;
   const int li = lane & 15;
   const int lg = lane >> 4;
 
@@ -150,11 +156,11 @@ void stats_bf16_kernel(const uint16_t* __restrict__ K, const uint16_t* __restric
     }
   };
 
-  floatx4 acc[RPW][CB];
+  floatx4 acc[RPW][CPW];
 #pragma unroll
   for (int r = 0; r < RPW; ++r)
 #pragma unroll
-    for (int cb = 0; cb < CB; ++cb) acc[r][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
+    for (int c = 0; c < CPW; ++c) acc[r][c] = floatx4{0.f, 0.f, 0.f, 0.f};
 
   // Consume one tile from the ring, then refill its slot with tile n_next.
   auto tile_step = [&](int n_next, u32x4 (&kr)[NKC], float (&kbv)[NKC], u32x4 (&vr)[NVC]) {
@@ -164,17 +170,18 @@ void stats_bf16_kernel(const uint16_t* __restrict__ K, const uint16_t* __restric
     load_tile(n_next, kr, kbv, vr);
 #pragma unroll
     for (int ks = 0; ks < kStatsTile / 32; ++ks) {
-      bf16x8 bop[CB];
+      bf16x8 bop[CPW];
 #pragma unroll
-      for (int cb = 0; cb < CB; ++cb) bop[cb] = tr_operand<LDY>(yt, ks * 32, cb * 16, li, lg);
+      for (int c = 0; c < CPW; ++c)
+        bop[c] = tr_operand<LDY>(yt, ks * 32, (wc * CPW + c) * 16, li, lg);
 #pragma unroll
       for (int r = 0; r < RPW; ++r) {
-        const int rb = wave + 4 * r;
-        if (RB % 4 == 0 || rb < RB) {
+        const int rb = wr * RPW + r;
+        if (RB % 2 == 0 || rb < RB) {
           const bf16x8 aop = tr_operand<LDX>(xt, ks * 32, rb * 16, li, lg);
 #pragma unroll
-          for (int cb = 0; cb < CB; ++cb)
-            acc[r][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aop, bop[cb], acc[r][cb], 0, 0, 0);
+          for (int c = 0; c < CPW; ++c)
+            acc[r][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aop, bop[c], acc[r][c], 0, 0, 0);
         }
       }
     }
@@ -197,18 +204,18 @@ void stats_bf16_kernel(const uint16_t* __restrict__ K, const uint16_t* __restric
   float* Bb = B_part + ((size_t)split * fh_count + fh) * (DV * DK);
 #pragma unroll
   for (int r = 0; r < RPW; ++r) {
-    const int rb = wave + 4 * r;
-    if (RB % 4 == 0 || rb < RB) {
+    const int rb = wr * RPW + r;
+    if (RB % 2 == 0 || rb < RB) {
 #pragma unroll
-      for (int cb = 0; cb < CB; ++cb)
+      for (int c = 0; c < CPW; ++c)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int x = rb * 16 + lg * 4 + i;
-          const int col = cb * 16 + li;
+          const int col = (wc * CPW + c) * 16 + li;
           if (rb * 16 < KH)
-            Ab[(half * KH + x) * DK + col] = acc[r][cb][i];
+            Ab[(half * KH + x) * DK + col] = acc[r][c][i];
           else
-            Bb[(half * VH + x - KH) * DK + col] = acc[r][cb][i];
+            Bb[(half * VH + x - KH) * DK + col] = acc[r][c][i];
         }
     }
   }
