@@ -79,6 +79,17 @@ __device__ __forceinline__ void store_b128(__amdgpu_buffer_rsrc_t r, uint32_t by
 // per lane.
 __device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
 
+// Workgroup barrier after which LDS written before it by any wave is
+// visible.  Each wave first waits for its own outstanding LDS operations
+// (s_waitcnt lgkmcnt(0); the immediate leaves the other counters at their
+// maximum): the compiler is relied on for that wait inside __syncthreads(),
+// but it has been seen to drop it where a loop's back edge reaches the
+// barrier right after LDS stores, which lets another wave read stale data.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_s_waitcnt(0xc07f);
+  __syncthreads();
+}
+
 // Map a linear workgroup id onto a logical id so that consecutive logical
 // ids land on the same XCD.  Workgroups are dispatched round-robin over the
 // 8 XCDs (id % 8), each with its own L2; grouping logically adjacent work

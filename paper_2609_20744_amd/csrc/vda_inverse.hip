@@ -4,24 +4,27 @@
 // a Gram matrix weighted by beta >= 0; Appendix A.1), so Gauss-Jordan
 // elimination needs no pivoting and every leading block is invertible.
 //
-// One wavefront inverts one d_k x d_k matrix in fp32 by blocked Gauss-Jordan
-// with 16 x 16 blocks, the whole matrix held in MFMA accumulator layout
-// (block (i, j): lane (c, g) holds rows 4g..4g+3, column c).  No LDS and no
-// barriers are needed, because symmetry puts every operand in the lane's own
-// registers.  After eliminating block columns 0..kb-1 the matrix is
-// [[X, Y], [Z, S]] with X and S symmetric and Z = -Y^T, so block (i, kb) is
-// the transpose of the stored block (kb, i), negated when i < kb.  The
-// v_mfma_f32_16x16x4_f32 operand a lane supplies at k = 4g + s is then
-// element s of its own accumulator of that transposed block.  Block step kb:
-//   1. D^{-1} of the pivot block D = M[kb][kb] by scalar Gauss-Jordan (rows
-//      and columns exchanged by cross-lane shuffles);
-//   2. R_j = D^{-1} M[kb][j] for j != kb (D^{-1} is symmetric, so it is its
-//      own A-operand);
-//   3. M[i][j] -= M[i][kb] R_j and M[i][kb] = -M[i][kb] D^{-1} for i != kb;
-//   4. M[kb][j] = R_j, M[kb][kb] = D^{-1}.
-// Only the pivot row of each step is ever read, so a block (i, j) with
-// j > kb that step j will overwrite (i < kb, or i > j) is not updated: about
-// a third of the Gauss-Jordan products are skipped.
+// One workgroup inverts one d_k x d_k matrix in fp32 by blocked Gauss-Jordan
+// with 16 x 16 blocks on v_mfma_f32_16x16x4_f32.  Block rows are dealt out
+// to the waves (wave w owns rows w, w + W, ...), each held in MFMA
+// accumulator layout (block (i, j): lane (c, g) holds rows 4g..4g+3, column
+// c).  Block step kb:
+//   1. the owner of row kb inverts the pivot block D = M[kb][kb] by scalar
+//      Gauss-Jordan (rows and columns exchanged by cross-lane shuffles) and
+//      publishes D^{-1} and the pivot row P_j = M[kb][j] in LDS;
+//   2. every wave forms R_j = D^{-1} P_j (D^{-1} is symmetric, so it is its
+//      own A-operand) and, for its rows i != kb,
+//        M[i][j] -= M[i][kb] R_j,   M[i][kb] = -M[i][kb] D^{-1};
+//      the owner of row kb sets M[kb][j] = R_j, M[kb][kb] = D^{-1}.
+// After eliminating block columns 0..kb-1 the matrix is [[X, Y], [Z, S]]
+// with X and S symmetric and Z = -Y^T, so M[i][kb] is the transpose of the
+// published P_i, negated when i < kb: the A-operand a lane supplies at
+// k = 4g + s is element s of its own slot of P_i.  A block (i, j) with
+// j > kb that step j will overwrite (i < kb, or i > j) is not updated:
+// about a third of the products are skipped.  The LDS pivot row is double
+// buffered, so each block step needs one barrier.  With several matrices'
+// workgroups per SIMD, one wave's serial pivot work hides behind another's
+// products.
 // Both A_t and its inverse are symmetric, so the column segments of the
 // accumulator layout are loaded and stored as contiguous row segments of the
 // transposed block (the result is the transpose of the computed inverse,
@@ -35,40 +38,52 @@
 namespace vda {
 namespace {
 
-template <int DK>
-__global__ __launch_bounds__(64)
-void inverse_kernel(const float* A_part, int splits, size_t part_stride,
-                    float* Inv,  // may alias A_part (in place)
-                    float* B_part, size_t b_mat, size_t b_stride) {
-  constexpr int NB = DK / 16;  // 16-wide blocks per side
-  const size_t base = (size_t)blockIdx.x * (DK * DK);
-  const int lane = threadIdx.x;
+// Pivot block inverse: lane (li, lg) holds D[4lg + r][li] in d[r] on entry
+// and D^{-1} in the same layout on exit.  Hardware reciprocal refined by one
+// Newton step (error <= 1 ulp); the IEEE division sequence would sit on the
+// serial path once per pivot.
+__device__ __forceinline__ void invert_pivot_block(float (&d)[4], int li, int lg) {
+#pragma unroll
+  for (int p = 0; p < 16; ++p) {
+    const float rowv = __shfl(d[p & 3], li + 16 * (p >> 2));   // D[p][li]
+    float colv[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) colv[r] = __shfl(d[r], p + 16 * lg);  // D[4lg+r][p]
+    const float piv = __shfl(rowv, p);                           // D[p][p]
+    float inv = __builtin_amdgcn_rcpf(piv);
+    inv = inv * fmaf(-piv, inv, 2.0f);
+    const float rs = rowv * inv;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) d[r] = fmaf(-colv[r], rs, d[r]);
+    if (lg == (p >> 2)) d[p & 3] = (li == p) ? inv : rs;          // pivot row
+    if (li == p) {                                               // pivot column
+#pragma unroll
+      for (int r = 0; r < 4; ++r) d[r] = (4 * lg + r == p) ? inv : -colv[r] * inv;
+    }
+  }
+}
+
+// The elimination for the block rows of wave WV (rows WV, WV + W, ...); a
+// template on the wave so that every row-dependent condition is resolved at
+// compile time.  All W waves of the workgroup take the same NB barriers.
+template <int DK, int WV>
+__device__ __forceinline__ void invert_rows(const float* A_part, int splits, size_t part_stride,
+                                            size_t base, float* Inv, float (*piv)[DK / 16][64 * 4],
+                                            int lane) {
+  constexpr int NB = DK / 16;          // 16-wide blocks per side
+  constexpr int W = NB < 4 ? NB : 4;   // waves
+  constexpr int RPW = NB / W;          // block rows per wave
   const int li = lane & 15;
   const int lg = lane >> 4;
 
-  // Fold the token-split partials of B_t into the first partial (in place).
-  if (splits > 1) {
-    float* b0 = B_part + (size_t)blockIdx.x * b_mat;
-    for (size_t idx = (size_t)lane * 4; idx < b_mat; idx += 64 * 4) {
-      float4 a4 = *reinterpret_cast<const float4*>(b0 + idx);
-      for (int s = 1; s < splits; ++s) {
-        const float4 x = *reinterpret_cast<const float4*>(b0 + s * b_stride + idx);
-        a4.x += x.x;
-        a4.y += x.y;
-        a4.z += x.z;
-        a4.w += x.w;
-      }
-      *reinterpret_cast<float4*>(b0 + idx) = a4;
-    }
-  }
-
-  // The accumulator of block (i, j) holds the column segment
-  // M[16i + 4lg .. +3][16j + li]; A_t is symmetric, so it is read as the
-  // contiguous row segment M[16j + li][16i + 4lg .. +3] with 16-byte loads
-  // (and the result is written back the same way).
-  floatx4 acc[NB][NB];
+  // acc[q][j]: block (i, j) with i = WV + W q.  Its accumulator holds the
+  // column segment M[16i + 4lg .. +3][16j + li]; A_t is symmetric, so it is
+  // read as the contiguous row segment M[16j + li][16i + 4lg .. +3] with
+  // 16-byte loads (and the result is written back the same way).
+  floatx4 acc[RPW][NB];
 #pragma unroll
-  for (int i = 0; i < NB; ++i)
+  for (int q = 0; q < RPW; ++q) {
+    const int i = WV + W * q;
 #pragma unroll
     for (int j = 0; j < NB; ++j) {
       floatx4 v = {0.f, 0.f, 0.f, 0.f};
@@ -85,56 +100,62 @@ void inverse_kernel(const float* A_part, int splits, size_t part_stride,
         for (int r = 0; r < 4; ++r)
           if (4 * lg + r == li) v[r] += 1.0f;
       }
-      acc[i][j] = v;
+      acc[q][j] = v;
     }
+  }
 
 #pragma unroll
   for (int kb = 0; kb < NB; ++kb) {
-    // 1. D^{-1}: lane holds D[4*lg + r][li] in d[r].
-    float d[4] = {acc[kb][kb][0], acc[kb][kb][1], acc[kb][kb][2], acc[kb][kb][3]};
-#pragma unroll
-    for (int p = 0; p < 16; ++p) {
-      const float rowv = __shfl(d[p & 3], li + 16 * (p >> 2));   // D[p][li]
-      float colv[4];
-#pragma unroll
-      for (int r = 0; r < 4; ++r) colv[r] = __shfl(d[r], p + 16 * lg);  // D[4lg+r][p]
-      const float piv = __shfl(rowv, p);                           // D[p][p]
-      // Hardware reciprocal refined by one Newton step (error <= 1 ulp); the
-      // IEEE division sequence would sit 128 times on the serial path.
-      float inv = __builtin_amdgcn_rcpf(piv);
-      inv = inv * fmaf(-piv, inv, 2.0f);
-      const float rs = rowv * inv;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) d[r] = fmaf(-colv[r], rs, d[r]);
-      if (lg == (p >> 2)) d[p & 3] = (li == p) ? inv : rs;          // pivot row
-      if (li == p) {                                               // pivot column
-#pragma unroll
-        for (int r = 0; r < 4; ++r) d[r] = (4 * lg + r == p) ? inv : -colv[r] * inv;
-      }
-    }
-
-    // 2. R_j = D^{-1} M[kb][j]; A-operand D^{-1}[li][4lg+s] = d[s] (symmetric).
-    floatx4 R[NB];
-#pragma unroll
-    for (int j = 0; j < NB; ++j) R[j] = floatx4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int s = 0; s < 4; ++s)
+    float* pb = &piv[kb & 1][0][0];
+    // 1. The owner of row kb publishes D^{-1} (in slot kb) and P_j (j != kb).
+    if (kb % W == WV) {
+      const floatx4 dd = acc[kb / W][kb];
+      float d[4] = {dd[0], dd[1], dd[2], dd[3]};
+      invert_pivot_block(d, li, lg);
 #pragma unroll
       for (int j = 0; j < NB; ++j) {
-        if (j == kb) continue;
-        R[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(d[s], acc[kb][j][s], R[j], 0, 0, 0);
+        const floatx4 v = j == kb ? floatx4{d[0], d[1], d[2], d[3]} : acc[kb / W][j];
+        *reinterpret_cast<float4*>(pb + (j * 64 + lane) * 4) = make_float4(v[0], v[1], v[2], v[3]);
       }
+    }
+    lds_barrier();
 
-    // 3. rows i != kb.  A-operand of -M[i][kb] at k = 4lg + s:
-    //    i > kb: -acc[kb][i][s];  i < kb: +acc[kb][i][s].
+    // 2. R_j = D^{-1} P_j; A-operand D^{-1}[li][4lg+s] = d[s] (symmetric).
+    float d[4];
+    {
+      const float4 v = *reinterpret_cast<const float4*>(pb + (kb * 64 + lane) * 4);
+      d[0] = v.x;
+      d[1] = v.y;
+      d[2] = v.z;
+      d[3] = v.w;
+    }
+    floatx4 R[NB];
 #pragma unroll
-    for (int i = 0; i < NB; ++i) {
-      if (i == kb) continue;
-      float a[4];
+    for (int j = 0; j < NB; ++j) {
+      R[j] = floatx4{0.f, 0.f, 0.f, 0.f};
+      if (j == kb) continue;
+      const float4 p = *reinterpret_cast<const float4*>(pb + (j * 64 + lane) * 4);
+      R[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(d[0], p.x, R[j], 0, 0, 0);
+      R[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(d[1], p.y, R[j], 0, 0, 0);
+      R[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(d[2], p.z, R[j], 0, 0, 0);
+      R[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(d[3], p.w, R[j], 0, 0, 0);
+    }
+
 #pragma unroll
-      for (int s = 0; s < 4; ++s) a[s] = (i > kb) ? -acc[kb][i][s] : acc[kb][i][s];
-      // Independent accumulators innermost, so consecutive products do not
-      // wait on each other.
+    for (int q = 0; q < RPW; ++q) {
+      const int i = WV + W * q;
+      if (i == kb) {
+        // 4. pivot row.
+#pragma unroll
+        for (int j = 0; j < NB; ++j)
+          acc[q][j] = j == kb ? floatx4{d[0], d[1], d[2], d[3]} : R[j];
+        continue;
+      }
+      // 3. A-operand of -M[i][kb] at k = 4lg + s, from P_i = M[kb][i]:
+      //    i > kb: -P_i[s];  i < kb: +P_i[s].
+      const float4 p = *reinterpret_cast<const float4*>(pb + (i * 64 + lane) * 4);
+      const float sg = i > kb ? -1.0f : 1.0f;
+      const float a[4] = {sg * p.x, sg * p.y, sg * p.z, sg * p.w};
       floatx4 o = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int s = 0; s < 4; ++s) {
@@ -143,29 +164,60 @@ void inverse_kernel(const float* A_part, int splits, size_t part_stride,
           // Block (i, j), j > kb, is overwritten at step j (from the pivot
           // row's transpose) unless kb < i <= j: skip those dead updates.
           if (j == kb || (j > kb && (i > j || i < kb))) continue;
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[s], R[j][s], acc[i][j], 0, 0, 0);
+          acc[q][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[s], R[j][s], acc[q][j], 0, 0, 0);
         }
         o = __builtin_amdgcn_mfma_f32_16x16x4f32(a[s], d[s], o, 0, 0, 0);
       }
-      acc[i][kb] = o;
-    }
-
-    // 4. pivot row.
-#pragma unroll
-    for (int j = 0; j < NB; ++j) {
-      if (j == kb)
-        acc[kb][j] = floatx4{d[0], d[1], d[2], d[3]};
-      else
-        acc[kb][j] = R[j];
+      acc[q][kb] = o;
     }
   }
 
 #pragma unroll
-  for (int i = 0; i < NB; ++i)
+  for (int q = 0; q < RPW; ++q) {
+    const int i = WV + W * q;
 #pragma unroll
     for (int j = 0; j < NB; ++j)
       *reinterpret_cast<float4*>(Inv + base + (size_t)(16 * j + li) * DK + 16 * i + 4 * lg) =
-          make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+          make_float4(acc[q][j][0], acc[q][j][1], acc[q][j][2], acc[q][j][3]);
+  }
+}
+
+template <int DK>
+__global__ __launch_bounds__(64 * (DK / 16 < 4 ? DK / 16 : 4))
+void inverse_kernel(const float* A_part, int splits, size_t part_stride,
+                    float* Inv,  // may alias A_part (in place)
+                    float* B_part, size_t b_mat, size_t b_stride) {
+  constexpr int NB = DK / 16;
+  constexpr int W = NB < 4 ? NB : 4;
+  __shared__ __align__(16) float piv[2][NB][64 * 4];  // [buffer][block j][lane][4]
+
+  const size_t base = (size_t)blockIdx.x * (DK * DK);
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+
+  // Fold the token-split partials of B_t into the first partial (in place).
+  if (splits > 1) {
+    float* b0 = B_part + (size_t)blockIdx.x * b_mat;
+    for (size_t idx = (size_t)tid * 4; idx < b_mat; idx += 64 * W * 4) {
+      float4 a4 = *reinterpret_cast<const float4*>(b0 + idx);
+      for (int s = 1; s < splits; ++s) {
+        const float4 x = *reinterpret_cast<const float4*>(b0 + s * b_stride + idx);
+        a4.x += x.x;
+        a4.y += x.y;
+        a4.z += x.z;
+        a4.w += x.w;
+      }
+      *reinterpret_cast<float4*>(b0 + idx) = a4;
+    }
+  }
+
+  switch (wave) {
+    case 0: invert_rows<DK, 0>(A_part, splits, part_stride, base, Inv, piv, lane); break;
+    case 1: invert_rows<DK, 1 % W>(A_part, splits, part_stride, base, Inv, piv, lane); break;
+    case 2: invert_rows<DK, 2 % W>(A_part, splits, part_stride, base, Inv, piv, lane); break;
+    default: invert_rows<DK, 3 % W>(A_part, splits, part_stride, base, Inv, piv, lane); break;
+  }
 }
 
 }  // namespace
@@ -178,15 +230,15 @@ hipError_t launch_frame_inverse(const float* A_part, float* B_part, int splits, 
   const dim3 grid((unsigned)count);
   switch (d_k) {
     case 32:
-      hipLaunchKernelGGL(inverse_kernel<32>, grid, dim3(64), 0, stream, A_part, splits,
+      hipLaunchKernelGGL(inverse_kernel<32>, grid, dim3(64 * 2), 0, stream, A_part, splits,
                          part_stride, Inv, B_part, b_mat, b_stride);
       break;
     case 64:
-      hipLaunchKernelGGL(inverse_kernel<64>, grid, dim3(64), 0, stream, A_part, splits,
+      hipLaunchKernelGGL(inverse_kernel<64>, grid, dim3(64 * 4), 0, stream, A_part, splits,
                          part_stride, Inv, B_part, b_mat, b_stride);
       break;
     case 128:
-      hipLaunchKernelGGL(inverse_kernel<128>, grid, dim3(64), 0, stream, A_part, splits,
+      hipLaunchKernelGGL(inverse_kernel<128>, grid, dim3(64 * 4), 0, stream, A_part, splits,
                          part_stride, Inv, B_part, b_mat, b_stride);
       break;
     default:

@@ -56,7 +56,7 @@ void readout_bf16_kernel(const uint16_t* __restrict__ Q, const float* __restrict
           make_uint2(pack_bf16x2(a.x + b.x, a.y + b.y), pack_bf16x2(a.z + b.z, a.w + b.w));
     }
   }
-  __syncthreads();
+  lds_barrier();
 
   bf16x8 sop[MB][KB];
 #pragma unroll
@@ -167,13 +167,13 @@ void readout_f32_kernel(const float* __restrict__ Q, const float* __restrict__ S
   const int tok = tid >> 4;  // token within the group of 16
   const int part = tid & 15;
   for (int n0 = n_begin; n0 < n_end; n0 += 16) {
-    __syncthreads();
+    lds_barrier();
     for (int idx = tid; idx < 16 * DK; idx += kThreads) {
       const int e = idx / DK, c = idx % DK;
       const int n = n0 + e;
       qs[e][c] = n < n_end ? Q[((size_t)fh * N + n) * DK + c] : 0.f;
     }
-    __syncthreads();
+    lds_barrier();
     float o[VPT];
 #pragma unroll
     for (int m = 0; m < VPT; ++m) o[m] = 0.f;

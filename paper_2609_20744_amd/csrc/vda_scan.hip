@@ -11,7 +11,7 @@
 // wavefronts multiply the block by Inv_t, each producing d_k/64 16-column
 // slices.  Inv_t is symmetric ((I + A_t)^{-1} of a symmetric A_t), so the
 // k-th column slice a lane needs is read as a contiguous piece of row j of
-// Inv_t with 16-byte loads.  Inv_t and B_t of the next three frames are in
+// Inv_t with 16-byte loads.  Inv_t and B_t of the next two frames are in
 // flight in a register ring, so memory latency stays off the serial path,
 // which holds only the matrix product and two barriers.  Workgroups of one
 // chain are placed on one XCD so they share Inv_t in its L2.
@@ -47,6 +47,10 @@ void scan_kernel(const float* __restrict__ Inv, const float* __restrict__ Bm,
   constexpr int KL = DK / 4;         // k values per lane and slice
   constexpr int E = DK / 16;         // state elements per thread in the row-wise phase
   static_assert(E % 2 == 0, "float2 granularity");
+  // Row-wise accesses in 16-byte pieces where the row slice allows: fewer
+  // memory operations keep the prefetch ring within what the hardware's
+  // outstanding-load counter can track precisely.
+  constexpr int VW = E % 4 == 0 ? 4 : 2;
   __shared__ __align__(16) float xs[2][16 * XLD];
 
   const int nrb = DV / 16;
@@ -85,10 +89,12 @@ void scan_kernel(const float* __restrict__ Inv, const float* __restrict__ Bm,
     return EXACT_F32 ? lg * KL + s : (s / 8) * 32 + 8 * lg + (s % 8);
   };
 
-  // Operands of the next kPrefetch frames are in flight in a register ring
-  // (one workgroup per CU, so registers are plentiful): slot d holds frame
-  // step0 + d, refilled with frame step0 + d + kPrefetch once consumed.
-  constexpr int kPrefetch = 3;
+  // Operands of the next kPrefetch frames are in flight in a register ring:
+  // slot d holds frame step0 + d, refilled with frame step0 + d + kPrefetch
+  // once consumed.  A deeper ring no longer fits in the vector registers; the
+  // compiler then parks slots in accumulation registers and must wait for
+  // each load before copying it there, which drains the ring.
+  constexpr int kPrefetch = 2;
   float ops[kPrefetch][NBW][KL];
   float bs[kPrefetch][E];
   auto load_ops = [&](int step, float (&op)[NBW][KL], float (&bb)[E]) {
@@ -112,10 +118,18 @@ void scan_kernel(const float* __restrict__ Inv, const float* __restrict__ Bm,
     }
     const float* src = Bm + fh * mat_b + row_off;
 #pragma unroll
-    for (int e = 0; e < E; e += 2) {
-      const float2 x = *reinterpret_cast<const float2*>(src + e);
-      bb[e] = x.x;
-      bb[e + 1] = x.y;
+    for (int e = 0; e < E; e += VW) {
+      if constexpr (VW == 4) {
+        const float4 x = *reinterpret_cast<const float4*>(src + e);
+        bb[e] = x.x;
+        bb[e + 1] = x.y;
+        bb[e + 2] = x.z;
+        bb[e + 3] = x.w;
+      } else {
+        const float2 x = *reinterpret_cast<const float2*>(src + e);
+        bb[e] = x.x;
+        bb[e + 1] = x.y;
+      }
     }
   };
 
@@ -138,20 +152,32 @@ void scan_kernel(const float* __restrict__ Inv, const float* __restrict__ Bm,
       // Frame index within the head; past the end it is out of the buffer
       // range (>= F forward, negative and so huge as unsigned in reverse).
       const int frame = dir == 0 ? step : F - 1 - step;
-      __syncthreads();  // xs[cur] holds the entering state
+      lds_barrier();  // xs[cur] holds the entering state
       {
         float* x = &xs[cur][pr * XLD + pc];
         const uint32_t off = (uint32_t)((size_t)(unsigned)frame * mat_b + row_off) * 4u;
 #pragma unroll
-        for (int e = 0; e < E; e += 2) {
-          float2 v = *reinterpret_cast<float2*>(x + e);
-          store_b64(srsrc, off + e * 4u, make_uint2(__float_as_uint(v.x), __float_as_uint(v.y)));
-          v.x += bs[d][e];
-          v.y += bs[d][e + 1];
-          *reinterpret_cast<float2*>(x + e) = v;
+        for (int e = 0; e < E; e += VW) {
+          if constexpr (VW == 4) {
+            float4 v = *reinterpret_cast<float4*>(x + e);
+            store_b128(srsrc, off + e * 4u,
+                       u32x4{__float_as_uint(v.x), __float_as_uint(v.y), __float_as_uint(v.z),
+                             __float_as_uint(v.w)});
+            v.x += bs[d][e];
+            v.y += bs[d][e + 1];
+            v.z += bs[d][e + 2];
+            v.w += bs[d][e + 3];
+            *reinterpret_cast<float4*>(x + e) = v;
+          } else {
+            float2 v = *reinterpret_cast<float2*>(x + e);
+            store_b64(srsrc, off + e * 4u, make_uint2(__float_as_uint(v.x), __float_as_uint(v.y)));
+            v.x += bs[d][e];
+            v.y += bs[d][e + 1];
+            *reinterpret_cast<float2*>(x + e) = v;
+          }
         }
       }
-      __syncthreads();
+      lds_barrier();
       if (NB >= 4 || wave < NB) {
         // A-operand: row li of the block at this lane's k indices.
         float a[KL];

@@ -164,9 +164,9 @@ void stats_bf16_kernel(const uint16_t* __restrict__ K, const uint16_t* __restric
 
   // Consume one tile from the ring, then refill its slot with tile n_next.
   auto tile_step = [&](int n_next, u32x4 (&kr)[NKC], float (&kbv)[NKC], u32x4 (&vr)[NVC]) {
-    __syncthreads();  // previous tile's operand reads are done
+    lds_barrier();  // previous tile's operand reads are done
     store_tile(kr, kbv, vr);
-    __syncthreads();
+    lds_barrier();
     load_tile(n_next, kr, kbv, vr);
 #pragma unroll
     for (int ks = 0; ks < kStatsTile / 32; ++ks) {
@@ -245,7 +245,7 @@ void stats_f32_kernel(const float* __restrict__ K, const float* __restrict__ V,
   for (int m = 0; m < OPT; ++m) acc[m] = 0.f;
 
   for (int n0 = n_begin; n0 < n_end; n0 += T) {
-    __syncthreads();
+    lds_barrier();
     for (int idx = tid; idx < T * DX; idx += kThreads) {
       const int e = idx / DX, c = idx % DX;
       const int n = n0 + e;
@@ -255,7 +255,7 @@ void stats_f32_kernel(const float* __restrict__ K, const float* __restrict__ V,
       xs[e][c] = x;
       if (c < DK) ys[e][c] = n < n_end ? x * beta[(size_t)fh * N + n] : 0.f;
     }
-    __syncthreads();
+    lds_barrier();
     for (int e = 0; e < T; ++e) {
 #pragma unroll
       for (int m = 0; m < OPT; ++m) {

@@ -132,6 +132,39 @@ def test_scan_stage(V, dk, dv):
         assert np.all(Sf[:, 0].cpu().numpy() == 0) and np.all(Sr[:, -1].cpu().numpy() == 0)
 
 
+@pytest.mark.parametrize("dk,dv", [(64, 128), (128, 128)])
+def test_scan_many_workgroups_per_cu(V, dk, dv):
+    """Enough chains that several scan workgroups share a compute unit, where
+    waves drift apart and a missing wait before a barrier shows up as wrong,
+    run-to-run varying states.  Checked against the fp64 recurrence on the
+    same (fp32) Inv_t and B_t, and for bitwise repeatability."""
+    import torch
+    H, F = 40, 16
+    _log(f"scan many workgroups dk={dk} dv={dv} H={H} F={F}")
+    rng = np.random.default_rng(dk + dv)
+    G = rng.standard_normal((H, F, dk, dk)) / np.sqrt(dk)
+    Inv = np.linalg.inv(np.eye(dk) + G @ np.swapaxes(G, -1, -2))
+    Inv = (0.5 * (Inv + np.swapaxes(Inv, -1, -2))).astype(np.float32)
+    Bm = rng.standard_normal((H, F, dv, dk)).astype(np.float32)
+    I64, B64 = Inv.astype(np.float64), Bm.astype(np.float64)
+    P_exp = np.zeros((H, F, dv, dk))
+    R_exp = np.zeros((H, F, dv, dk))
+    for t in range(1, F):
+        P_exp[:, t] = (P_exp[:, t - 1] + B64[:, t - 1]) @ I64[:, t - 1]
+    for t in range(F - 2, -1, -1):
+        R_exp[:, t] = (R_exp[:, t + 1] + B64[:, t + 1]) @ I64[:, t + 1]
+    Id, Bd = to_device(Inv, "f32"), to_device(Bm, "f32")
+    for exact, tol in ((True, 1e-5), (False, 1e-4)):
+        Sf, Sr = V.state_scan(Id, Bd, exact_f32=exact)
+        Sf2, Sr2 = V.state_scan(Id, Bd, exact_f32=exact)
+        torch.cuda.synchronize()
+        assert torch.equal(Sf, Sf2) and torch.equal(Sr, Sr2)
+        ef = rel_max_err(Sf.double().cpu().numpy(), P_exp)
+        er = rel_max_err(Sr.double().cpu().numpy(), R_exp)
+        _log(f"  exact_f32={exact}: fwd {ef:.2e} rev {er:.2e}")
+        assert ef < tol and er < tol
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("dk,dv", DIMS)
 def test_readout_stage(V, dtype, dk, dv):
