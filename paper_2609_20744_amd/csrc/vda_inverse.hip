@@ -10,16 +10,17 @@
 // accumulator layout (block (i, j): lane (c, g) holds rows 4g..4g+3, column
 // c).  Block step kb:
 //   1. the owner of row kb inverts the pivot block D = M[kb][kb] by scalar
-//      Gauss-Jordan (rows and columns exchanged by cross-lane shuffles) and
-//      publishes D^{-1} and the pivot row P_j = M[kb][j] in LDS;
-//   2. every wave forms R_j = D^{-1} P_j (D^{-1} is symmetric, so it is its
-//      own A-operand) and, for its rows i != kb,
-//        M[i][j] -= M[i][kb] R_j,   M[i][kb] = -M[i][kb] D^{-1};
-//      the owner of row kb sets M[kb][j] = R_j, M[kb][kb] = D^{-1}.
+//      Gauss-Jordan and publishes D^{-1} and the pivot row P_j = M[kb][j]
+//      in LDS;
+//   2. for its rows i != kb every wave applies
+//        M[i][j] -= M[i][kb] D^{-1} P_j,   M[i][kb] = -M[i][kb] D^{-1},
+//      and the owner of row kb sets M[kb][j] = D^{-1} P_j, M[kb][kb] = D^{-1}.
 // After eliminating block columns 0..kb-1 the matrix is [[X, Y], [Z, S]]
 // with X and S symmetric and Z = -Y^T, so M[i][kb] is the transpose of the
-// published P_i, negated when i < kb: the A-operand a lane supplies at
-// k = 4g + s is element s of its own slot of P_i.  A block (i, j) with
+// published P_i, negated when i < kb, and M[i][kb] D^{-1} is (up to that
+// sign) the transpose of R_i = D^{-1} P_i.  The A-operands a lane supplies
+// at k = 4g + s are therefore element s of its own slot of P_i or R_i, and
+// each wave forms R_i only for its own rows.  A block (i, j) with
 // j > kb that step j will overwrite (i < kb, or i > j) is not updated:
 // about a third of the products are skipped.  The LDS pivot row is double
 // buffered, so each block step needs one barrier.  With several matrices'
@@ -38,29 +39,52 @@
 namespace vda {
 namespace {
 
-// Pivot block inverse: lane (li, lg) holds D[4lg + r][li] in d[r] on entry
-// and D^{-1} in the same layout on exit.  Hardware reciprocal refined by one
+// Pivot block inverse by scalar Gauss-Jordan: lane (li, lg) holds
+// D[4lg + r][li] in d[r] on entry and D^{-1} in the same layout on exit.
+// Every cross-lane move is a VALU operation, so a pivot costs no LDS round
+// trip: the pivot element comes from one lane (v_readlane), pivot row p
+// (held by lane group p/4) is copied to all four lane groups by a 16-lane
+// and a 32-lane row swap (v_permlane16_swap, v_permlane32_swap), and pivot
+// column p (held by lane p of every group) by a row broadcast (DPP
+// row_newbcast).  The reciprocal is the hardware estimate refined by one
 // Newton step (error <= 1 ulp); the IEEE division sequence would sit on the
 // serial path once per pivot.
-__device__ __forceinline__ void invert_pivot_block(float (&d)[4], int li, int lg) {
+template <int P>
+__device__ __forceinline__ float row_of_group(float x) {
+  constexpr int G = P >> 2;
+  const uint32_t u = __float_as_uint(x);
+  const auto t = __builtin_amdgcn_permlane16_swap(u, u, false, false);  // [r0 r0 r2 r2], [r1 r1 r3 r3]
+  const uint32_t y = (G & 1) ? t[1] : t[0];
+  const auto v = __builtin_amdgcn_permlane32_swap(y, y, false, false);  // lower / upper pair
+  return __uint_as_float((G & 2) ? v[1] : v[0]);
+}
+
+template <int P>
+__device__ __forceinline__ void pivot_step(float (&d)[4], int li, int lg) {
+  const float rowv = row_of_group<P>(d[P & 3]);                            // D[P][li]
+  float colv[4];
 #pragma unroll
-  for (int p = 0; p < 16; ++p) {
-    const float rowv = __shfl(d[p & 3], li + 16 * (p >> 2));   // D[p][li]
-    float colv[4];
+  for (int r = 0; r < 4; ++r)                                              // D[4lg+r][P]
+    colv[r] = __int_as_float(
+        __builtin_amdgcn_update_dpp(0, __float_as_int(d[r]), 0x150 + P, 0xf, 0xf, false));
+  const float piv = __int_as_float(
+      __builtin_amdgcn_readlane(__float_as_int(d[P & 3]), P + 16 * (P >> 2)));  // D[P][P]
+  float inv = __builtin_amdgcn_rcpf(piv);
+  inv = inv * fmaf(-piv, inv, 2.0f);
+  const float rs = rowv * inv;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) colv[r] = __shfl(d[r], p + 16 * lg);  // D[4lg+r][p]
-    const float piv = __shfl(rowv, p);                           // D[p][p]
-    float inv = __builtin_amdgcn_rcpf(piv);
-    inv = inv * fmaf(-piv, inv, 2.0f);
-    const float rs = rowv * inv;
+  for (int r = 0; r < 4; ++r) d[r] = fmaf(-colv[r], rs, d[r]);
+  if (lg == (P >> 2)) d[P & 3] = (li == P) ? inv : rs;                     // pivot row
+  if (li == P) {                                                           // pivot column
 #pragma unroll
-    for (int r = 0; r < 4; ++r) d[r] = fmaf(-colv[r], rs, d[r]);
-    if (lg == (p >> 2)) d[p & 3] = (li == p) ? inv : rs;          // pivot row
-    if (li == p) {                                               // pivot column
-#pragma unroll
-      for (int r = 0; r < 4; ++r) d[r] = (4 * lg + r == p) ? inv : -colv[r] * inv;
-    }
+    for (int r = 0; r < 4; ++r) d[r] = (4 * lg + r == P) ? inv : -colv[r] * inv;
   }
+}
+
+template <int P = 0>
+__device__ __forceinline__ void invert_pivot_block(float (&d)[4], int li, int lg) {
+  pivot_step<P>(d, li, lg);
+  if constexpr (P + 1 < 16) invert_pivot_block<P + 1>(d, li, lg);
 }
 
 // The elimination for the block rows of wave WV (rows WV, WV + W, ...); a
@@ -120,7 +144,8 @@ __device__ __forceinline__ void invert_rows(const float* A_part, int splits, siz
     }
     lds_barrier();
 
-    // 2. R_j = D^{-1} P_j; A-operand D^{-1}[li][4lg+s] = d[s] (symmetric).
+    // D^{-1}: accumulator layout, and (being symmetric) its own A-operand
+    // D^{-1}[li][4lg+s] = d[s].
     float d[4];
     {
       const float4 v = *reinterpret_cast<const float4*>(pb + (kb * 64 + lane) * 4);
@@ -129,44 +154,52 @@ __device__ __forceinline__ void invert_rows(const float* A_part, int splits, siz
       d[2] = v.z;
       d[3] = v.w;
     }
-    floatx4 R[NB];
-#pragma unroll
-    for (int j = 0; j < NB; ++j) {
-      R[j] = floatx4{0.f, 0.f, 0.f, 0.f};
-      if (j == kb) continue;
-      const float4 p = *reinterpret_cast<const float4*>(pb + (j * 64 + lane) * 4);
-      R[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(d[0], p.x, R[j], 0, 0, 0);
-      R[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(d[1], p.y, R[j], 0, 0, 0);
-      R[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(d[2], p.z, R[j], 0, 0, 0);
-      R[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(d[3], p.w, R[j], 0, 0, 0);
-    }
-
 #pragma unroll
     for (int q = 0; q < RPW; ++q) {
       const int i = WV + W * q;
       if (i == kb) {
-        // 4. pivot row.
-#pragma unroll
-        for (int j = 0; j < NB; ++j)
-          acc[q][j] = j == kb ? floatx4{d[0], d[1], d[2], d[3]} : R[j];
-        continue;
-      }
-      // 3. A-operand of -M[i][kb] at k = 4lg + s, from P_i = M[kb][i]:
-      //    i > kb: -P_i[s];  i < kb: +P_i[s].
-      const float4 p = *reinterpret_cast<const float4*>(pb + (i * 64 + lane) * 4);
-      const float sg = i > kb ? -1.0f : 1.0f;
-      const float a[4] = {sg * p.x, sg * p.y, sg * p.z, sg * p.w};
-      floatx4 o = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int s = 0; s < 4; ++s) {
+        // 4. pivot row: M[kb][j] = D^{-1} P_j from this wave's own P_j.
 #pragma unroll
         for (int j = 0; j < NB; ++j) {
-          // Block (i, j), j > kb, is overwritten at step j (from the pivot
-          // row's transpose) unless kb < i <= j: skip those dead updates.
-          if (j == kb || (j > kb && (i > j || i < kb))) continue;
-          acc[q][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[s], R[j][s], acc[q][j], 0, 0, 0);
+          if (j == kb) continue;
+          const floatx4 pj = acc[q][j];
+          floatx4 r = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int s = 0; s < 4; ++s) r = __builtin_amdgcn_mfma_f32_16x16x4f32(d[s], pj[s], r, 0, 0, 0);
+          acc[q][j] = r;
         }
-        o = __builtin_amdgcn_mfma_f32_16x16x4f32(a[s], d[s], o, 0, 0, 0);
+        acc[q][kb] = floatx4{d[0], d[1], d[2], d[3]};
+        continue;
+      }
+      // 3. Row i != kb.  With sigma = +1 for i > kb and -1 for i < kb,
+      //    M[i][kb] = sigma P_i^T, so C_i = M[i][kb] D^{-1} = sigma R_i^T with
+      //    R_i = D^{-1} P_i, and
+      //      M[i][j] -= C_i P_j  (j != kb),   M[i][kb] = -C_i.
+      //    A-operands at k = 4lg + s: -M[i][kb] -> -sigma P_i[s] and
+      //    -C_i -> -sigma R_i[s]; B-operands P_j[s] and D^{-1}: d[s].
+      const float4 p4 = *reinterpret_cast<const float4*>(pb + (i * 64 + lane) * 4);
+      const float pi[4] = {p4.x, p4.y, p4.z, p4.w};
+      const float ms = i > kb ? -1.0f : 1.0f;  // -sigma
+      floatx4 o = {0.f, 0.f, 0.f, 0.f};
+      floatx4 ri = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < 4; ++s) {
+        o = __builtin_amdgcn_mfma_f32_16x16x4f32(ms * pi[s], d[s], o, 0, 0, 0);
+        ri = __builtin_amdgcn_mfma_f32_16x16x4f32(d[s], pi[s], ri, 0, 0, 0);
+      }
+      float c[4];
+#pragma unroll
+      for (int s = 0; s < 4; ++s) c[s] = ms * ri[s];
+#pragma unroll
+      for (int j = 0; j < NB; ++j) {
+        // Block (i, j), j > kb, is overwritten at step j (from the pivot
+        // row's transpose) unless kb < i <= j: skip those dead updates.
+        if (j == kb || (j > kb && (i > j || i < kb))) continue;
+        const float4 pj = *reinterpret_cast<const float4*>(pb + (j * 64 + lane) * 4);
+        acc[q][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(c[0], pj.x, acc[q][j], 0, 0, 0);
+        acc[q][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(c[1], pj.y, acc[q][j], 0, 0, 0);
+        acc[q][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(c[2], pj.z, acc[q][j], 0, 0, 0);
+        acc[q][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(c[3], pj.w, acc[q][j], 0, 0, 0);
       }
       acc[q][kb] = o;
     }
