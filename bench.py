@@ -5,11 +5,12 @@
 
 A step is one whole forward pass (frame statistics, inverse, both scans,
 readout + RMSNorm + gate) over the workload's synthetic inputs, which are
-resident in HBM before timing starts.  The timed region runs K steps through
-the library's stage entry points (the same kernels and launch configuration
-as vda_forward) with HIP events between the stages on the launch stream, so
-each kernel's average duration is measured live; vda_forward itself is timed
-in a second region as a cross-check.  Prints one JSON line.
+resident in HBM before timing starts.  The first timed region runs K steps of
+the library's forward entry point (the value reported).  A second timed
+region runs the same kernel launches (same head ranges and splits) through
+the stage entry points with HIP events around each launch on the launch
+stream, so each kernel's average launch duration is measured live (for the
+roofline).  Prints one JSON line.
 """
 from __future__ import annotations
 
@@ -42,16 +43,24 @@ def bytes_alg(w) -> float:
     return w.heads * w.F * w.N * (e * (2 * w.d_k + w.d_v) + e * w.d_v + 4) + 4 * w.heads
 
 
-def kernel_bytes(w):
-    """Algorithmic bytes per launch of each kernel: what it must read and
-    write once (its inputs and its outputs), without split partials."""
+def head_groups(H: int):
+    """Head ranges of the forward pass's launches: one launch of each kernel
+    over all heads, as the library schedules them."""
+    return [(0, H)]
+
+
+def kernel_bytes(w, heads=None):
+    """Algorithmic bytes per launch of each kernel over `heads` heads (default:
+    all): what it must read and write once (its inputs and its outputs),
+    without split partials."""
     e = 4 if w.dtype == "f32" else 2
-    fh, N, dk, dv = w.frame_heads, w.N, w.d_k, w.d_v
+    heads = w.heads if heads is None else heads
+    fh, N, dk, dv = heads * w.F, w.N, w.d_k, w.d_v
     return {
         "frame_stats": fh * (N * (e * (dk + dv) + 4) + 4 * (dk * dk + dv * dk)),
         "frame_inverse": fh * 8 * dk * dk,
         "state_scan": fh * 2 * (4 * dk * dk + 4 * dv * dk + 4 * dv * dk),
-        "readout": fh * (N * e * (dk + dv) + 8 * dv * dk) + 4 * w.heads,
+        "readout": fh * (N * e * (dk + dv) + 8 * dv * dk) + 4 * heads,
     }
 
 
@@ -232,75 +241,82 @@ def main() -> int:
     beta, gate = dev(x["beta"], "f32"), dev(x["gate"], "f32")
     del x
     H, F, N, dk, dv = w.heads, w.F, w.N, w.d_k, w.d_v
-    splits = vda.default_splits(F, N, H)
-    A_part = torch.empty((splits, H, F, dk, dk), dtype=torch.float32, device="cuda")
-    B_part = torch.empty((splits, H, F, dv, dk), dtype=torch.float32, device="cuda")
-    S_fwd = torch.empty((H, F, dv, dk), dtype=torch.float32, device="cuda")
-    S_rev = torch.empty((H, F, dv, dk), dtype=torch.float32, device="cuda")
     out = torch.empty((H, F, N, dv), dtype=q.dtype, device="cuda")
-    Inv = A_part[0]
+    K = args.steps
 
-    names = ["frame_stats", "frame_inverse", "state_scan", "readout"]
-
-    def step(evs=None):
-        vda.frame_stats(k, v, beta, splits=splits, A_part=A_part, B_part=B_part)
-        if evs is not None:
-            evs[1].record()
-        vda.frame_inverse(A_part, B_part, Inv=Inv)
-        if evs is not None:
-            evs[2].record()
-        vda.state_scan(Inv, B_part[0], S_fwd, S_rev, exact_f32=(w.dtype == "f32"))
-        if evs is not None:
-            evs[3].record()
-        vda.readout(q, S_fwd, S_rev, gate, out=out)
-        if evs is not None:
-            evs[4].record()
-
+    # 1. The headline: the library's forward entry point.
     print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
     for _ in range(args.warmup):
-        step()
+        vda.forward(q, k, v, beta, gate, out=out)
     torch.cuda.synchronize()
-
-    K = args.steps
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(K)]
-    t_start = torch.cuda.Event(enable_timing=True)
-    t_end = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
+    fev = [torch.cuda.Event(enable_timing=True) for _ in range(K + 1)]
     wall0 = time.perf_counter()
-    t_start.record()
+    fev[0].record()
     for i in range(K):
-        evs[i][0].record()
-        step(evs[i])
-    t_end.record()
+        vda.forward(q, k, v, beta, gate, out=out)
+        fev[i + 1].record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
-    total_ms = t_start.elapsed_time(t_end)
-    ms = total_ms / K
-    per_kernel = {n: sum(evs[i][j].elapsed_time(evs[i][j + 1]) for i in range(K)) / K
-                  for j, n in enumerate(names)}
-    step_ms = sorted(evs[i][0].elapsed_time(evs[i][4]) for i in range(K))
+    ms = fev[0].elapsed_time(fev[K]) / K
+    step_ms = sorted(fev[i].elapsed_time(fev[i + 1]) for i in range(K))
     pct = lambda p: step_ms[min(K - 1, int(p * (K - 1) + 0.5))]
-    print(f"[bench] timed {K} steps: {ms:.4f} ms/step", file=sys.stderr, flush=True)
+    print(f"[bench] timed {K} forward steps: {ms:.4f} ms/step", file=sys.stderr, flush=True)
 
-    # Cross-check: the all-in-one entry point over the same number of steps.
+    # 2. Per-kernel durations: the same launches (same head ranges and splits)
+    #    through the stage entry points on one stream, HIP events around every
+    #    launch.
+    names = ["frame_stats", "frame_inverse", "state_scan", "readout"]
+    groups = head_groups(H)
+    bufs = []
+    for h0, h1 in groups:
+        Hg = h1 - h0
+        sp = vda.default_splits(F, N, Hg)
+        A_part = torch.empty((sp, Hg, F, dk, dk), dtype=torch.float32, device="cuda")
+        B_part = torch.empty((sp, Hg, F, dv, dk), dtype=torch.float32, device="cuda")
+        S_fwd = torch.empty((Hg, F, dv, dk), dtype=torch.float32, device="cuda")
+        S_rev = torch.empty((Hg, F, dv, dk), dtype=torch.float32, device="cuda")
+        bufs.append((slice(h0, h1), sp, A_part, B_part, S_fwd, S_rev))
+
+    def staged(evs=None):
+        j = 0
+        for sl, sp, A_part, B_part, S_fwd, S_rev in bufs:
+            launches = (
+                lambda: vda.frame_stats(k[sl], v[sl], beta[sl], splits=sp, A_part=A_part, B_part=B_part),
+                lambda: vda.frame_inverse(A_part, B_part, Inv=A_part[0]),
+                lambda: vda.state_scan(A_part[0], B_part[0], S_fwd, S_rev,
+                                       exact_f32=(w.dtype == "f32")),
+                lambda: vda.readout(q[sl], S_fwd, S_rev, gate[sl], out=out[sl]),
+            )
+            for fn in launches:
+                fn()
+                if evs is not None:
+                    evs[j + 1].record()
+                j += 1
+
     for _ in range(2):
-        vda.forward(q, k, v, beta, gate, out=out)
+        staged()
     torch.cuda.synchronize()
-    f0 = torch.cuda.Event(enable_timing=True)
-    f1 = torch.cuda.Event(enable_timing=True)
-    f0.record()
-    for _ in range(K):
-        vda.forward(q, k, v, beta, gate, out=out)
-    f1.record()
+    nl = 4 * len(groups)
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(nl + 1)] for _ in range(K)]
+    for i in range(K):
+        evs[i][0].record()
+        staged(evs[i])
     torch.cuda.synchronize()
-    fused_ms = f0.elapsed_time(f1) / K
+    launch_ms = {n: [] for n in names}
+    for i in range(K):
+        for j in range(nl):
+            launch_ms[names[j % 4]].append(evs[i][j].elapsed_time(evs[i][j + 1]))
+    per_launch = {n: sum(v_) / len(v_) for n, v_ in launch_ms.items()}
+    staged_ms = sum(evs[i][0].elapsed_time(evs[i][nl]) for i in range(K)) / K
 
     t = ms / 1e3
     tflops = flops_alg(w) / t / 1e12
     gbs = bytes_alg(w) / t / 1e9
-    kb = kernel_bytes(w)
-    dominant = max(("frame_stats", "readout"), key=lambda n: per_kernel[n])
-    ach = kb[dominant] / (per_kernel[dominant] / 1e3) / 1e9
+    # Per-launch algorithmic bytes (mean over the launches timed).
+    kb = {n: sum(kernel_bytes(w, h1 - h0)[n] for h0, h1 in groups) / len(groups) for n in names}
+    dominant = max(("frame_stats", "readout"), key=lambda n: per_launch[n])
+    ach = kb[dominant] / (per_launch[dominant] / 1e3) / 1e9
+    splits = [b[1] for b in bufs]
     result = {
         "metric": METRIC,
         "value": w.tokens / t,
@@ -315,15 +331,17 @@ def main() -> int:
         "dtype": "bf16" if w.dtype == "bf16" else "f32",
         "data": "synthetic (seeded; L2-normalised q,k; sigmoid write strengths and gates)",
         "config": {"workload": w.name, "B": w.B, "H": w.H, "F": F, "N": N, "d_k": dk, "d_v": dv,
-                   "storage": w.dtype, "state": "fp32", "splits": splits},
+                   "storage": w.dtype, "state": "fp32", "head_groups": len(groups),
+                   "splits": splits},
         "tflops": tflops,
         "pct_bf16_mfma_peak": 100.0 * tflops / PEAK_BF16_TFLOPS,
         "hbm_gbs_alg": gbs,
         "pct_hbm_peak": 100.0 * gbs / PEAK_HBM_GBS,
         "token_heads_per_s": w.tokens * w.H / t,
         "step_ms_p10_p50_p90": [pct(0.1), pct(0.5), pct(0.9)],
-        "kernel_ms": per_kernel,
-        "forward_entry_ms_per_step": fused_ms,
+        "kernel_ms_per_launch": per_launch,
+        "kernel_launches_per_step": len(groups),
+        "staged_ms_per_step": staged_ms,
         "wall_s_timed_region": wall,
         "roofline": {"bound": "hbm", "kernel": dominant, "achieved": ach, "peak": PEAK_HBM_GBS,
                      "unit": "GB/s", "frac": ach / PEAK_HBM_GBS,

@@ -313,28 +313,55 @@ def test_deterministic_and_guarded(V):
     assert torch.equal(y1.view(torch.int16), y2.view(torch.int16))
 
 
+def _staged_forward(V, d, exact_f32):
+    """The forward pass through the stage entry points, with the library's
+    default split of the statistics step."""
+    A_part, B_part = V.frame_stats(d["k"], d["v"], d["beta"])
+    Inv = V.frame_inverse(A_part, B_part, Inv=A_part[0])
+    Sf, Sr = V.state_scan(Inv, B_part[0], exact_f32=exact_f32)
+    return V.readout(d["q"], Sf, Sr, d["gate"]), A_part.shape[0]
+
+
 def test_stages_compose_to_forward(V):
+    """vda_forward equals its stages run one after another."""
     import torch
     w = I.custom("compose", 1, 3, 5, 700, 128, 128, "bf16", seed=13)
-    x = I.make_inputs(w)
-    d = device_inputs(w, x)
+    d = device_inputs(w, I.make_inputs(w))
     y = V.forward(d["q"], d["k"], d["v"], d["beta"], d["gate"])
-    A_part, B_part = V.frame_stats(d["k"], d["v"], d["beta"])
-    assert A_part.shape[0] > 1          # exercises the split reduction
-    Inv = V.frame_inverse(A_part, B_part, Inv=A_part[0])
-    Sf, Sr = V.state_scan(Inv, B_part[0])
-    y2 = V.readout(d["q"], Sf, Sr, d["gate"])
+    y2, splits = _staged_forward(V, d, exact_f32=False)
+    assert splits > 1                   # exercises the split reduction
     # the same for fp32 storage
     wf = I.custom("compose32", 1, 2, 4, 100, 64, 64, "f32", seed=14)
     df = device_inputs(wf, I.make_inputs(wf))
     yf = V.forward(df["q"], df["k"], df["v"], df["beta"], df["gate"])
-    Af, Bf = V.frame_stats(df["k"], df["v"], df["beta"])
-    Invf = V.frame_inverse(Af, Bf, Inv=Af[0])
-    Sff, Srf = V.state_scan(Invf, Bf[0], exact_f32=True)
-    yf2 = V.readout(df["q"], Sff, Srf, df["gate"])
+    yf2, _ = _staged_forward(V, df, exact_f32=True)
+    # one head: no grouping
+    w1 = I.custom("compose1", 1, 1, 3, 300, 64, 128, "bf16", seed=15)
+    d1 = device_inputs(w1, I.make_inputs(w1))
+    y1 = V.forward(d1["q"], d1["k"], d1["v"], d1["beta"], d1["gate"])
+    y12, _ = _staged_forward(V, d1, exact_f32=False)
     torch.cuda.synchronize()
     assert torch.equal(y.view(torch.int16), y2.view(torch.int16))
     assert torch.equal(yf, yf2)
+    assert torch.equal(y1.view(torch.int16), y12.view(torch.int16))
+
+
+def test_forward_on_many_streams(V):
+    """Calls issued on several streams at once (sharing the library's
+    workspace pool) each equal the single-stream result."""
+    import torch
+    w = I.custom("streams", 1, 4, 6, 500, 64, 128, "bf16", seed=17)
+    d = device_inputs(w, I.make_inputs(w))
+    ref = V.forward(d["q"], d["k"], d["v"], d["beta"], d["gate"])
+    torch.cuda.synchronize()
+    streams = [torch.cuda.Stream() for _ in range(3)]
+    outs = []
+    for s in streams:
+        with torch.cuda.stream(s):
+            outs.append(V.forward(d["q"], d["k"], d["v"], d["beta"], d["gate"]))
+    torch.cuda.synchronize()
+    for o in outs:
+        assert torch.equal(o.view(torch.int16), ref.view(torch.int16))
 
 
 def test_invalid_arguments_raise(V):
