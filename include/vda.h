@@ -36,7 +36,7 @@
  *    never synchronises.  Invalid arguments are reported before anything is
  *    enqueued.  A device fault surfaces at the caller's next synchronisation.
  *  - Calls keep no state between them except per-device cached properties
- *    and the workspace memory pool; they may be issued concurrently from
+ *    and cached workspace buffers; they may be issued concurrently from
  *    several threads on different streams.
  *  - Results are deterministic: no floating-point atomics are used.
  *  - No C++ exception crosses this interface.
@@ -76,8 +76,12 @@ const char* vda_status_string(int status);
  * Frame statistics and the readout run on bf16 matrix cores with fp32
  * accumulation; (I + A_t)^{-1}, the recurrent states and the epilogue are
  * fp32, and the state products use split-bf16 operands (see vda_state_scan).
- * Workspace (about H*F*(3*d_k*d_k + 4*d_v*d_k)*4 bytes) is taken from a
- * library-owned stream-ordered memory pool and released on `stream`.
+ * Workspace of H*F*(S*(d_k*d_k + d_v*d_k) + 2*d_v*d_k)*4 bytes, with
+ * S = vda_default_splits(F, N, H), comes from a per-device cache of
+ * library-owned device buffers: a buffer is reused by later calls on the
+ * same stream, or on another stream once the work of its last call has
+ * finished, and otherwise a new one is allocated (hipMalloc; VDA_ERR_NOMEM
+ * on failure).  Cached buffers are kept until the process ends.
  */
 int vda_forward(const void* q, const void* k, const void* v,
                 const float* beta, const float* gate,

@@ -4,6 +4,7 @@
 #include <string.h>
 
 #include <mutex>
+#include <vector>
 
 #include "../../include/vda.h"
 #include "vda_common.h"
@@ -54,27 +55,76 @@ int current_device_cus() {
   return cus[dev];
 }
 
-// Library-owned stream-ordered pool per device.  Freed blocks stay in the
-// pool (release threshold = max), so repeated calls do not remap memory.
-hipMemPool_t device_pool(int dev) {
-  static std::mutex mu;
-  static hipMemPool_t pools[kMaxDevices] = {nullptr};
-  if (dev < 0 || dev >= kMaxDevices) return nullptr;
-  std::lock_guard<std::mutex> lock(mu);
-  if (pools[dev] == nullptr) {
-    hipMemPoolProps props;
-    memset(&props, 0, sizeof(props));
-    props.allocType = hipMemAllocationTypePinned;
-    props.handleTypes = hipMemHandleTypeNone;
-    props.location.type = hipMemLocationTypeDevice;
-    props.location.id = dev;
-    hipMemPool_t pool = nullptr;
-    if (hipMemPoolCreate(&pool, &props) != hipSuccess) return nullptr;
-    uint64_t threshold = UINT64_MAX;
-    (void)hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &threshold);
-    pools[dev] = pool;
+// Library-owned workspace cache per device.  Buffers come from hipMalloc
+// and stay cached until the process ends (a free would synchronise the
+// device).  A buffer is reused by a later call on the same stream (stream
+// order makes that safe) or, on another stream, once the event recorded after
+// its last use has completed; between acquire and release it is marked busy
+// so concurrent host threads never share it.  (Stream-ordered pool
+// allocations were measured slower: a gap before every call and slower
+// kernels on the pool's memory.)
+struct WsEntry {
+  void* ptr = nullptr;
+  size_t bytes = 0;
+  hipStream_t stream = nullptr;
+  hipEvent_t done = nullptr;
+  bool busy = false;
+};
+
+struct WsCache {
+  std::mutex mu;
+  std::vector<WsEntry> entries;
+};
+
+WsCache& ws_cache(int dev) {
+  static WsCache caches[kMaxDevices];
+  return caches[dev];
+}
+
+// Returns the entry index, or -1 (allocation failure).
+int acquire_workspace(int dev, size_t bytes, hipStream_t stream) {
+  WsCache& c = ws_cache(dev);
+  std::lock_guard<std::mutex> lock(c.mu);
+  int pick = -1;
+  for (int pass = 0; pass < 2 && pick < 0; ++pass) {
+    for (size_t i = 0; i < c.entries.size(); ++i) {
+      WsEntry& e = c.entries[i];
+      if (e.busy || e.bytes < bytes) continue;
+      if (pass == 0 ? e.stream == stream : hipEventQuery(e.done) == hipSuccess) {
+        pick = (int)i;
+        break;
+      }
+    }
   }
-  return pools[dev];
+  if (pick < 0) {
+    WsEntry e;
+    if (hipMalloc(&e.ptr, bytes) != hipSuccess) return -1;
+    if (hipEventCreateWithFlags(&e.done, hipEventDisableTiming) != hipSuccess) {
+      (void)hipFree(e.ptr);
+      return -1;
+    }
+    e.bytes = bytes;
+    c.entries.push_back(e);
+    pick = (int)c.entries.size() - 1;
+  }
+  c.entries[pick].busy = true;
+  c.entries[pick].stream = stream;
+  return pick;
+}
+
+void* workspace_ptr(int dev, int idx) {
+  WsCache& c = ws_cache(dev);
+  std::lock_guard<std::mutex> lock(c.mu);
+  return c.entries[idx].ptr;
+}
+
+hipError_t release_workspace(int dev, int idx, hipStream_t stream) {
+  WsCache& c = ws_cache(dev);
+  std::lock_guard<std::mutex> lock(c.mu);
+  WsEntry& e = c.entries[idx];
+  const hipError_t r = hipEventRecord(e.done, stream);
+  e.busy = false;
+  return r;
 }
 
 int default_splits(int F, int N, int H) {
@@ -128,14 +178,12 @@ int forward_impl(bool is_f32, const void* q, const void* k, const void* v, const
     return VDA_ERR_OVERLAP;
 
   int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess) return VDA_ERR_HIP;
-  hipMemPool_t pool = device_pool(dev);
-  if (!pool) return VDA_ERR_HIP;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return VDA_ERR_HIP;
   const int splits = default_splits(F, N, H);
   const Workspace w = workspace_layout(F, H, d_k, d_v, splits);
-  void* ws = nullptr;
-  if (hipMallocFromPoolAsync(&ws, w.total, pool, stream) != hipSuccess || !ws) return VDA_ERR_NOMEM;
-  char* base = static_cast<char*>(ws);
+  const int wsi = acquire_workspace(dev, w.total, stream);
+  if (wsi < 0) return VDA_ERR_NOMEM;
+  char* base = static_cast<char*>(workspace_ptr(dev, wsi));
   float* A_part = reinterpret_cast<float*>(base + w.a_part);
   float* B_part = reinterpret_cast<float*>(base + w.b_part);
   float* S_fwd = reinterpret_cast<float*>(base + w.s_fwd);
@@ -150,7 +198,7 @@ int forward_impl(bool is_f32, const void* q, const void* k, const void* v, const
     e = vda::launch_state_scan(is_f32, Inv, B_part, F, H, d_k, d_v, S_fwd, S_rev, stream);
   if (e == hipSuccess)
     e = vda::launch_readout(is_f32, q, S_fwd, S_rev, gate, F, N, H, d_k, d_v, out, stream);
-  const hipError_t ef = hipFreeAsync(ws, stream);
+  const hipError_t ef = release_workspace(dev, wsi, stream);
   if (e != hipSuccess) return VDA_ERR_HIP;
   return hip_status(ef);
 }
