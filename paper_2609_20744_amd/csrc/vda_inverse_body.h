@@ -1,0 +1,261 @@
+// Device code of step a2, Inv_t = (I + A_t)^{-1} (Eq. 5).
+//
+// I + A_t is symmetric positive definite with every eigenvalue >= 1 (A_t is
+// a Gram matrix weighted by beta >= 0; Appendix A.1), so Gauss-Jordan
+// elimination needs no pivoting and every leading block is invertible.
+//
+// One workgroup inverts one d_k x d_k matrix in fp32 by blocked Gauss-Jordan
+// with 16 x 16 blocks on v_mfma_f32_16x16x4_f32.  Block rows are dealt out
+// to the waves (wave w owns rows w, w + W, ...), each held in MFMA
+// accumulator layout (block (i, j): lane (c, g) holds rows 4g..4g+3, column
+// c).  Block step kb:
+//   1. the owner of row kb inverts the pivot block D = M[kb][kb] by scalar
+//      Gauss-Jordan and publishes D^{-1} and the pivot row P_j = M[kb][j]
+//      in LDS;
+//   2. for its rows i != kb every wave applies
+//        M[i][j] -= M[i][kb] D^{-1} P_j,   M[i][kb] = -M[i][kb] D^{-1},
+//      and the owner of row kb sets M[kb][j] = D^{-1} P_j, M[kb][kb] = D^{-1}.
+// After eliminating block columns 0..kb-1 the matrix is [[X, Y], [Z, S]]
+// with X and S symmetric and Z = -Y^T, so M[i][kb] is the transpose of the
+// published P_i, negated when i < kb, and M[i][kb] D^{-1} is (up to that
+// sign) the transpose of R_i = D^{-1} P_i.  The A-operands a lane supplies
+// at k = 4g + s are therefore element s of its own slot of P_i or R_i, and
+// each wave forms R_i only for its own rows.  A block (i, j) with
+// j > kb that step j will overwrite (i < kb, or i > j) is not updated:
+// about a third of the products are skipped.  The LDS pivot row is double
+// buffered, so each block step needs one barrier.  With several matrices'
+// workgroups per SIMD, one wave's serial pivot work hides behind another's
+// products.
+// Both A_t and its inverse are symmetric, so the column segments of the
+// accumulator layout are loaded and stored as contiguous row segments of the
+// transposed block (the result is the transpose of the computed inverse,
+// which equals it up to rounding).
+// The token-split partials of A_t are summed in split order while loading
+// (fold_b_partials does the same for B_t).  All products and sums are fp32.
+#pragma once
+
+#include "vda_common.h"
+
+namespace vda {
+namespace inv {
+
+// Pivot block inverse by scalar Gauss-Jordan: lane (li, lg) holds
+// D[4lg + r][li] in d[r] on entry and D^{-1} in the same layout on exit.
+// Every cross-lane move is a VALU operation, so a pivot costs no LDS round
+// trip: the pivot element comes from one lane (v_readlane), pivot row p
+// (held by lane group p/4) is copied to all four lane groups by a 16-lane
+// and a 32-lane row swap (v_permlane16_swap, v_permlane32_swap), and pivot
+// column p (held by lane p of every group) by a row broadcast (DPP
+// row_newbcast).  The reciprocal is the hardware estimate refined by one
+// Newton step (error <= 1 ulp); the IEEE division sequence would sit on the
+// serial path once per pivot.
+template <int P>
+__device__ __forceinline__ float row_of_group(float x) {
+  constexpr int G = P >> 2;
+  const uint32_t u = __float_as_uint(x);
+  const auto t = __builtin_amdgcn_permlane16_swap(u, u, false, false);  // [r0 r0 r2 r2], [r1 r1 r3 r3]
+  const uint32_t y = (G & 1) ? t[1] : t[0];
+  const auto v = __builtin_amdgcn_permlane32_swap(y, y, false, false);  // lower / upper pair
+  return __uint_as_float((G & 2) ? v[1] : v[0]);
+}
+
+template <int P>
+__device__ __forceinline__ void pivot_step(float (&d)[4], int li, int lg) {
+  const float rowv = row_of_group<P>(d[P & 3]);                            // D[P][li]
+  float colv[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r)                                              // D[4lg+r][P]
+    colv[r] = __int_as_float(
+        __builtin_amdgcn_update_dpp(0, __float_as_int(d[r]), 0x150 + P, 0xf, 0xf, false));
+  const float piv = __int_as_float(
+      __builtin_amdgcn_readlane(__float_as_int(d[P & 3]), P + 16 * (P >> 2)));  // D[P][P]
+  float inv = __builtin_amdgcn_rcpf(piv);
+  inv = inv * fmaf(-piv, inv, 2.0f);
+  const float rs = rowv * inv;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) d[r] = fmaf(-colv[r], rs, d[r]);
+  if (lg == (P >> 2)) d[P & 3] = (li == P) ? inv : rs;                     // pivot row
+  if (li == P) {                                                           // pivot column
+#pragma unroll
+    for (int r = 0; r < 4; ++r) d[r] = (4 * lg + r == P) ? inv : -colv[r] * inv;
+  }
+}
+
+template <int P = 0>
+__device__ __forceinline__ void invert_pivot_block(float (&d)[4], int li, int lg) {
+  pivot_step<P>(d, li, lg);
+  if constexpr (P + 1 < 16) invert_pivot_block<P + 1>(d, li, lg);
+}
+
+// The elimination for the block rows of wave WV (rows WV, WV + W, ...); a
+// template on the wave so that every row-dependent condition is resolved at
+// compile time.  All W waves of the workgroup take the same NB barriers.
+template <int DK, int WV>
+__device__ __forceinline__ void invert_rows(const float* A_part, int splits, size_t part_stride,
+                                            size_t base, float* Inv, float (*piv)[DK / 16][64 * 4],
+                                            int lane) {
+  constexpr int NB = DK / 16;          // 16-wide blocks per side
+  constexpr int W = NB < 4 ? NB : 4;   // waves
+  constexpr int RPW = NB / W;          // block rows per wave
+  const int li = lane & 15;
+  const int lg = lane >> 4;
+
+  // acc[q][j]: block (i, j) with i = WV + W q.  Its accumulator holds the
+  // column segment M[16i + 4lg .. +3][16j + li]; A_t is symmetric, so it is
+  // read as the contiguous row segment M[16j + li][16i + 4lg .. +3] with
+  // 16-byte loads (and the result is written back the same way).
+  floatx4 acc[RPW][NB];
+#pragma unroll
+  for (int q = 0; q < RPW; ++q) {
+    const int i = WV + W * q;
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      floatx4 v = {0.f, 0.f, 0.f, 0.f};
+      for (int s = 0; s < splits; ++s) {
+        const float4 x = *reinterpret_cast<const float4*>(
+            A_part + s * part_stride + base + (size_t)(16 * j + li) * DK + 16 * i + 4 * lg);
+        v[0] += x.x;
+        v[1] += x.y;
+        v[2] += x.z;
+        v[3] += x.w;
+      }
+      if (i == j) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (4 * lg + r == li) v[r] += 1.0f;
+      }
+      acc[q][j] = v;
+    }
+  }
+
+#pragma unroll
+  for (int kb = 0; kb < NB; ++kb) {
+    float* pb = &piv[kb & 1][0][0];
+    // 1. The owner of row kb publishes D^{-1} (in slot kb) and P_j (j != kb).
+    if (kb % W == WV) {
+      const floatx4 dd = acc[kb / W][kb];
+      float d[4] = {dd[0], dd[1], dd[2], dd[3]};
+      invert_pivot_block(d, li, lg);
+#pragma unroll
+      for (int j = 0; j < NB; ++j) {
+        const floatx4 v = j == kb ? floatx4{d[0], d[1], d[2], d[3]} : acc[kb / W][j];
+        *reinterpret_cast<float4*>(pb + (j * 64 + lane) * 4) = make_float4(v[0], v[1], v[2], v[3]);
+      }
+    }
+    lds_barrier();
+
+    // D^{-1}: accumulator layout, and (being symmetric) its own A-operand
+    // D^{-1}[li][4lg+s] = d[s].
+    float d[4];
+    {
+      const float4 v = *reinterpret_cast<const float4*>(pb + (kb * 64 + lane) * 4);
+      d[0] = v.x;
+      d[1] = v.y;
+      d[2] = v.z;
+      d[3] = v.w;
+    }
+#pragma unroll
+    for (int q = 0; q < RPW; ++q) {
+      const int i = WV + W * q;
+      if (i == kb) {
+        // 4. pivot row: M[kb][j] = D^{-1} P_j from this wave's own P_j.
+#pragma unroll
+        for (int j = 0; j < NB; ++j) {
+          if (j == kb) continue;
+          const floatx4 pj = acc[q][j];
+          floatx4 r = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int s = 0; s < 4; ++s) r = __builtin_amdgcn_mfma_f32_16x16x4f32(d[s], pj[s], r, 0, 0, 0);
+          acc[q][j] = r;
+        }
+        acc[q][kb] = floatx4{d[0], d[1], d[2], d[3]};
+        continue;
+      }
+      // 3. Row i != kb.  With sigma = +1 for i > kb and -1 for i < kb,
+      //    M[i][kb] = sigma P_i^T, so C_i = M[i][kb] D^{-1} = sigma R_i^T with
+      //    R_i = D^{-1} P_i, and
+      //      M[i][j] -= C_i P_j  (j != kb),   M[i][kb] = -C_i.
+      //    A-operands at k = 4lg + s: -M[i][kb] -> -sigma P_i[s] and
+      //    -C_i -> -sigma R_i[s]; B-operands P_j[s] and D^{-1}: d[s].
+      const float4 p4 = *reinterpret_cast<const float4*>(pb + (i * 64 + lane) * 4);
+      const float pi[4] = {p4.x, p4.y, p4.z, p4.w};
+      const float ms = i > kb ? -1.0f : 1.0f;  // -sigma
+      floatx4 o = {0.f, 0.f, 0.f, 0.f};
+      floatx4 ri = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < 4; ++s) {
+        o = __builtin_amdgcn_mfma_f32_16x16x4f32(ms * pi[s], d[s], o, 0, 0, 0);
+        ri = __builtin_amdgcn_mfma_f32_16x16x4f32(d[s], pi[s], ri, 0, 0, 0);
+      }
+      float c[4];
+#pragma unroll
+      for (int s = 0; s < 4; ++s) c[s] = ms * ri[s];
+#pragma unroll
+      for (int j = 0; j < NB; ++j) {
+        // Block (i, j), j > kb, is overwritten at step j (from the pivot
+        // row's transpose) unless kb < i <= j: skip those dead updates.
+        if (j == kb || (j > kb && (i > j || i < kb))) continue;
+        const float4 pj = *reinterpret_cast<const float4*>(pb + (j * 64 + lane) * 4);
+        acc[q][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(c[0], pj.x, acc[q][j], 0, 0, 0);
+        acc[q][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(c[1], pj.y, acc[q][j], 0, 0, 0);
+        acc[q][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(c[2], pj.z, acc[q][j], 0, 0, 0);
+        acc[q][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(c[3], pj.w, acc[q][j], 0, 0, 0);
+      }
+      acc[q][kb] = o;
+    }
+  }
+
+#pragma unroll
+  for (int q = 0; q < RPW; ++q) {
+    const int i = WV + W * q;
+#pragma unroll
+    for (int j = 0; j < NB; ++j)
+      *reinterpret_cast<float4*>(Inv + base + (size_t)(16 * j + li) * DK + 16 * i + 4 * lg) =
+          make_float4(acc[q][j][0], acc[q][j][1], acc[q][j][2], acc[q][j][3]);
+  }
+}
+
+// Sum the token-split partials of B_t into the first one (in place); all
+// threads of the workgroup take part.
+__device__ __forceinline__ void fold_b_partials(float* b0, int splits, size_t b_mat, size_t b_stride,
+                                                int tid, int nthreads) {
+  for (size_t idx = (size_t)tid * 4; idx < b_mat; idx += (size_t)nthreads * 4) {
+    float4 a4 = *reinterpret_cast<const float4*>(b0 + idx);
+    for (int s = 1; s < splits; ++s) {
+      const float4 x = *reinterpret_cast<const float4*>(b0 + s * b_stride + idx);
+      a4.x += x.x;
+      a4.y += x.y;
+      a4.z += x.z;
+      a4.w += x.w;
+    }
+    *reinterpret_cast<float4*>(b0 + idx) = a4;
+  }
+}
+
+// Invert one matrix with the first min(4, d_k/16) waves of the workgroup
+// (any further waves only take part in the barriers); `piv` is
+// 2 * (d_k/16) * 256 floats of LDS.  The matrix is the sum of `splits`
+// partials at A_part + s * part_stride + base; the result goes to Inv + base
+// (which may alias the first partial).
+template <int DK>
+__device__ __forceinline__ void invert_matrix(const float* A_part, int splits, size_t part_stride,
+                                              size_t base, float* Inv, float* piv_lds, int tid) {
+  constexpr int NB = DK / 16;
+  constexpr int W = NB < 4 ? NB : 4;
+  auto piv = reinterpret_cast<float (*)[NB][64 * 4]>(piv_lds);
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  if (wave >= W) {  // a workgroup with more waves: the others only keep the barriers
+    for (int kb = 0; kb < NB; ++kb) lds_barrier();
+    return;
+  }
+  switch (wave) {
+    case 0: invert_rows<DK, 0>(A_part, splits, part_stride, base, Inv, piv, lane); break;
+    case 1: invert_rows<DK, 1 % W>(A_part, splits, part_stride, base, Inv, piv, lane); break;
+    case 2: invert_rows<DK, 2 % W>(A_part, splits, part_stride, base, Inv, piv, lane); break;
+    default: invert_rows<DK, 3 % W>(A_part, splits, part_stride, base, Inv, piv, lane); break;
+  }
+}
+
+}  // namespace inv
+}  // namespace vda
