@@ -28,7 +28,8 @@
  *                                 and give undefined results)
  *        gate      [H]           fp32, per-head output gate (already squashed)
  *    H counts independent head problems (batch folded in: H = B * heads).
- *  - Supported head dimensions: d_k, d_v in {32, 64, 128}.  F, N, H >= 1.
+ *  - Supported head dimensions: d_k, d_v in {32, 64, 128} for every entry
+ *    point, and also 16 for vda_forward / vda_forward_f32.  F, N, H >= 1.
  *  - q, k, v, out and the fp32 work buffers must be 16-byte aligned; beta and
  *    gate 4-byte aligned.  out must not overlap any input.
  *  - Every call is asynchronous on `stream` (0 = the null stream): it
@@ -56,7 +57,7 @@ typedef enum {
   VDA_OK = 0,
   VDA_ERR_NULL = 1,        /* a required pointer is NULL                      */
   VDA_ERR_SIZE = 2,        /* F, N, H or splits < 1, or sizes overflow limits */
-  VDA_ERR_UNSUPPORTED = 3, /* d_k or d_v not in {32, 64, 128}                 */
+  VDA_ERR_UNSUPPORTED = 3, /* d_k or d_v not a supported head dimension      */
   VDA_ERR_ALIGN = 4,       /* a pointer is not aligned as required            */
   VDA_ERR_OVERLAP = 5,     /* the output overlaps an input                    */
   VDA_ERR_HIP = 6,         /* the HIP runtime reported an error               */
@@ -82,6 +83,13 @@ const char* vda_status_string(int status);
  * same stream, or on another stream once the work of its last call has
  * finished, and otherwise a new one is allocated (hipMalloc; VDA_ERR_NOMEM
  * on failure).  Cached buffers are kept until the process ends.
+ * A 16-channel d_k or d_v is run as a 32-channel head whose extra channels
+ * are zero: q, k (and v) are copied into padded workspace buffers, zero
+ * channels leave A_t, B_t, the states and the readout unchanged, RMSNorm
+ * averages over the true d_v, and the padded output is copied back into
+ * out.  The workspace then also holds those padded copies (the formula above
+ * with 32 for the padded dimension, plus 2*H*F*N*32 elements of the storage
+ * type per padded dimension).
  */
 int vda_forward(const void* q, const void* k, const void* v,
                 const float* beta, const float* gate,

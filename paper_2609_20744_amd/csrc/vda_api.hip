@@ -16,6 +16,14 @@ constexpr int kMaxDevices = 64;
 
 bool supported_dim(int d) { return d == 32 || d == 64 || d == 128; }
 
+// The whole forward also takes 16-channel heads, run as zero-padded 32-channel
+// heads (the stage entry points take only the kernels' own widths).
+bool forward_dim(int d) { return d == 16 || supported_dim(d); }
+
+int padded_dim(int d) { return d < 32 ? 32 : d; }
+
+size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
 struct Range {
@@ -31,12 +39,15 @@ bool overlaps(Range a, Range b) { return a.lo < b.hi && b.lo < a.hi; }
 
 // Shape checks shared by every entry point.  Grids are one-dimensional with
 // one workgroup per (frame, head, split/chunk), so H*F*64 must fit 31 bits.
-int check_shape(int F, int N, int H, int d_k, int d_v) {
+int check_shape(int F, int N, int H, int d_k, int d_v, bool forward = false) {
   if (F < 1 || N < 1 || H < 1) return VDA_ERR_SIZE;
-  if (!supported_dim(d_k) || !supported_dim(d_v)) return VDA_ERR_UNSUPPORTED;
+  if (forward ? !(forward_dim(d_k) && forward_dim(d_v))
+              : !(supported_dim(d_k) && supported_dim(d_v)))
+    return VDA_ERR_UNSUPPORTED;
   if ((long long)H * F * 64 > 0x7fffffffLL) return VDA_ERR_SIZE;
   // Byte offsets within one frame of one head are 32-bit.
-  if ((long long)N * (d_k > d_v ? d_k : d_v) * 4 > 0x7fffffffLL) return VDA_ERR_SIZE;
+  const int dmax = padded_dim(d_k > d_v ? d_k : d_v);
+  if ((long long)N * dmax * 4 > 0x7fffffffLL) return VDA_ERR_SIZE;
   return VDA_OK;
 }
 
@@ -164,7 +175,7 @@ int forward_impl(bool is_f32, const void* q, const void* k, const void* v, const
                  const float* gate, int F, int N, int H, int d_k, int d_v, void* out,
                  hipStream_t stream) {
   if (!q || !k || !v || !beta || !gate || !out) return VDA_ERR_NULL;
-  int st = check_shape(F, N, H, d_k, d_v);
+  int st = check_shape(F, N, H, d_k, d_v, true);
   if (st != VDA_OK) return st;
   if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 16) ||
       !aligned(beta, 4) || !aligned(gate, 4))
@@ -180,8 +191,14 @@ int forward_impl(bool is_f32, const void* q, const void* k, const void* v, const
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return VDA_ERR_HIP;
   const int splits = default_splits(F, N, H);
-  const Workspace w = workspace_layout(F, H, d_k, d_v, splits);
-  const int wsi = acquire_workspace(dev, w.total, stream);
+  // Heads narrower than 32 channels run as zero-padded 32-channel heads; the
+  // padded q, k, v and output live after the state buffers.
+  const int pk = padded_dim(d_k), pv = padded_dim(d_v);
+  const Workspace w = workspace_layout(F, H, pk, pv, splits);
+  const size_t qk_pad = pk != d_k ? round_up(tok * pk * es, 256) : 0;
+  const size_t v_pad = pv != d_v ? round_up(tok * pv * es, 256) : 0;
+  const size_t ws_bytes = round_up(w.total, 256) + 2 * qk_pad + 2 * v_pad;
+  const int wsi = acquire_workspace(dev, ws_bytes, stream);
   if (wsi < 0) return VDA_ERR_NOMEM;
   char* base = static_cast<char*>(workspace_ptr(dev, wsi));
   float* A_part = reinterpret_cast<float*>(base + w.a_part);
@@ -189,15 +206,39 @@ int forward_impl(bool is_f32, const void* q, const void* k, const void* v, const
   float* S_fwd = reinterpret_cast<float*>(base + w.s_fwd);
   float* S_rev = reinterpret_cast<float*>(base + w.s_rev);
   float* Inv = A_part;  // the inverse overwrites the first partial
+  char* pad_base = base + round_up(w.total, 256);
+  const void* qx = q;
+  const void* kx = k;
+  const void* vx = v;
+  void* ox = out;
 
-  hipError_t e = vda::launch_frame_stats(is_f32, k, v, beta, F, N, H, d_k, d_v, splits, A_part,
-                                         B_part, stream);
+  hipError_t e = hipSuccess;
+  if (qk_pad) {
+    void* qp = pad_base;
+    void* kp = pad_base + qk_pad;
+    e = vda::launch_pad_rows(q, qp, (long long)tok, (int)(d_k * es), (int)(pk * es), stream);
+    if (e == hipSuccess)
+      e = vda::launch_pad_rows(k, kp, (long long)tok, (int)(d_k * es), (int)(pk * es), stream);
+    qx = qp;
+    kx = kp;
+  }
+  if (v_pad && e == hipSuccess) {
+    void* vp = pad_base + 2 * qk_pad;
+    e = vda::launch_pad_rows(v, vp, (long long)tok, (int)(d_v * es), (int)(pv * es), stream);
+    vx = vp;
+    ox = pad_base + 2 * qk_pad + v_pad;
+  }
   if (e == hipSuccess)
-    e = vda::launch_frame_inverse(A_part, B_part, splits, (long long)H * F, d_k, d_v, Inv, stream);
+    e = vda::launch_frame_stats(is_f32, kx, vx, beta, F, N, H, pk, pv, splits, A_part, B_part,
+                                stream);
   if (e == hipSuccess)
-    e = vda::launch_state_scan(is_f32, Inv, B_part, F, H, d_k, d_v, S_fwd, S_rev, stream);
+    e = vda::launch_frame_inverse(A_part, B_part, splits, (long long)H * F, pk, pv, Inv, stream);
   if (e == hipSuccess)
-    e = vda::launch_readout(is_f32, q, S_fwd, S_rev, gate, F, N, H, d_k, d_v, out, stream);
+    e = vda::launch_state_scan(is_f32, Inv, B_part, F, H, pk, pv, S_fwd, S_rev, stream);
+  if (e == hipSuccess)
+    e = vda::launch_readout(is_f32, qx, S_fwd, S_rev, gate, F, N, H, pk, pv, d_v, ox, stream);
+  if (e == hipSuccess && ox != out)
+    e = vda::launch_unpad_rows(ox, out, (long long)tok, (int)(pv * es), (int)(d_v * es), stream);
   const hipError_t ef = release_workspace(dev, wsi, stream);
   if (e != hipSuccess) return VDA_ERR_HIP;
   return hip_status(ef);
@@ -212,7 +253,8 @@ const char* vda_status_string(int status) {
     case VDA_OK: return "VDA_OK";
     case VDA_ERR_NULL: return "VDA_ERR_NULL: a required pointer is NULL";
     case VDA_ERR_SIZE: return "VDA_ERR_SIZE: a size is out of range";
-    case VDA_ERR_UNSUPPORTED: return "VDA_ERR_UNSUPPORTED: d_k and d_v must be 32, 64 or 128";
+    case VDA_ERR_UNSUPPORTED:
+      return "VDA_ERR_UNSUPPORTED: d_k and d_v must be 32, 64 or 128 (16 too for the forward)";
     case VDA_ERR_ALIGN: return "VDA_ERR_ALIGN: a pointer is misaligned";
     case VDA_ERR_OVERLAP: return "VDA_ERR_OVERLAP: the output overlaps an input";
     case VDA_ERR_HIP: return "VDA_ERR_HIP: the HIP runtime reported an error";
@@ -317,7 +359,7 @@ int vda_readout(const void* q, const float* S_fwd, const float* S_rev, const flo
       overlaps(ro, range_of(S_rev, fh * d_v * d_k * 4)) || overlaps(ro, range_of(gate, H * 4)))
     return VDA_ERR_OVERLAP;
   return hip_status(vda::launch_readout(is_f32 != 0, q, S_fwd, S_rev, gate, F, N, H, d_k, d_v,
-                                        out, stream));
+                                        d_v, out, stream));
 }
 
 }  // extern "C"

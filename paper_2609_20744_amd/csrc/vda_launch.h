@@ -21,9 +21,17 @@ hipError_t launch_state_scan(bool exact_f32, const float* Inv, const float* Bm, 
                              int d_k, int d_v, float* S_fwd, float* S_rev, hipStream_t stream);
 
 // Steps a5-a7, Eq. A.4 / 1a / 1c: gather, readout, RMSNorm and gate.
+// d_v_norm: the number of channels RMSNorm averages over (d_v, or fewer
+// when the trailing value channels are zero padding).
 hipError_t launch_readout(bool is_f32, const void* q, const float* S_fwd, const float* S_rev,
                           const float* gate, int F, int N, int H, int d_k, int d_v,
-                          void* out, hipStream_t stream);
+                          int d_v_norm, void* out, hipStream_t stream);
+
+// Row-wise channel padding (zero fill) and its inverse, in 16-byte pieces.
+hipError_t launch_pad_rows(const void* src, void* dst, long long rows, int src_bytes,
+                           int dst_bytes, hipStream_t stream);
+hipError_t launch_unpad_rows(const void* src, void* dst, long long rows, int src_bytes,
+                             int dst_bytes, hipStream_t stream);
 
 // Token count of each statistics split (a multiple of the 64-token tile).
 inline int stats_tokens_per_split(int N, int splits) {

@@ -23,7 +23,7 @@ __global__ __launch_bounds__(kThreads, 2)
 void readout_bf16_kernel(const uint16_t* __restrict__ Q, const float* __restrict__ S_fwd,
                          const float* __restrict__ S_rev, const float* __restrict__ gate,
                          int F, int N, int chunks, int tokens_per_chunk, unsigned nwg,
-                         uint16_t* __restrict__ out) {
+                         float inv_norm, uint16_t* __restrict__ out) {
   constexpr int SLD = DK + 8;  // bf16 row stride of S~ in LDS
   constexpr int MB = DV / 16;  // 16-row blocks of S~ (output channels)
   constexpr int KB = DK / 32;  // 32-wide k steps
@@ -46,9 +46,12 @@ void readout_bf16_kernel(const uint16_t* __restrict__ Q, const float* __restrict
   {
     const float* sf = S_fwd + (size_t)fh * (DV * DK);
     const float* sr = S_rev + (size_t)fh * (DV * DK);
-    // Fully unrolled, so all of a thread's loads are in flight together.
+    // Fully unrolled (a compile-time trip count; DV * DK is a multiple of
+    // kThreads * 4), so all of a thread's loads are in flight together.
+    static_assert((DV * DK) % (kThreads * 4) == 0, "state size");
 #pragma unroll
-    for (int idx = tid * 4; idx < DV * DK; idx += kThreads * 4) {
+    for (int it = 0; it < (DV * DK) / (kThreads * 4); ++it) {
+      const int idx = tid * 4 + it * (kThreads * 4);
       const float4 a = *reinterpret_cast<const float4*>(sf + idx);
       const float4 b = *reinterpret_cast<const float4*>(sr + idx);
       const int i = idx / DK, j = idx % DK;
@@ -117,7 +120,7 @@ void readout_bf16_kernel(const uint16_t* __restrict__ Q, const float* __restrict
         for (int i = 0; i < 4; ++i) ss = fmaf(acc[mb][i], acc[mb][i], ss);
       ss += __shfl_xor(ss, 16);
       ss += __shfl_xor(ss, 32);
-      const float scale = g / sqrtf(ss * (1.0f / DV) + kRmsEps);
+      const float scale = g / sqrtf(ss * inv_norm + kRmsEps);
       // 16-byte stores: for each pair of row blocks (2m, 2m+1), lane groups
       // 2p and 2p+1 (lanes l and l ^ 16) swap one 4-channel piece with
       // v_permlane16_swap, after which lane group 2p holds channels
@@ -146,7 +149,8 @@ template <int DK, int DV>
 __global__ __launch_bounds__(kThreads)
 void readout_f32_kernel(const float* __restrict__ Q, const float* __restrict__ S_fwd,
                         const float* __restrict__ S_rev, const float* __restrict__ gate,
-                        int F, int N, int chunks, int tokens_per_chunk, float* __restrict__ out) {
+                        int F, int N, int chunks, int tokens_per_chunk, float inv_norm,
+                        float* __restrict__ out) {
   constexpr int SLD = DK + 1;
   constexpr int VPT = DV / 16;  // output channels per thread
   __shared__ float st[DV * SLD];
@@ -187,7 +191,7 @@ void readout_f32_kernel(const float* __restrict__ Q, const float* __restrict__ S
     for (int m = 0; m < VPT; ++m) ss = fmaf(o[m], o[m], ss);
 #pragma unroll
     for (int off = 1; off < 16; off <<= 1) ss += __shfl_xor(ss, off);
-    const float scale = g / sqrtf(ss * (1.0f / DV) + kRmsEps);
+    const float scale = g / sqrtf(ss * inv_norm + kRmsEps);
     const int n = n0 + tok;
     if (n < n_end) {
 #pragma unroll
@@ -207,8 +211,9 @@ inline int readout_chunks(long long fh_count, int N) {
 
 template <int DK, int DV>
 hipError_t launch_readout_t(bool is_f32, const void* q, const float* S_fwd, const float* S_rev,
-                            const float* gate, int F, int N, int H, void* out,
+                            const float* gate, int F, int N, int H, int d_v_norm, void* out,
                             hipStream_t stream) {
+  const float inv_norm = 1.0f / (float)d_v_norm;
   const long long fh_count = (long long)H * F;
   const int chunks = readout_chunks(fh_count, N);
   int tpc = (N + chunks - 1) / chunks;
@@ -217,22 +222,23 @@ hipError_t launch_readout_t(bool is_f32, const void* q, const float* S_fwd, cons
   if (is_f32)
     hipLaunchKernelGGL((readout_f32_kernel<DK, DV>), grid, dim3(kThreads), 0, stream,
                        static_cast<const float*>(q), S_fwd, S_rev, gate, F, N, chunks, tpc,
-                       static_cast<float*>(out));
+                       inv_norm, static_cast<float*>(out));
   else
     hipLaunchKernelGGL((readout_bf16_kernel<DK, DV>), grid, dim3(kThreads), 0, stream,
                        static_cast<const uint16_t*>(q), S_fwd, S_rev, gate, F, N, chunks, tpc,
-                       (unsigned)(fh_count * chunks), static_cast<uint16_t*>(out));
+                       (unsigned)(fh_count * chunks), inv_norm, static_cast<uint16_t*>(out));
   return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_readout(bool is_f32, const void* q, const float* S_fwd, const float* S_rev,
-                          const float* gate, int F, int N, int H, int d_k, int d_v, void* out,
-                          hipStream_t stream) {
-#define VDA_READOUT_CASE(DKV, DVV) \
-  if (d_k == DKV && d_v == DVV)    \
-    return launch_readout_t<DKV, DVV>(is_f32, q, S_fwd, S_rev, gate, F, N, H, out, stream);
+                          const float* gate, int F, int N, int H, int d_k, int d_v, int d_v_norm,
+                          void* out, hipStream_t stream) {
+#define VDA_READOUT_CASE(DKV, DVV)                                                         \
+  if (d_k == DKV && d_v == DVV)                                                            \
+    return launch_readout_t<DKV, DVV>(is_f32, q, S_fwd, S_rev, gate, F, N, H, d_v_norm, out, \
+                                      stream);
   VDA_READOUT_CASE(32, 32) VDA_READOUT_CASE(32, 64) VDA_READOUT_CASE(32, 128)
   VDA_READOUT_CASE(64, 32) VDA_READOUT_CASE(64, 64) VDA_READOUT_CASE(64, 128)
   VDA_READOUT_CASE(128, 32) VDA_READOUT_CASE(128, 64) VDA_READOUT_CASE(128, 128)

@@ -45,7 +45,11 @@ def test_forward_validation():
     assert _fwd(**ok, H=-1) == 2
     assert _fwd(**ok, d_k=48) == 3
     assert _fwd(**ok, d_v=256) == 3
-    assert _fwd(**ok, d_k=16) == 3
+    assert _fwd(**ok, d_k=8) == 3
+    assert _fwd(**ok, d_v=24) == 3
+    # 16-channel heads pass the forward's shape check (padded to 32 inside);
+    # the output-overlap check still runs on the true sizes
+    assert _fwd(**{**ok, "out": 3 * big + 64}, d_k=16, d_v=16) == 5
     assert _fwd(**{**ok, "q": big + 8}) == 4
     assert _fwd(**{**ok, "beta": 4 * big + 2}) == 4
     # out overlapping v
@@ -76,6 +80,11 @@ def test_stage_validation():
     assert L.vda_state_scan(big, 2 * big, 4, 2, 64, 48, 0, 3 * big, 4 * big, None) == 3
     assert L.vda_readout(big, 2 * big, 3 * big, 4 * big, 4, 64, 2, 64, 64, 0, big, None) == 5
     assert L.vda_readout(big, 2 * big, 3 * big, None, 4, 64, 2, 64, 64, 0, 5 * big, None) == 1
+    # the stage entry points take only the kernels' own widths (no 16)
+    assert L.vda_frame_stats(big, 2 * big, 3 * big, 4, 64, 2, 16, 64, 1, 0, 4 * big, 5 * big, None) == 3
+    assert L.vda_frame_inverse(big, None, 1, 8, 16, 64, 2 * big, None) == 3
+    assert L.vda_state_scan(big, 2 * big, 4, 2, 64, 16, 0, 3 * big, 4 * big, None) == 3
+    assert L.vda_readout(big, 2 * big, 3 * big, 4 * big, 4, 64, 2, 64, 16, 0, 5 * big, None) == 3
 
 
 def test_single_hip_runtime_loaded():

@@ -256,6 +256,22 @@ def test_head_dims(V, dtype, dk, dv):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("dk,dv", [(16, 16), (16, 32), (16, 64), (16, 128), (32, 16), (64, 16),
+                                   (128, 16)])
+def test_narrow_head_dims(V, dtype, dk, dv):
+    # 16-channel heads run zero-padded to 32 channels inside vda_forward
+    _log(f"narrow dims dtype={dtype} dk={dk} dv={dv}")
+    _check_small(V, I.custom("narrow", 2, 1, 5, 150, dk, dv, dtype, seed=dk * 3 + dv))
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_narrow_head_dims_ragged(V, dtype):
+    _log(f"narrow ragged dtype={dtype}")
+    for N in (1, 17, 333):
+        _check_small(V, I.custom("narrow_ragged", 1, 3, 4, N, 16, 16, dtype, seed=N))
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("N", [1, 2, 15, 16, 17, 63, 64, 65, 129, 300])
 def test_ragged_tokens(V, dtype, N):
     _log(f"ragged N={N} dtype={dtype}")
