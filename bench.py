@@ -280,21 +280,26 @@ def main() -> int:
     bufs = []
     for h0, h1 in groups:
         Hg = h1 - h0
-        sp = vda.default_splits(F, N, Hg)
-        A_part = torch.empty((sp, Hg, F, dk, dk), dtype=torch.float32, device="cuda")
-        B_part = torch.empty((sp, Hg, F, dv, dk), dtype=torch.float32, device="cuda")
+        plan = vda.default_split_plan(F, N, Hg, dk, dv, w.dtype == "f32")
+        P = vda.partial_count(Hg * F, *plan)
+        A_part = torch.empty((P, dk, dk), dtype=torch.float32, device="cuda")
+        B_part = torch.empty((P, dv, dk), dtype=torch.float32, device="cuda")
         S_fwd = torch.empty((Hg, F, dv, dk), dtype=torch.float32, device="cuda")
         S_rev = torch.empty((Hg, F, dv, dk), dtype=torch.float32, device="cuda")
-        bufs.append((slice(h0, h1), sp, A_part, B_part, S_fwd, S_rev))
+        bufs.append((slice(h0, h1), plan, A_part, B_part, S_fwd, S_rev))
 
     def staged(evs=None):
         j = 0
-        for sl, sp, A_part, B_part, S_fwd, S_rev in bufs:
+        for sl, (tail, sp), A_part, B_part, S_fwd, S_rev in bufs:
+            c = S_fwd.shape[0] * F
+            Inv = A_part[:c]
             launches = (
-                lambda: vda.frame_stats(k[sl], v[sl], beta[sl], splits=sp, A_part=A_part, B_part=B_part),
-                lambda: vda.frame_inverse(A_part, B_part, Inv=A_part[0]),
-                lambda: vda.state_scan(A_part[0], B_part[0], S_fwd, S_rev,
-                                       exact_f32=(w.dtype == "f32")),
+                lambda: vda.frame_stats(k[sl], v[sl], beta[sl], splits=sp, tail_frames=tail,
+                                        A_part=A_part, B_part=B_part),
+                lambda: vda.frame_inverse(A_part, B_part, count=c, tail_frames=tail, splits=sp,
+                                          Inv=Inv),
+                lambda: vda.state_scan(Inv.view(-1, F, dk, dk), B_part[:c].view(-1, F, dv, dk),
+                                       S_fwd, S_rev, exact_f32=(w.dtype == "f32")),
                 lambda: vda.readout(q[sl], S_fwd, S_rev, gate[sl], out=out[sl]),
             )
             for fn in launches:
@@ -326,7 +331,7 @@ def main() -> int:
     kb = {n: sum(kernel_bytes(w, h1 - h0)[n] for h0, h1 in groups) / len(groups) for n in names}
     dominant = max(("frame_stats", "readout"), key=lambda n: per_launch[n])
     ach = kb[dominant] / (per_launch[dominant] / 1e3) / 1e9
-    splits = [b[1] for b in bufs]
+    plans = [{"tail_frames": b[1][0], "splits": b[1][1]} for b in bufs]
     result = {
         "metric": METRIC,
         "value": w.tokens / t,
@@ -342,7 +347,7 @@ def main() -> int:
         "data": "synthetic (seeded; L2-normalised q,k; sigmoid write strengths and gates)",
         "config": {"workload": w.name, "B": w.B, "H": w.H, "F": F, "N": N, "d_k": dk, "d_v": dv,
                    "storage": w.dtype, "state": "fp32", "head_groups": len(groups),
-                   "splits": splits},
+                   "split_plan": plans},
         "tflops": tflops,
         "pct_bf16_mfma_peak": 100.0 * tflops / PEAK_BF16_TFLOPS,
         "hbm_gbs_alg": gbs,

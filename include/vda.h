@@ -77,8 +77,9 @@ const char* vda_status_string(int status);
  * Frame statistics and the readout run on bf16 matrix cores with fp32
  * accumulation; (I + A_t)^{-1}, the recurrent states and the epilogue are
  * fp32, and the state products use split-bf16 operands (see vda_state_scan).
- * Workspace of H*F*(S*(d_k*d_k + d_v*d_k) + 2*d_v*d_k)*4 bytes, with
- * S = vda_default_splits(F, N, H), comes from a per-device cache of
+ * Workspace of (P*(d_k*d_k + d_v*d_k) + 2*H*F*d_v*d_k)*4 bytes, with
+ * P = H*F + T*(S-1) partials of the plan (T, S) = vda_default_split_plan(F,
+ * N, H, d_k, d_v, is_f32) (P = H*F when S == 1), comes from a per-device cache of
  * library-owned device buffers: a buffer is reused by later calls on the
  * same stream, or on another stream once the work of its last call has
  * finished, and otherwise a new one is allocated (hipMalloc; VDA_ERR_NOMEM
@@ -111,39 +112,60 @@ int vda_forward_f32(const float* q, const float* k, const float* v,
 /* ------------------------------------------------------------------------- */
 
 /*
- * vda_default_splits -- number of token ranges the frame-statistics step
- * splits each frame into on the current device (>= 1).  Each range yields one
- * partial A and B; the later steps add the partials in index order.
+ * Split plans.  The frame-statistics step may split frames into token
+ * ranges; each range yields one partial A and B, which the later steps add in
+ * range order.  A plan (tail_frames T, splits S) splits the last T of the
+ * count = H*F frames (frame index i = h*F + t) into S ranges each and leaves
+ * the others whole (S == 1: no frame is split; T is then ignored).  Range s of
+ * a split frame covers tokens [s*R, min(N, (s+1)*R)) with
+ * R = 64 * ceil(ceil(N / S) / 64).  Partials are stored as one array of
+ * count + T*(S-1) matrices (count when S == 1): matrix i holds frame i's
+ * first (or only) range, and range s >= 1 of split frame i is matrix
+ * i + s*T.
  */
-int vda_default_splits(int F, int N, int H);
 
 /*
- * vda_frame_stats -- step a1, Eq. 3b.  For split s covering tokens
- * [s*T, min(N, (s+1)*T)) with T = 64 * ceil(ceil(N / splits) / 64):
- *     A_part[s][h][t] = sum_u beta k k^T   (d_k x d_k, fp32)
- *     B_part[s][h][t] = sum_u beta v k^T   (d_v x d_k, fp32)
- * A_part is [splits][H][F][d_k][d_k], B_part is [splits][H][F][d_v][d_k].
+ * vda_default_split_plan -- the plan vda_forward uses on the current device
+ * for these sizes and storage type (is_f32 != 0: fp32).  Whole frames occupy
+ * the device in rounds; when the last round is partial its frames are split
+ * (at most 4 ranges of at least 256 tokens).  Writes *tail_frames and
+ * *splits.
+ */
+int vda_default_split_plan(int F, int N, int H, int d_k, int d_v, int is_f32,
+                           int* tail_frames, int* splits);
+
+/*
+ * vda_frame_stats -- step a1, Eq. 3b, under the split plan (tail_frames,
+ * splits).  For the token range of partial matrix m of frame i = h*F + t:
+ *     A_part[m] = sum_u beta k k^T   (d_k x d_k, fp32)
+ *     B_part[m] = sum_u beta v k^T   (d_v x d_k, fp32)
+ * A_part is [P][d_k][d_k] and B_part is [P][d_v][d_k] with
+ * P = H*F + tail_frames*(splits-1) (H*F when splits == 1).
  * k, v are bf16 (is_f32 == 0) or fp32 (is_f32 != 0).  With bf16 storage the
  * products beta * k are rounded to bf16 before the fp32-accumulated matrix
- * product; with fp32 storage everything is fp32.  splits must not exceed
- * ceil(N / 64).
+ * product, and only A's 16 x 16 blocks on and above the diagonal are
+ * computed (the blocks below are their transposes); with fp32 storage
+ * everything is fp32.  splits must not
+ * exceed ceil(N / 64); with splits > 1, 1 <= tail_frames <= H*F.
  */
 int vda_frame_stats(const void* k, const void* v, const float* beta,
-                    int F, int N, int H, int d_k, int d_v, int splits, int is_f32,
-                    float* A_part, float* B_part, hipStream_t stream);
+                    int F, int N, int H, int d_k, int d_v, int tail_frames, int splits,
+                    int is_f32, float* A_part, float* B_part, hipStream_t stream);
 
 /*
- * vda_frame_inverse -- step a2, Eq. 5: Inv[i] = (I + sum_s A_part[s][i])^{-1}
- * for i < count, in fp32 by blocked Gauss-Jordan elimination without
- * pivoting (I + A is symmetric positive definite with eigenvalues >= 1 when
- * beta >= 0).  Inv is [count][d_k][d_k].  Inv may alias A_part (in-place when
- * splits == 1, or onto the first partial); it must not overlap any other
- * partial.  When splits > 1 the call also folds the split partials of B in
- * place: B_part[0][i] = sum_s B_part[s][i] (B_part is [splits][count][d_v][d_k];
- * d_v and B_part are ignored when splits == 1), so the state scan reads one B.
+ * vda_frame_inverse -- step a2, Eq. 5: Inv[i] = (I + sum of frame i's A
+ * partials)^{-1} for i < count, under the split plan (tail_frames, splits)
+ * that produced the partials, in fp32 by blocked Gauss-Jordan elimination
+ * without pivoting (I + A is symmetric positive definite with eigenvalues
+ * >= 1 when beta >= 0).  Inv is [count][d_k][d_k].  Inv may alias A_part
+ * (in place onto the first count matrices); it must not overlap any other
+ * partial.  When splits > 1 the call also folds the partials of B in place
+ * (B_part[i] = sum of frame i's B partials; B_part as in vda_frame_stats;
+ * d_v and B_part are ignored when splits == 1), so the state scan reads B_part
+ * as [count][d_v][d_k].
  */
-int vda_frame_inverse(const float* A_part, float* B_part, int splits, int count,
-                      int d_k, int d_v, float* Inv, hipStream_t stream);
+int vda_frame_inverse(const float* A_part, float* B_part, int tail_frames, int splits,
+                      int count, int d_k, int d_v, float* Inv, hipStream_t stream);
 
 /*
  * vda_state_scan -- steps a3 and a4, Eq. A.1 and Algorithm 1 step 5 with a

@@ -3,6 +3,7 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <atomic>
 #include <mutex>
 #include <vector>
 
@@ -138,29 +139,50 @@ hipError_t release_workspace(int dev, int idx, hipStream_t stream) {
   return r;
 }
 
-int default_splits(int F, int N, int H) {
-  // The statistics step runs two workgroups (row halves) per frame and split;
-  // split the tokens only when that leaves fewer than about three workgroups
-  // per compute unit, and never below 256 tokens per split.  Splits cost a
-  // partial sum per split and a fold in the inverse step.
-  const long long wg_per_split = 2LL * H * F;
-  const long long target = 3LL * current_device_cus();
-  long long s = (target + wg_per_split - 1) / wg_per_split;
-  long long cap = N / 256;
-  if (cap < 1) cap = 1;
-  if (s > cap) s = cap;
-  if (s < 1) s = 1;
-  return (int)s;
+// Workgroups of the statistics kernel one compute unit holds at once, per
+// device, storage type and head dimensions (cached; 0 = not yet known).
+int stats_blocks_per_cu(int dev, bool is_f32, int d_k, int d_v) {
+  static std::atomic<int> cache[kMaxDevices][2][3][3];
+  auto idx = [](int d) { return d == 32 ? 0 : d == 64 ? 1 : 2; };
+  std::atomic<int>& c = cache[dev][is_f32 ? 1 : 0][idx(d_k)][idx(d_v)];
+  int n = c.load(std::memory_order_relaxed);
+  if (n == 0) {
+    n = vda::stats_blocks_per_cu(is_f32, d_k, d_v);
+    if (n < 1) n = 1;
+    c.store(n, std::memory_order_relaxed);
+  }
+  return n;
+}
+
+// Split plan of the statistics step.  Whole frames fill the device in
+// rounds of (resident workgroups) frames; when the last round is partial,
+// its frames are split into up to four token ranges (at least 256 tokens
+// each) so that the end of the launch keeps more compute units streaming.
+// Each extra range costs one partial A_t, B_t written here and read back by
+// the inverse step, which is why the split is kept small and limited to
+// the partial round.
+vda::SplitPlan default_plan(int dev, int F, int N, int H, int d_k, int d_v, bool is_f32) {
+  constexpr int kMaxSplits = 4;
+  const long long count = (long long)H * F;
+  const long long slots = (long long)stats_blocks_per_cu(dev, is_f32, d_k, d_v) * current_device_cus();
+  const long long rem = count % slots;
+  if (rem == 0) return vda::SplitPlan{0, 1};
+  long long k = slots / rem;
+  if (k > kMaxSplits) k = kMaxSplits;
+  if (k > N / 256) k = N / 256;
+  if (k < 2) return vda::SplitPlan{0, 1};
+  return vda::SplitPlan{(int)rem, (int)k};
 }
 
 struct Workspace {
   size_t a_part, b_part, s_fwd, s_rev, total;  // byte offsets / total
 };
 
-Workspace workspace_layout(int F, int H, int d_k, int d_v, int splits) {
+Workspace workspace_layout(int F, int H, int d_k, int d_v, vda::SplitPlan plan) {
   const size_t fh = (size_t)H * F;
-  const size_t a = (size_t)splits * fh * d_k * d_k * sizeof(float);
-  const size_t b = (size_t)splits * fh * d_v * d_k * sizeof(float);
+  const size_t parts = (size_t)vda::partial_count((long long)fh, plan);
+  const size_t a = parts * d_k * d_k * sizeof(float);
+  const size_t b = parts * d_v * d_k * sizeof(float);
   const size_t s = fh * d_v * d_k * sizeof(float);
   Workspace w;
   w.a_part = 0;
@@ -190,11 +212,11 @@ int forward_impl(bool is_f32, const void* q, const void* k, const void* v, const
 
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return VDA_ERR_HIP;
-  const int splits = default_splits(F, N, H);
   // Heads narrower than 32 channels run as zero-padded 32-channel heads; the
   // padded q, k, v and output live after the state buffers.
   const int pk = padded_dim(d_k), pv = padded_dim(d_v);
-  const Workspace w = workspace_layout(F, H, pk, pv, splits);
+  const vda::SplitPlan plan = default_plan(dev, F, N, H, pk, pv, is_f32);
+  const Workspace w = workspace_layout(F, H, pk, pv, plan);
   const size_t qk_pad = pk != d_k ? round_up(tok * pk * es, 256) : 0;
   const size_t v_pad = pv != d_v ? round_up(tok * pv * es, 256) : 0;
   const size_t ws_bytes = round_up(w.total, 256) + 2 * qk_pad + 2 * v_pad;
@@ -229,10 +251,10 @@ int forward_impl(bool is_f32, const void* q, const void* k, const void* v, const
     ox = pad_base + 2 * qk_pad + v_pad;
   }
   if (e == hipSuccess)
-    e = vda::launch_frame_stats(is_f32, kx, vx, beta, F, N, H, pk, pv, splits, A_part, B_part,
+    e = vda::launch_frame_stats(is_f32, kx, vx, beta, F, N, H, pk, pv, plan, A_part, B_part,
                                 stream);
   if (e == hipSuccess)
-    e = vda::launch_frame_inverse(A_part, B_part, splits, (long long)H * F, pk, pv, Inv, stream);
+    e = vda::launch_frame_inverse(A_part, B_part, plan, (long long)H * F, pk, pv, Inv, stream);
   if (e == hipSuccess)
     e = vda::launch_state_scan(is_f32, Inv, B_part, F, H, pk, pv, S_fwd, S_rev, stream);
   if (e == hipSuccess)
@@ -274,55 +296,79 @@ int vda_forward_f32(const float* q, const float* k, const float* v, const float*
   return forward_impl(true, q, k, v, beta, gate, F, N, H, d_k, d_v, out, stream);
 }
 
-int vda_default_splits(int F, int N, int H) {
-  if (F < 1 || N < 1 || H < 1) return 1;
-  return default_splits(F, N, H);
+int vda_default_split_plan(int F, int N, int H, int d_k, int d_v, int is_f32, int* tail_frames,
+                           int* splits) {
+  if (!tail_frames || !splits) return VDA_ERR_NULL;
+  int st = check_shape(F, N, H, d_k, d_v);
+  if (st != VDA_OK) return st;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return VDA_ERR_HIP;
+  const vda::SplitPlan p = default_plan(dev, F, N, H, d_k, d_v, is_f32 != 0);
+  *tail_frames = p.tail;
+  *splits = p.splits;
+  return VDA_OK;
+}
+
+// Shared checks of a split plan over `count` frames of N tokens.
+int check_plan(long long count, int N, int tail_frames, int splits) {
+  if (splits < 1) return VDA_ERR_SIZE;
+  if (splits == 1) return VDA_OK;  // no frame is split; tail_frames is ignored
+  if (tail_frames < 1 || tail_frames > count || splits > ((long long)N + 63) / 64)
+    return VDA_ERR_SIZE;
+  const vda::SplitPlan p{tail_frames, splits};
+  if (vda::stats_workgroups(count, p) > 0x7fffffffLL) return VDA_ERR_SIZE;
+  return VDA_OK;
 }
 
 int vda_frame_stats(const void* k, const void* v, const float* beta, int F, int N, int H,
-                    int d_k, int d_v, int splits, int is_f32, float* A_part, float* B_part,
-                    hipStream_t stream) {
+                    int d_k, int d_v, int tail_frames, int splits, int is_f32, float* A_part,
+                    float* B_part, hipStream_t stream) {
   if (!k || !v || !beta || !A_part || !B_part) return VDA_ERR_NULL;
   int st = check_shape(F, N, H, d_k, d_v);
   if (st != VDA_OK) return st;
-  if (splits < 1 || splits > (N + 63) / 64 || (long long)H * F * splits > 0x7fffffffLL)
-    return VDA_ERR_SIZE;
+  const size_t fh = (size_t)H * F;
+  st = check_plan((long long)fh, N, tail_frames, splits);
+  if (st != VDA_OK) return st;
   if (!aligned(k, 16) || !aligned(v, 16) || !aligned(beta, 4) || !aligned(A_part, 16) ||
       !aligned(B_part, 16))
     return VDA_ERR_ALIGN;
-  const size_t fh = (size_t)H * F;
-  const Range ra = range_of(A_part, (size_t)splits * fh * d_k * d_k * 4);
-  const Range rb = range_of(B_part, (size_t)splits * fh * d_v * d_k * 4);
+  const vda::SplitPlan plan{splits > 1 ? tail_frames : 0, splits};
+  const size_t parts = (size_t)vda::partial_count((long long)fh, plan);
+  const Range ra = range_of(A_part, parts * d_k * d_k * 4);
+  const Range rb = range_of(B_part, parts * d_v * d_k * 4);
   const size_t es = is_f32 ? 4 : 2;
   const Range rk = range_of(k, fh * N * d_k * es), rv = range_of(v, fh * N * d_v * es),
               rbeta = range_of(beta, fh * N * 4);
   if (overlaps(ra, rb) || overlaps(ra, rk) || overlaps(ra, rv) || overlaps(ra, rbeta) ||
       overlaps(rb, rk) || overlaps(rb, rv) || overlaps(rb, rbeta))
     return VDA_ERR_OVERLAP;
-  return hip_status(vda::launch_frame_stats(is_f32 != 0, k, v, beta, F, N, H, d_k, d_v, splits,
+  return hip_status(vda::launch_frame_stats(is_f32 != 0, k, v, beta, F, N, H, d_k, d_v, plan,
                                             A_part, B_part, stream));
 }
 
-int vda_frame_inverse(const float* A_part, float* B_part, int splits, int count, int d_k,
-                      int d_v, float* Inv, hipStream_t stream) {
+int vda_frame_inverse(const float* A_part, float* B_part, int tail_frames, int splits, int count,
+                      int d_k, int d_v, float* Inv, hipStream_t stream) {
   if (!A_part || !Inv || (splits > 1 && !B_part)) return VDA_ERR_NULL;
-  if (splits < 1 || count < 1 || (long long)count * 64 > 0x7fffffffLL) return VDA_ERR_SIZE;
+  if (count < 1 || (long long)count * 64 > 0x7fffffffLL) return VDA_ERR_SIZE;
+  // N is not known here; any split count the statistics step accepted is fine.
+  int st = check_plan(count, 0x7fffffff, tail_frames, splits);
+  if (st != VDA_OK) return st;
   if (!supported_dim(d_k) || (splits > 1 && !supported_dim(d_v))) return VDA_ERR_UNSUPPORTED;
   if (!aligned(A_part, 16) || !aligned(Inv, 16) || !aligned(B_part, 16)) return VDA_ERR_ALIGN;
-  const size_t mat = (size_t)count * d_k * d_k * 4;
-  const Range ri = range_of(Inv, mat);
-  for (int s = 0; s < splits; ++s) {
-    const Range rs = range_of(reinterpret_cast<const char*>(A_part) + s * mat, mat);
-    const bool same = rs.lo == ri.lo;
-    if (overlaps(ri, rs) && !(same && s == 0)) return VDA_ERR_OVERLAP;
-  }
+  const vda::SplitPlan plan{splits > 1 ? tail_frames : 0, splits};
+  const size_t mat = (size_t)d_k * d_k * 4;
+  const size_t parts = (size_t)vda::partial_count(count, plan);
+  // Inv may be the first `count` partials (in place), but no other partial.
+  const Range ri = range_of(Inv, count * mat);
+  const Range ra = range_of(A_part, parts * mat);
+  const Range rextra = range_of(reinterpret_cast<const char*>(A_part) + count * mat,
+                                (parts - count) * mat);
+  if (overlaps(ri, ra) && (ri.lo != ra.lo || overlaps(ri, rextra))) return VDA_ERR_OVERLAP;
   if (splits > 1) {
-    const size_t bmat = (size_t)count * d_v * d_k * 4;
-    const Range rb = range_of(B_part, splits * bmat);
-    if (overlaps(rb, ri) || overlaps(rb, range_of(A_part, splits * mat))) return VDA_ERR_OVERLAP;
+    const Range rb = range_of(B_part, parts * d_v * d_k * 4);
+    if (overlaps(rb, ri) || overlaps(rb, ra)) return VDA_ERR_OVERLAP;
   }
-  return hip_status(
-      vda::launch_frame_inverse(A_part, B_part, splits, count, d_k, d_v, Inv, stream));
+  return hip_status(vda::launch_frame_inverse(A_part, B_part, plan, count, d_k, d_v, Inv, stream));
 }
 
 int vda_state_scan(const float* Inv, const float* B, int F, int H, int d_k, int d_v, int is_f32,

@@ -10,43 +10,55 @@ namespace {
 
 template <int DK>
 __global__ __launch_bounds__(64 * (DK / 16 < 4 ? DK / 16 : 4))
-void inverse_kernel(const float* A_part, int splits, size_t part_stride,
+void inverse_kernel(const float* A_part, unsigned first_split, int plan_splits, unsigned extra,
+                    size_t part_stride,
                     float* Inv,  // may alias A_part (in place)
                     float* B_part, size_t b_mat, size_t b_stride) {
   constexpr int NB = DK / 16;
   constexpr int W = NB < 4 ? NB : 4;
   __shared__ __align__(16) float piv[2][NB][64 * 4];  // [buffer][block j][lane][4]
 
-  const size_t base = (size_t)blockIdx.x * (DK * DK);
   const int tid = threadIdx.x;
-
-  // Fold the token-split partials of B_t into the first partial (in place).
-  if (splits > 1)
-    inv::fold_b_partials(B_part + (size_t)blockIdx.x * b_mat, splits, b_mat, b_stride, tid, 64 * W);
-
+  if (blockIdx.x >= gridDim.x - extra) {
+    // One of the workgroups past the matrices: fold the token-range partials
+    // of B_t of split frame first_split + (its index) into the first partial
+    // (in place), alongside the inversions.
+    const size_t f = first_split + (blockIdx.x - (gridDim.x - extra));
+    inv::fold_b_partials(B_part + f * b_mat, plan_splits, b_mat, b_stride, tid, 64 * W);
+    return;
+  }
+  const size_t base = (size_t)blockIdx.x * (DK * DK);
+  // Frames from first_split on were split into plan_splits token ranges.
+  const int splits = blockIdx.x >= first_split ? plan_splits : 1;
   inv::invert_matrix<DK>(A_part, splits, part_stride, base, Inv, &piv[0][0][0], tid);
 }
 
 }  // namespace
 
-hipError_t launch_frame_inverse(const float* A_part, float* B_part, int splits, long long count,
-                                int d_k, int d_v, float* Inv, hipStream_t stream) {
-  const size_t part_stride = (size_t)count * d_k * d_k;
+hipError_t launch_frame_inverse(const float* A_part, float* B_part, SplitPlan plan,
+                                long long count, int d_k, int d_v, float* Inv,
+                                hipStream_t stream) {
+  const int splits = plan.splits > 1 && plan.tail > 0 ? plan.splits : 1;
+  const unsigned first_split = splits > 1 ? (unsigned)(count - plan.tail) : (unsigned)count;
+  // Partial p of frame f is matrix f + p * tail.
+  const size_t part_stride = (size_t)plan.tail * d_k * d_k;
   const size_t b_mat = (size_t)d_v * d_k;
-  const size_t b_stride = (size_t)count * b_mat;
-  const dim3 grid((unsigned)count);
+  const size_t b_stride = (size_t)plan.tail * b_mat;
+  // One workgroup per matrix, then one per split frame to fold its B partials.
+  const unsigned extra = splits > 1 ? (unsigned)plan.tail : 0u;
+  const dim3 grid((unsigned)count + extra);
   switch (d_k) {
     case 32:
-      hipLaunchKernelGGL(inverse_kernel<32>, grid, dim3(64 * 2), 0, stream, A_part, splits,
-                         part_stride, Inv, B_part, b_mat, b_stride);
+      hipLaunchKernelGGL(inverse_kernel<32>, grid, dim3(64 * 2), 0, stream, A_part, first_split,
+                         splits, extra, part_stride, Inv, B_part, b_mat, b_stride);
       break;
     case 64:
-      hipLaunchKernelGGL(inverse_kernel<64>, grid, dim3(64 * 4), 0, stream, A_part, splits,
-                         part_stride, Inv, B_part, b_mat, b_stride);
+      hipLaunchKernelGGL(inverse_kernel<64>, grid, dim3(64 * 4), 0, stream, A_part, first_split,
+                         splits, extra, part_stride, Inv, B_part, b_mat, b_stride);
       break;
     case 128:
-      hipLaunchKernelGGL(inverse_kernel<128>, grid, dim3(64 * 4), 0, stream, A_part, splits,
-                         part_stride, Inv, B_part, b_mat, b_stride);
+      hipLaunchKernelGGL(inverse_kernel<128>, grid, dim3(64 * 4), 0, stream, A_part, first_split,
+                         splits, extra, part_stride, Inv, B_part, b_mat, b_stride);
       break;
     default:
       return hipErrorInvalidValue;

@@ -104,28 +104,43 @@ __device__ __forceinline__ void invert_rows(const float* A_part, int splits, siz
   // column segment M[16i + 4lg .. +3][16j + li]; A_t is symmetric, so it is
   // read as the contiguous row segment M[16j + li][16i + 4lg .. +3] with
   // 16-byte loads (and the result is written back the same way).
+  // The loads of a block row of one partial are issued together (one memory
+  // round trip per block row and partial, not one per block); one block row
+  // at a time keeps the registers of loads in flight within budget.
   floatx4 acc[RPW][NB];
+  const float* a0 = A_part + base + (size_t)li * DK + 4 * lg;
+#pragma unroll
+  for (int q = 0; q < RPW; ++q) {
+#pragma unroll
+    for (int j = 0; j < NB; ++j)
+      acc[q][j] = *reinterpret_cast<const floatx4*>(a0 + (16 * j) * DK + 16 * (WV + W * q));
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  // Further token ranges of a split frame, four blocks per round trip (the
+  // registers of these loads would otherwise lower the occupancy).
+  constexpr int XB = NB < 4 ? NB : 4;
+  for (int s = 1; s < splits; ++s) {
+#pragma unroll
+    for (int q = 0; q < RPW; ++q) {
+#pragma unroll
+      for (int j0 = 0; j0 < NB; j0 += XB) {
+        floatx4 x[XB];
+#pragma unroll
+        for (int j = 0; j < XB; ++j)
+          x[j] = *reinterpret_cast<const floatx4*>(a0 + s * part_stride + (16 * (j0 + j)) * DK +
+                                                   16 * (WV + W * q));
+#pragma unroll
+        for (int j = 0; j < XB; ++j) acc[q][j0 + j] += x[j];
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+  }
 #pragma unroll
   for (int q = 0; q < RPW; ++q) {
     const int i = WV + W * q;
 #pragma unroll
-    for (int j = 0; j < NB; ++j) {
-      floatx4 v = {0.f, 0.f, 0.f, 0.f};
-      for (int s = 0; s < splits; ++s) {
-        const float4 x = *reinterpret_cast<const float4*>(
-            A_part + s * part_stride + base + (size_t)(16 * j + li) * DK + 16 * i + 4 * lg);
-        v[0] += x.x;
-        v[1] += x.y;
-        v[2] += x.z;
-        v[3] += x.w;
-      }
-      if (i == j) {
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-          if (4 * lg + r == li) v[r] += 1.0f;
-      }
-      acc[q][j] = v;
-    }
+    for (int r = 0; r < 4; ++r)
+      if (4 * lg + r == li) acc[q][i][r] += 1.0f;
   }
 
 #pragma unroll
@@ -215,20 +230,36 @@ __device__ __forceinline__ void invert_rows(const float* A_part, int splits, siz
   }
 }
 
-// Sum the token-split partials of B_t into the first one (in place); all
-// threads of the workgroup take part.
+// Sum the token-split partials of B_t into the first one (in place, in
+// partial order); all threads of the workgroup take part.  Each thread
+// handles four 16-byte pieces per pass, so four loads of every partial are
+// in flight together.
 __device__ __forceinline__ void fold_b_partials(float* b0, int splits, size_t b_mat, size_t b_stride,
                                                 int tid, int nthreads) {
-  for (size_t idx = (size_t)tid * 4; idx < b_mat; idx += (size_t)nthreads * 4) {
-    float4 a4 = *reinterpret_cast<const float4*>(b0 + idx);
-    for (int s = 1; s < splits; ++s) {
-      const float4 x = *reinterpret_cast<const float4*>(b0 + s * b_stride + idx);
-      a4.x += x.x;
-      a4.y += x.y;
-      a4.z += x.z;
-      a4.w += x.w;
+  const size_t step = (size_t)nthreads * 4;
+  for (size_t idx0 = (size_t)tid * 4; idx0 < b_mat; idx0 += 4 * step) {
+    floatx4 a[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const size_t idx = idx0 + e * step;
+      a[e] = idx < b_mat ? *reinterpret_cast<const floatx4*>(b0 + idx) : floatx4{0.f, 0.f, 0.f, 0.f};
     }
-    *reinterpret_cast<float4*>(b0 + idx) = a4;
+    for (int s = 1; s < splits; ++s) {
+      floatx4 x[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const size_t idx = idx0 + e * step;
+        x[e] = idx < b_mat ? *reinterpret_cast<const floatx4*>(b0 + s * b_stride + idx)
+                           : floatx4{0.f, 0.f, 0.f, 0.f};
+      }
+#pragma unroll
+      for (int e = 0; e < 4; ++e) a[e] += x[e];
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const size_t idx = idx0 + e * step;
+      if (idx < b_mat) *reinterpret_cast<floatx4*>(b0 + idx) = a[e];
+    }
   }
 }
 

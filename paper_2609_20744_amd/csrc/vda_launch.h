@@ -5,15 +5,36 @@
 
 namespace vda {
 
-// Step a1, Eq. 3b: partial frame statistics per token split.
+// Split plan of the statistics step: the last `tail` of the `count` frames
+// are split into `splits` token ranges; every other frame is one range.
+// Partial p of frame f sits at matrix index f + p * tail (p = 0: index f).
+struct SplitPlan {
+  int tail;
+  int splits;
+};
+
+inline long long partial_count(long long count, SplitPlan plan) {
+  return plan.splits > 1 ? count + (long long)plan.tail * (plan.splits - 1) : count;
+}
+
+// Workgroups of the statistics step under `plan`.
+inline long long stats_workgroups(long long count, SplitPlan plan) {
+  return plan.splits > 1 ? count - plan.tail + (long long)plan.tail * plan.splits : count;
+}
+
+// Statistics workgroups one compute unit holds at once (occupancy query).
+int stats_blocks_per_cu(bool is_f32, int d_k, int d_v);
+
+// Step a1, Eq. 3b: partial frame statistics per token range.
 hipError_t launch_frame_stats(bool is_f32, const void* k, const void* v, const float* beta,
-                              int F, int N, int H, int d_k, int d_v, int splits,
+                              int F, int N, int H, int d_k, int d_v, SplitPlan plan,
                               float* A_part, float* B_part, hipStream_t stream);
 
 // Step a2, Eq. 5: Inv = (I + sum of A partials)^{-1}; also folds the B
-// partials into B_part[0].
-hipError_t launch_frame_inverse(const float* A_part, float* B_part, int splits, long long count,
-                                int d_k, int d_v, float* Inv, hipStream_t stream);
+// partials of every split frame into its first partial.
+hipError_t launch_frame_inverse(const float* A_part, float* B_part, SplitPlan plan,
+                                long long count, int d_k, int d_v, float* Inv,
+                                hipStream_t stream);
 
 // Steps a3/a4, Eq. A.1: forward and reverse state scans (exact fp32 products,
 // or split-bf16 products with fp32 accumulation).

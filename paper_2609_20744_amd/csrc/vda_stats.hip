@@ -1,12 +1,15 @@
 // Step a1: per-frame statistics A_t = K_t^T Diag(beta_t) K_t and
 // B_t = V_t^T Diag(beta_t) K_t (Eq. 3b), computed in one pass over K and V.
 //
-// Two workgroups share a frame (and a token range): workgroup half h owns
-// the output rows of K channels [h*d_k/2, (h+1)*d_k/2) (rows of A_t) and of
-// V channels [h*d_v/2, ...) (rows of B_t), against all d_k columns of
-// beta*K.  So no partial sums are written, each lane holds half the
-// accumulators, and the two halves (placed on one XCD) read the same K
-// tiles, which the second one finds in L2.
+// One workgroup per frame (and token range).  A_t is symmetric, so only its
+// blocks on or above the diagonal are accumulated (16 x 16 blocks (i, j),
+// i <= j) and each off-diagonal block is also written transposed.  The four
+// waves split the work by output columns (channels of beta*k): with 8 column
+// blocks, wave w owns columns w and 7 - w, which carry (w + 1) + (8 - w)
+// upper-triangle blocks of A_t and 2 * d_v / 16 blocks of B_t: the same count
+// for every wave.  Per 32 tokens a wave reads two beta*k operands and the k
+// and v row operands its blocks need, so each operand read from LDS feeds
+// one or two matrix products.
 //
 // Both products contract over tokens, the slow axis of the frame-major
 // [token][channel] layout.  Tiles of 64 tokens are copied into LDS in that
@@ -19,10 +22,10 @@
 // c0 + 4 (j mod 4), lane i receives tokens t0..t0+3 of channel c0 + i: one
 // half of a v_mfma_f32_16x16x32_bf16 operand column.  Lane group g takes the
 // tokens {4g + e} and {16 + 4g + e} of each 32-token step (the same order in
-// both operands), which with a row stride of 288 bytes (32 mod 256) keeps
-// the 32 lanes of one LDS pass on distinct banks.  Tokens past the range are
-// read through range-checked buffer loads as zero, so they contribute
-// nothing and no load sits behind a branch or feeds a select.
+// both operands), which with a row stride of 32 mod 256 bytes keeps the 32
+// lanes of one LDS pass on distinct banks.  Tokens past the range are read
+// through range-checked buffer loads as zero, so they contribute nothing and
+// no load sits behind a branch or feeds a select.
 #include "vda_common.h"
 #include "vda_launch.h"
 
@@ -53,76 +56,65 @@ __device__ __forceinline__ uint32_t scale_pair(uint32_t w, float b) {
   return pack_bf16x2(bf16_lo(w) * b, bf16_hi(w) * b);
 }
 
+// Work item of statistics workgroup L under a split plan (count frames; the
+// last `tail` are split into `splits` token ranges, whose workgroups come
+// after those of the unsplit frames so that they fill the end of the launch).
+struct StatsItem {
+  unsigned fh;    // frame-head
+  unsigned slot;  // partial matrix index: fh + piece * tail
+  int n_begin;    // token range [n_begin, n_end)
+  int n_end;
+};
+
+__device__ __forceinline__ StatsItem stats_item(unsigned L, unsigned count, unsigned tail,
+                                                int splits, int N, int tokens_per_split) {
+  const unsigned head = count - tail;
+  if (splits <= 1 || L < head) return StatsItem{L, L, 0, N};
+  const unsigned u = L - head;
+  const unsigned fh = head + u / (unsigned)splits;
+  const int piece = (int)(u % (unsigned)splits);
+  const int n_begin = piece * tokens_per_split;
+  return StatsItem{fh, fh + (unsigned)piece * tail, n_begin, min(N, n_begin + tokens_per_split)};
+}
+
+// Output blocks of wave W (compile time).  CB = d_k / 16 column blocks,
+// RBV = d_v / 16 row blocks of B_t.  The wave owns the columns col(c),
+// c < ncols; in each it accumulates the A_t blocks i = 0 .. col(c) (when
+// has_a) and the B_t blocks v_begin .. v_end - 1.
+template <int CB, int RBV, int W>
+struct WavePlan {
+  static constexpr int ncols = CB == 8 ? 2 : 1;
+  static constexpr int col(int c) {
+    return CB == 8 ? (c == 0 ? W : 7 - W) : (CB == 4 ? W : (W & 1));
+  }
+  static constexpr bool has_a = CB != 2 || (W >> 1) == 0;
+  static constexpr int v_begin = CB == 2 ? (W >> 1) * (RBV / 2) : 0;
+  static constexpr int v_end = CB == 2 ? v_begin + RBV / 2 : RBV;
+  static constexpr int imax = ncols == 2 ? (col(0) > col(1) ? col(0) : col(1)) : col(0);
+};
+
 template <int DK, int DV>
-__global__ __launch_bounds__(kThreads, 2)
-void stats_bf16_kernel(const uint16_t* __restrict__ K, const uint16_t* __restrict__ V,
-                       const float* __restrict__ beta, int N, int tokens_per_split,
-                       int splits, unsigned fh_count, unsigned nwg,
-                       float* __restrict__ A_part, float* __restrict__ B_part) {
-  constexpr int KH = DK / 2;          // K channels (A rows) owned by a half
-  constexpr int VH = DV / 2;          // V channels (B rows) owned by a half
-  constexpr int XC = KH + VH;         // channels of the X tile [K_h | V_h]
-  constexpr int LDX = tile_ld(XC);
-  constexpr int LDY = tile_ld(DK);
-  constexpr int RB = XC / 16;         // 16-row output blocks
-  constexpr int CB = DK / 16;         // 16-column output blocks
-  // The four waves split the workgroup's XC x DK output 2 x 2: wave (wr, wc)
-  // owns row blocks wr*RPW .. and column blocks wc*CPW .. .  Per token a wave
-  // reads RPW + CPW operand blocks from LDS, fewer than a 4 x 1 split.
-  constexpr int RPW = (RB + 1) / 2;   // output row blocks per wave
-  constexpr int CPW = CB / 2;         // output column blocks per wave
-  constexpr int KCH = DK / 8;         // 16-byte chunks per K row
-  constexpr int VCH = VH / 8;         // 16-byte chunks per V-half row
-  constexpr int NKC = kStatsTile * KCH / kThreads;                // K chunks per thread
-  constexpr int NVC = (kStatsTile * VCH + kThreads - 1) / kThreads;  // V chunks per thread
-  static_assert(kStatsTile * KCH % kThreads == 0, "K chunks divide evenly");
+struct StatsFrame {
+  static constexpr int LDK = tile_ld(DK);
+  static constexpr int LDV = tile_ld(DV);
+  static constexpr int KCH = DK / 8;  // 16-byte chunks per K row
+  static constexpr int VCH = DV / 8;  // 16-byte chunks per V row
+  static constexpr int NKC = kStatsTile * KCH / kThreads;  // K chunks per thread and tile
+  static constexpr int NVC = kStatsTile * VCH / kThreads;  // V chunks per thread and tile
+  static constexpr int KROWS = kThreads / KCH;
+  static constexpr int VROWS = kThreads / VCH;
+  static_assert(NKC * kThreads == kStatsTile * KCH && NVC * kThreads == kStatsTile * VCH,
+                "chunks divide evenly");
 
-  // One extra row absorbs the stores of lanes with nothing to store, so the
-  // stores need no branch.
-  __shared__ __align__(16) uint16_t xt[(kStatsTile + 1) * LDX];  // [token][K_h | V_h]
-  __shared__ __align__(16) uint16_t yt[kStatsTile * LDY];  // [token][beta * K]
+  uint16_t* kt;  // [token][k]          (LDS)
+  uint16_t* yt;  // [token][beta * k]   (LDS)
+  uint16_t* vt;  // [token][v]          (LDS)
+  __amdgpu_buffer_rsrc_t krsrc, vrsrc, brsrc;
+  int kc, kr0, vc, vr0, li, lg;
 
-  // Logical id: (frame-head, split, half), halves adjacent on one XCD.
-  const unsigned L = xcd_grouped_id(blockIdx.x, nwg);
-  const int half = uniform(L & 1);
-  const unsigned fs = L >> 1;
-  const unsigned fh = (unsigned)uniform((int)(fs / splits));
-  const int split = uniform((int)(fs % splits));
-  const int n_begin = split * tokens_per_split;
-  const int n_end = uniform(min(N, n_begin + tokens_per_split));
-
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (scalar)
-  const int wr = wave & 1;
-  const int wc = wave >> 1;
-  const int li = lane & 15;
-  const int lg = lane >> 4;
-
-  // Range-checked views of this frame's rows [0, n_end): rows past the end
-  // read as zero (so they add nothing to either product), with no clamp or
-  // select between a load and its use.
-  const __amdgpu_buffer_rsrc_t krsrc = make_rsrc(K + (size_t)fh * N * DK, (uint32_t)(n_end * DK * 2));
-  const __amdgpu_buffer_rsrc_t vrsrc =
-      make_rsrc(V + (size_t)fh * N * DV + half * VH, (uint32_t)(n_end * DV * 2 - half * VH * 2));
-  const __amdgpu_buffer_rsrc_t brsrc = make_rsrc(beta + (size_t)fh * N, (uint32_t)(n_end * 4));
-
-  // Loader roles: K chunk i of this thread is (row kr0 + i*kRowStep, col kc),
+  // Loader roles: chunk i of this thread is (row r0 + i * ROWS, column c),
   // consecutive lanes reading consecutive 16-byte chunks of a row.
-  constexpr int KROWS = kThreads / KCH;  // K rows covered per pass
-  const int kc = tid % KCH;
-  const int kr0 = tid / KCH;
-  const bool kc_in_half = (kc / (KH / 8)) == half;
-  const int vch = tid % VCH;
-  const int vr0 = tid / VCH;
-  constexpr int VROWS = kThreads / VCH;
-
-  // Two-tile register ring, as separately named arrays so that every access
-  // has a compile-time index (a two-dimensional ring was moved to scratch).
-  u32x4 kraw0[NKC], kraw1[NKC];
-  float kb0[NKC], kb1[NKC];
-  u32x4 vraw0[NVC], vraw1[NVC];
-  auto load_tile = [&](int n0, u32x4 (&kr)[NKC], float (&kbv)[NKC], u32x4 (&vr)[NVC]) {
+  __device__ void load_tile(int n0, u32x4 (&kr)[NKC], float (&kbv)[NKC], u32x4 (&vr)[NVC]) const {
 #pragma unroll
     for (int i = 0; i < NKC; ++i) {
       const uint32_t n = (uint32_t)(n0 + kr0 + i * KROWS);
@@ -132,92 +124,166 @@ void stats_bf16_kernel(const uint16_t* __restrict__ K, const uint16_t* __restric
     }
 #pragma unroll
     for (int i = 0; i < NVC; ++i) {
-      const int r = vr0 + i * VROWS;  // >= kStatsTile only when the tile needs fewer chunks
-      const uint32_t off = r < kStatsTile ? (uint32_t)(n0 + r) * (DV * 2) + vch * 16 : kOutOfRange;
-      vr[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(vrsrc, (int)off, 0, 0));
+      const uint32_t n = (uint32_t)(n0 + vr0 + i * VROWS);
+      vr[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                            vrsrc, (int)(n * (DV * 2) + vc * 16), 0, 0));
     }
-  };
-  auto store_tile = [&](const u32x4 (&kr)[NKC], const float (&kbv)[NKC], const u32x4 (&vr)[NVC]) {
+  }
+
+  __device__ void store_tile(const u32x4 (&kr)[NKC], const float (&kbv)[NKC],
+                             const u32x4 (&vr)[NVC]) const {
 #pragma unroll
     for (int i = 0; i < NKC; ++i) {
       const int r = kr0 + i * KROWS;
       const u32x4 w = kr[i];
       const float b = kbv[i];
-      *reinterpret_cast<u32x4*>(&yt[r * LDY + kc * 8]) =
+      *reinterpret_cast<u32x4*>(&yt[r * LDK + kc * 8]) =
           u32x4{scale_pair(w[0], b), scale_pair(w[1], b), scale_pair(w[2], b), scale_pair(w[3], b)};
-      const int xo = kc_in_half ? r * LDX + (kc * 8 - half * KH) : kStatsTile * LDX;
-      *reinterpret_cast<u32x4*>(&xt[xo]) = w;
+      *reinterpret_cast<u32x4*>(&kt[r * LDK + kc * 8]) = w;
     }
 #pragma unroll
-    for (int i = 0; i < NVC; ++i) {
-      const int r = vr0 + i * VROWS;
-      const int xo = r < kStatsTile ? r * LDX + KH + vch * 8 : kStatsTile * LDX;
-      *reinterpret_cast<u32x4*>(&xt[xo]) = vr[i];
+    for (int i = 0; i < NVC; ++i)
+      *reinterpret_cast<u32x4*>(&vt[(vr0 + i * VROWS) * LDV + vc * 8]) = vr[i];
+  }
+
+  // The whole token loop and the output stores of wave W.
+  template <int W>
+  __device__ void run(int n_begin, int n_end, float* Ab, float* Bb) const {
+    using P = WavePlan<DK / 16, DV / 16, W>;
+    constexpr int NC = P::ncols;
+    floatx4 accA[NC][DK / 16];  // [column c][row block i], i <= col(c)
+    floatx4 accB[DV / 16][NC];  // [row block v][column c]
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+#pragma unroll
+      for (int i = 0; i < DK / 16; ++i) accA[c][i] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int v = 0; v < DV / 16; ++v) accB[v][c] = floatx4{0.f, 0.f, 0.f, 0.f};
     }
-  };
 
-  floatx4 acc[RPW][CPW];
-#pragma unroll
-  for (int r = 0; r < RPW; ++r)
-#pragma unroll
-    for (int c = 0; c < CPW; ++c) acc[r][c] = floatx4{0.f, 0.f, 0.f, 0.f};
+    // Two-tile register ring, as separately named arrays so that every
+    // access has a compile-time index (a two-dimensional ring was moved to
+    // scratch).
+    u32x4 kraw0[NKC], kraw1[NKC];
+    float kb0[NKC], kb1[NKC];
+    u32x4 vraw0[NVC], vraw1[NVC];
 
-  // Consume one tile from the ring, then refill its slot with tile n_next.
-  auto tile_step = [&](int n_next, u32x4 (&kr)[NKC], float (&kbv)[NKC], u32x4 (&vr)[NVC]) {
-    lds_barrier();  // previous tile's operand reads are done
-    store_tile(kr, kbv, vr);
-    lds_barrier();
-    load_tile(n_next, kr, kbv, vr);
+    // Consume one tile from the ring, then refill its slot with tile n_next.
+    auto tile_step = [&](int n_next, u32x4 (&kr)[NKC], float (&kbv)[NKC], u32x4 (&vr)[NVC]) {
+      lds_barrier();  // previous tile's operand reads are done
+      store_tile(kr, kbv, vr);
+      lds_barrier();
+      load_tile(n_next, kr, kbv, vr);
 #pragma unroll
-    for (int ks = 0; ks < kStatsTile / 32; ++ks) {
-      bf16x8 bop[CPW];
+      for (int ks = 0; ks < kStatsTile / 32; ++ks) {
+        bf16x8 bop[NC];
 #pragma unroll
-      for (int c = 0; c < CPW; ++c)
-        bop[c] = tr_operand<LDY>(yt, ks * 32, (wc * CPW + c) * 16, li, lg);
+        for (int c = 0; c < NC; ++c) bop[c] = tr_operand<LDK>(yt, ks * 32, P::col(c) * 16, li, lg);
+        if (P::has_a) {
 #pragma unroll
-      for (int r = 0; r < RPW; ++r) {
-        const int rb = wr * RPW + r;
-        if (RB % 2 == 0 || rb < RB) {
-          const bf16x8 aop = tr_operand<LDX>(xt, ks * 32, rb * 16, li, lg);
+          for (int i = 0; i <= P::imax; ++i) {
+            const bf16x8 aop = tr_operand<LDK>(kt, ks * 32, i * 16, li, lg);
 #pragma unroll
-          for (int c = 0; c < CPW; ++c)
-            acc[r][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aop, bop[c], acc[r][c], 0, 0, 0);
+            for (int c = 0; c < NC; ++c)
+              if (i <= P::col(c))
+                accA[c][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aop, bop[c], accA[c][i], 0, 0, 0);
+          }
+        }
+#pragma unroll
+        for (int v = P::v_begin; v < P::v_end; ++v) {
+          const bf16x8 aop = tr_operand<LDV>(vt, ks * 32, v * 16, li, lg);
+#pragma unroll
+          for (int c = 0; c < NC; ++c)
+            accB[v][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aop, bop[c], accB[v][c], 0, 0, 0);
         }
       }
+    };
+
+    if (n_begin < n_end) {
+      load_tile(n_begin, kraw0, kb0, vraw0);
+      __builtin_amdgcn_sched_barrier(0);
+      load_tile(n_begin + kStatsTile, kraw1, kb1, vraw1);
+      __builtin_amdgcn_sched_barrier(0);
     }
-  };
+    // Pairs of tiles per iteration (a surplus tile has beta = 0 everywhere).
+    for (int n0 = n_begin; n0 < n_end; n0 += 2 * kStatsTile) {
+      tile_step(n0 + 2 * kStatsTile, kraw0, kb0, vraw0);
+      tile_step(n0 + 3 * kStatsTile, kraw1, kb1, vraw1);
+    }
 
-  if (n_begin < n_end) {
-    load_tile(n_begin, kraw0, kb0, vraw0);
-    __builtin_amdgcn_sched_barrier(0);
-    load_tile(n_begin + kStatsTile, kraw1, kb1, vraw1);
-    __builtin_amdgcn_sched_barrier(0);
-  }
-  // Pairs of tiles per iteration (a surplus tile has beta = 0 everywhere).
-  for (int n0 = n_begin; n0 < n_end; n0 += 2 * kStatsTile) {
-    tile_step(n0 + 2 * kStatsTile, kraw0, kb0, vraw0);
-    tile_step(n0 + 3 * kStatsTile, kraw1, kb1, vraw1);
-  }
-
-  // Output block (rb, cb): lane holds rows rb*16 + 4*lg + i, column cb*16 + li.
-  float* Ab = A_part + ((size_t)split * fh_count + fh) * (DK * DK);
-  float* Bb = B_part + ((size_t)split * fh_count + fh) * (DV * DK);
+    // Block (rows rb, columns cb): lane holds rows 16 rb + 4 lg + e, column
+    // 16 cb + li.  The transposed copy of an off-diagonal A_t block puts the
+    // four rows of a lane into one 16-byte row piece.
 #pragma unroll
-  for (int r = 0; r < RPW; ++r) {
-    const int rb = wr * RPW + r;
-    if (RB % 2 == 0 || rb < RB) {
+    for (int c = 0; c < NC; ++c) {
+      const int j = P::col(c);
+      if (P::has_a) {
 #pragma unroll
-      for (int c = 0; c < CPW; ++c)
+        for (int i = 0; i <= P::imax; ++i) {
+          if (i <= P::col(c)) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int x = rb * 16 + lg * 4 + i;
-          const int col = (wc * CPW + c) * 16 + li;
-          if (rb * 16 < KH)
-            Ab[(half * KH + x) * DK + col] = acc[r][c][i];
-          else
-            Bb[(half * VH + x - KH) * DK + col] = acc[r][c][i];
+            for (int e = 0; e < 4; ++e)
+              Ab[(i * 16 + lg * 4 + e) * DK + j * 16 + li] = accA[c][i][e];
+            if (i < P::col(c))
+              *reinterpret_cast<floatx4*>(&Ab[(j * 16 + li) * DK + i * 16 + lg * 4]) = accA[c][i];
+          }
         }
+      }
+#pragma unroll
+      for (int v = P::v_begin; v < P::v_end; ++v)
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          Bb[(v * 16 + lg * 4 + e) * DK + j * 16 + li] = accB[v][c][e];
     }
+  }
+};
+
+template <int DK, int DV>
+__global__ __launch_bounds__(kThreads, 2)
+void stats_bf16_kernel(const uint16_t* __restrict__ K, const uint16_t* __restrict__ V,
+                       const float* __restrict__ beta, int N, int tokens_per_split,
+                       unsigned tail, int splits, unsigned fh_count,
+                       float* __restrict__ A_part, float* __restrict__ B_part) {
+  using S = StatsFrame<DK, DV>;
+  __shared__ __align__(16) uint16_t kt[kStatsTile * S::LDK];
+  __shared__ __align__(16) uint16_t yt[kStatsTile * S::LDK];
+  __shared__ __align__(16) uint16_t vt[kStatsTile * S::LDV];
+
+  const StatsItem it = stats_item(blockIdx.x, fh_count, tail, splits, N, tokens_per_split);
+  const unsigned fh = (unsigned)uniform((int)it.fh);
+  const unsigned slot = (unsigned)uniform((int)it.slot);
+  const int n_begin = uniform(it.n_begin);
+  const int n_end = uniform(it.n_end);
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (scalar)
+
+  S s;
+  s.kt = kt;
+  s.yt = yt;
+  s.vt = vt;
+  // Range-checked views of this frame's rows [0, n_end): rows past the end
+  // read as zero (so they add nothing to either product), with no clamp or
+  // select between a load and its use.
+  s.krsrc = make_rsrc(K + (size_t)fh * N * DK, (uint32_t)(n_end * DK * 2));
+  s.vrsrc = make_rsrc(V + (size_t)fh * N * DV, (uint32_t)(n_end * DV * 2));
+  s.brsrc = make_rsrc(beta + (size_t)fh * N, (uint32_t)(n_end * 4));
+  s.kc = tid % S::KCH;
+  s.kr0 = tid / S::KCH;
+  s.vc = tid % S::VCH;
+  s.vr0 = tid / S::VCH;
+  s.li = lane & 15;
+  s.lg = lane >> 4;
+
+  float* Ab = A_part + (size_t)slot * (DK * DK);
+  float* Bb = B_part + (size_t)slot * (DV * DK);
+  // Every branch runs the same number of barriers.
+  switch (wave) {
+    case 0: s.template run<0>(n_begin, n_end, Ab, Bb); break;
+    case 1: s.template run<1>(n_begin, n_end, Ab, Bb); break;
+    case 2: s.template run<2>(n_begin, n_end, Ab, Bb); break;
+    default: s.template run<3>(n_begin, n_end, Ab, Bb); break;
   }
 }
 
@@ -226,7 +292,7 @@ template <int DK, int DV>
 __global__ __launch_bounds__(kThreads)
 void stats_f32_kernel(const float* __restrict__ K, const float* __restrict__ V,
                       const float* __restrict__ beta, int N, int tokens_per_split,
-                      int splits, unsigned fh_count,
+                      unsigned tail, int splits, unsigned fh_count,
                       float* __restrict__ A_part, float* __restrict__ B_part) {
   constexpr int DX = DK + DV;
   constexpr int T = 32;
@@ -234,10 +300,10 @@ void stats_f32_kernel(const float* __restrict__ K, const float* __restrict__ V,
   __shared__ float xs[T][DX];
   __shared__ float ys[T][DK];
 
-  const unsigned fh = blockIdx.x / splits;
-  const int split = blockIdx.x % splits;
-  const int n_begin = split * tokens_per_split;
-  const int n_end = min(N, n_begin + tokens_per_split);
+  const StatsItem it = stats_item(blockIdx.x, fh_count, tail, splits, N, tokens_per_split);
+  const unsigned fh = it.fh;
+  const int n_begin = it.n_begin;
+  const int n_end = it.n_end;
   const int tid = threadIdx.x;
 
   float acc[OPT];
@@ -264,8 +330,8 @@ void stats_f32_kernel(const float* __restrict__ K, const float* __restrict__ V,
       }
     }
   }
-  float* Ab = A_part + ((size_t)split * fh_count + fh) * (DK * DK);
-  float* Bb = B_part + ((size_t)split * fh_count + fh) * (DV * DK);
+  float* Ab = A_part + (size_t)it.slot * (DK * DK);
+  float* Bb = B_part + (size_t)it.slot * (DV * DK);
 #pragma unroll
   for (int m = 0; m < OPT; ++m) {
     const int o = tid + m * kThreads;
@@ -278,33 +344,53 @@ void stats_f32_kernel(const float* __restrict__ K, const float* __restrict__ V,
 }
 
 template <int DK, int DV>
+int blocks_per_cu_t(bool is_f32) {
+  int n = 0;
+  const void* fn = is_f32 ? reinterpret_cast<const void*>(&stats_f32_kernel<DK, DV>)
+                          : reinterpret_cast<const void*>(&stats_bf16_kernel<DK, DV>);
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, fn, kThreads, 0) != hipSuccess) return 1;
+  return n;
+}
+
+template <int DK, int DV>
 hipError_t launch_stats_t(bool is_f32, const void* k, const void* v, const float* beta,
-                          int F, int N, int H, int splits, float* A_part, float* B_part,
+                          int F, int N, int H, SplitPlan plan, float* A_part, float* B_part,
                           hipStream_t stream) {
   const unsigned fh_count = (unsigned)H * (unsigned)F;
+  const int splits = plan.splits > 1 && plan.tail > 0 ? plan.splits : 1;
+  const unsigned tail = splits > 1 ? (unsigned)plan.tail : 0u;
   const int tps = stats_tokens_per_split(N, splits);
+  const dim3 grid((unsigned)stats_workgroups(fh_count, SplitPlan{(int)tail, splits}));
   if (is_f32) {
-    const dim3 grid(fh_count * (unsigned)splits);
     hipLaunchKernelGGL((stats_f32_kernel<DK, DV>), grid, dim3(kThreads), 0, stream,
                        static_cast<const float*>(k), static_cast<const float*>(v), beta, N, tps,
-                       splits, fh_count, A_part, B_part);
+                       tail, splits, fh_count, A_part, B_part);
   } else {
-    const unsigned nwg = fh_count * (unsigned)splits * 2u;  // two row halves per frame
-    hipLaunchKernelGGL((stats_bf16_kernel<DK, DV>), dim3(nwg), dim3(kThreads), 0, stream,
+    hipLaunchKernelGGL((stats_bf16_kernel<DK, DV>), grid, dim3(kThreads), 0, stream,
                        static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v), beta, N,
-                       tps, splits, fh_count, nwg, A_part, B_part);
+                       tps, tail, splits, fh_count, A_part, B_part);
   }
   return hipGetLastError();
 }
 
 }  // namespace
 
+int stats_blocks_per_cu(bool is_f32, int d_k, int d_v) {
+#define VDA_OCC_CASE(DKV, DVV) \
+  if (d_k == DKV && d_v == DVV) return blocks_per_cu_t<DKV, DVV>(is_f32);
+  VDA_OCC_CASE(32, 32) VDA_OCC_CASE(32, 64) VDA_OCC_CASE(32, 128)
+  VDA_OCC_CASE(64, 32) VDA_OCC_CASE(64, 64) VDA_OCC_CASE(64, 128)
+  VDA_OCC_CASE(128, 32) VDA_OCC_CASE(128, 64) VDA_OCC_CASE(128, 128)
+#undef VDA_OCC_CASE
+  return 1;
+}
+
 hipError_t launch_frame_stats(bool is_f32, const void* k, const void* v, const float* beta,
-                              int F, int N, int H, int d_k, int d_v, int splits,
+                              int F, int N, int H, int d_k, int d_v, SplitPlan plan,
                               float* A_part, float* B_part, hipStream_t stream) {
-#define VDA_STATS_CASE(DKV, DVV)                                                         \
-  if (d_k == DKV && d_v == DVV)                                                          \
-    return launch_stats_t<DKV, DVV>(is_f32, k, v, beta, F, N, H, splits, A_part, B_part, \
+#define VDA_STATS_CASE(DKV, DVV)                                                       \
+  if (d_k == DKV && d_v == DVV)                                                        \
+    return launch_stats_t<DKV, DVV>(is_f32, k, v, beta, F, N, H, plan, A_part, B_part, \
                                     stream);
   VDA_STATS_CASE(32, 32) VDA_STATS_CASE(32, 64) VDA_STATS_CASE(32, 128)
   VDA_STATS_CASE(64, 32) VDA_STATS_CASE(64, 64) VDA_STATS_CASE(64, 128)

@@ -39,9 +39,9 @@ _SIGNATURES = {
     "vda_status_string": (ctypes.c_char_p, [_I]),
     "vda_forward": (_I, [_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _P, _P]),
     "vda_forward_f32": (_I, [_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _P, _P]),
-    "vda_default_splits": (_I, [_I, _I, _I]),
-    "vda_frame_stats": (_I, [_P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _P, _P, _P]),
-    "vda_frame_inverse": (_I, [_P, _P, _I, _I, _I, _I, _P, _P]),
+    "vda_default_split_plan": (_I, [_I, _I, _I, _I, _I, _I, _P, _P]),
+    "vda_frame_stats": (_I, [_P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _P, _P, _P]),
+    "vda_frame_inverse": (_I, [_P, _P, _I, _I, _I, _I, _I, _P, _P]),
     "vda_state_scan": (_I, [_P, _P, _I, _I, _I, _I, _I, _P, _P, _P]),
     "vda_readout": (_I, [_P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _P, _P]),
 }
@@ -163,49 +163,87 @@ def forward(q, k, v, beta, gate, out=None, stream=None):
     return out
 
 
-def default_splits(F: int, N: int, H: int) -> int:
-    return int(lib.vda_default_splits(F, N, H))
+def default_split_plan(F: int, N: int, H: int, d_k: int, d_v: int,
+                       is_f32: bool = False) -> tuple[int, int]:
+    """(tail_frames, splits) of the statistics step that vda_forward uses on
+    the current device (vda_default_split_plan)."""
+    t, s = ctypes.c_int(0), ctypes.c_int(0)
+    st = lib.vda_default_split_plan(F, N, H, d_k, d_v, int(bool(is_f32)), ctypes.byref(t),
+                                    ctypes.byref(s))
+    _check(st, "vda_default_split_plan")
+    return t.value, s.value
 
 
-def frame_stats(k, v, beta, splits=None, A_part=None, B_part=None, stream=None):
-    """Step a1 (vda_frame_stats): partial A, B per token split, fp32."""
+def partial_count(count: int, tail_frames: int, splits: int) -> int:
+    """Number of partial matrices of a split plan over `count` frames."""
+    return count + tail_frames * (splits - 1) if splits > 1 else count
+
+
+def fold_partials(P, count: int, tail_frames: int, splits: int):
+    """Sum each frame's partials of a [partials, ...] tensor into [count, ...]
+    (in range order, the order the library adds them)."""
+    out = P[:count].clone()
+    if splits > 1:
+        first = count - tail_frames
+        for s in range(1, splits):
+            out[first:] += P[count + (s - 1) * tail_frames:count + s * tail_frames]
+    return out
+
+
+def frame_stats(k, v, beta, splits=None, tail_frames=None, A_part=None, B_part=None,
+                stream=None):
+    """Step a1 (vda_frame_stats): partial A [P, d_k, d_k] and B [P, d_v, d_k],
+    fp32, under the split plan (tail_frames, splits); the first H*F partials
+    are the frames in [H, F] order.  Defaults: the library's plan; with only
+    `splits` given, every frame is split."""
     torch = _torch()
     dev, dt = k.device, k.dtype
     for t, n in ((k, "k"), (v, "v")):
         _require(t, n, dt, dev)
     _require(beta, "beta", torch.float32, dev)
     lead, F, N, H, d_k, d_v = _shape(k, k, v, beta)
-    splits = default_splits(F, N, H) if splits is None else int(splits)
+    if splits is None:
+        with torch.cuda.device(dev):
+            tail_frames, splits = default_split_plan(F, N, H, d_k, d_v, dt == torch.float32)
+    elif tail_frames is None:
+        tail_frames = H * F
+    splits, tail_frames = int(splits), int(tail_frames)
+    P = partial_count(H * F, tail_frames, splits)
     if A_part is None:
-        A_part = torch.empty((splits, H, F, d_k, d_k), dtype=torch.float32, device=dev)
+        A_part = torch.empty((P, d_k, d_k), dtype=torch.float32, device=dev)
     if B_part is None:
-        B_part = torch.empty((splits, H, F, d_v, d_k), dtype=torch.float32, device=dev)
+        B_part = torch.empty((P, d_v, d_k), dtype=torch.float32, device=dev)
     with torch.cuda.device(dev):
         st = lib.vda_frame_stats(k.data_ptr(), v.data_ptr(), beta.data_ptr(), F, N, H, d_k, d_v,
-                                 splits, int(dt == torch.float32), A_part.data_ptr(),
+                                 tail_frames, splits, int(dt == torch.float32), A_part.data_ptr(),
                                  B_part.data_ptr(), _stream_ptr(dev, stream))
     _check(st, "vda_frame_stats")
     return A_part, B_part
 
 
-def frame_inverse(A_part, B_part=None, Inv=None, stream=None):
-    """Step a2 (vda_frame_inverse): Inv = (I + sum of A partials)^-1, fp32.
-    A_part is [splits, count..., d_k, d_k].  With splits > 1, B_part
-    ([splits, count..., d_v, d_k]) is folded in place into B_part[0]."""
+def frame_inverse(A_part, B_part=None, count=None, tail_frames=0, splits=1, Inv=None,
+                  stream=None):
+    """Step a2 (vda_frame_inverse): Inv [count, d_k, d_k] = (I + sum of each
+    frame's A partials)^-1, fp32, under the split plan that made the partials
+    (A_part [P, d_k, d_k]; count defaults to P when splits == 1).  With
+    splits > 1 each frame's B partials ([P, d_v, d_k]) are folded in place into
+    B_part[frame]."""
     torch = _torch()
-    splits = A_part.shape[0]
     d_k = A_part.shape[-1]
-    count = math.prod(A_part.shape[1:-2])
+    if count is None:
+        if splits > 1:
+            raise ValueError("count is required with a split plan")
+        count = math.prod(A_part.shape[:-2])
     d_v = B_part.shape[-2] if B_part is not None else d_k
     if splits > 1 and B_part is None:
         raise ValueError("B_part is required when there is more than one split")
     if Inv is None:
-        Inv = torch.empty(A_part.shape[1:], dtype=torch.float32, device=A_part.device)
+        Inv = torch.empty((count, d_k, d_k), dtype=torch.float32, device=A_part.device)
     with torch.cuda.device(A_part.device):
         st = lib.vda_frame_inverse(A_part.data_ptr(),
                                    B_part.data_ptr() if B_part is not None else None,
-                                   splits, count, d_k, d_v, Inv.data_ptr(),
-                                   _stream_ptr(A_part.device, stream))
+                                   int(tail_frames), int(splits), int(count), d_k, d_v,
+                                   Inv.data_ptr(), _stream_ptr(A_part.device, stream))
     _check(st, "vda_frame_inverse")
     return Inv
 

@@ -14,7 +14,7 @@ def test_exports_every_declared_symbol():
     names = vda.header_functions()
     assert set(names) >= {"vda_forward", "vda_forward_f32", "vda_status_string", "vda_frame_stats",
                           "vda_frame_inverse", "vda_state_scan", "vda_readout",
-                          "vda_default_splits"}
+                          "vda_default_split_plan"}
     for n in names:
         assert hasattr(vda.lib, n), n
     assert set(names) == set(vda._SIGNATURES)
@@ -63,26 +63,41 @@ def test_forward_validation():
 def test_stage_validation():
     big = 1 << 32
     L = vda.lib
-    assert L.vda_frame_stats(None, big, 2 * big, 4, 64, 2, 64, 64, 1, 0, 3 * big, 4 * big, None) == 1
-    assert L.vda_frame_stats(big, 2 * big, 3 * big, 4, 64, 2, 64, 64, 0, 0, 4 * big, 5 * big, None) == 2
-    assert L.vda_frame_stats(big, 2 * big, 3 * big, 4, 64, 2, 64, 64, 2, 0, 4 * big, 5 * big, None) == 2
-    assert L.vda_frame_stats(big, 2 * big, 3 * big, 4, 64, 2, 64, 64, 1, 0, 4 * big + 4, 5 * big, None) == 4
-    assert L.vda_frame_stats(big, 2 * big, 3 * big, 4, 64, 2, 64, 64, 1, 0, big, 5 * big, None) == 5
-    assert L.vda_frame_inverse(None, None, 1, 8, 64, 64, big, None) == 1
-    assert L.vda_frame_inverse(big, None, 2, 8, 64, 64, 2 * big, None) == 1
-    assert L.vda_frame_inverse(big, None, 1, 8, 96, 64, 2 * big, None) == 3
-    assert L.vda_frame_inverse(big, None, 0, 8, 64, 64, 2 * big, None) == 2
-    # in place onto the first partial is allowed (would launch), onto the second is not
-    assert L.vda_frame_inverse(big, 3 * big, 2, 8, 64, 64, big + 8 * 64 * 64 * 4, None) == 5
+    st = L.vda_frame_stats
+    # (k, v, beta, F, N, H, d_k, d_v, tail_frames, splits, is_f32, A_part, B_part, stream)
+    assert st(None, big, 2 * big, 4, 64, 2, 64, 64, 0, 1, 0, 3 * big, 4 * big, None) == 1
+    assert st(big, 2 * big, 3 * big, 4, 64, 2, 64, 64, 0, 0, 0, 4 * big, 5 * big, None) == 2
+    # two ranges of a 64-token frame, a split plan without frames, too many frames
+    assert st(big, 2 * big, 3 * big, 4, 64, 2, 64, 64, 8, 2, 0, 4 * big, 5 * big, None) == 2
+    assert st(big, 2 * big, 3 * big, 4, 256, 2, 64, 64, 0, 2, 0, 4 * big, 5 * big, None) == 2
+    assert st(big, 2 * big, 3 * big, 4, 256, 2, 64, 64, 9, 2, 0, 4 * big, 5 * big, None) == 2
+    assert st(big, 2 * big, 3 * big, 4, 64, 2, 64, 64, 0, 1, 0, 4 * big + 4, 5 * big, None) == 4
+    assert st(big, 2 * big, 3 * big, 4, 64, 2, 64, 64, 0, 1, 0, big, 5 * big, None) == 5
+    # B partials of a tail plan (8 + 3 * 2 matrices) running into A's range
+    mat = 64 * 64 * 4
+    assert st(big, 2 * big, 3 * big, 4, 256, 2, 64, 64, 3, 3, 0, 4 * big,
+              4 * big + 13 * mat, None) == 5
+    inv = L.vda_frame_inverse
+    # (A_part, B_part, tail_frames, splits, count, d_k, d_v, Inv, stream)
+    assert inv(None, None, 0, 1, 8, 64, 64, big, None) == 1
+    assert inv(big, None, 8, 2, 8, 64, 64, 2 * big, None) == 1
+    assert inv(big, None, 0, 1, 8, 96, 64, 2 * big, None) == 3
+    assert inv(big, None, 0, 0, 8, 64, 64, 2 * big, None) == 2
+    assert inv(big, 3 * big, 9, 2, 8, 64, 64, 2 * big, None) == 2
+    # in place onto the first partials is allowed (would launch), onto the extra ones is not
+    assert inv(big, 3 * big, 8, 2, 8, 64, 64, big + 8 * mat, None) == 5
+    assert inv(big, 3 * big, 2, 3, 8, 64, 64, big + 4 * mat, None) == 5
     # B partials may not overlap the A partials or Inv
-    assert L.vda_frame_inverse(big, big + 4096, 2, 8, 64, 64, 2 * big, None) == 5
+    assert inv(big, big + 4096, 8, 2, 8, 64, 64, 2 * big, None) == 5
+    assert L.vda_default_split_plan(4, 64, 2, 64, 64, 0, None, None) == 1
     assert L.vda_state_scan(big, 2 * big, 4, 2, 64, 64, 0, 3 * big, 3 * big, None) == 5
     assert L.vda_state_scan(big, 2 * big, 4, 2, 64, 48, 0, 3 * big, 4 * big, None) == 3
     assert L.vda_readout(big, 2 * big, 3 * big, 4 * big, 4, 64, 2, 64, 64, 0, big, None) == 5
     assert L.vda_readout(big, 2 * big, 3 * big, None, 4, 64, 2, 64, 64, 0, 5 * big, None) == 1
     # the stage entry points take only the kernels' own widths (no 16)
-    assert L.vda_frame_stats(big, 2 * big, 3 * big, 4, 64, 2, 16, 64, 1, 0, 4 * big, 5 * big, None) == 3
-    assert L.vda_frame_inverse(big, None, 1, 8, 16, 64, 2 * big, None) == 3
+    assert L.vda_frame_stats(big, 2 * big, 3 * big, 4, 64, 2, 16, 64, 0, 1, 0, 4 * big, 5 * big,
+                             None) == 3
+    assert L.vda_frame_inverse(big, None, 0, 1, 8, 16, 64, 2 * big, None) == 3
     assert L.vda_state_scan(big, 2 * big, 4, 2, 64, 16, 0, 3 * big, 4 * big, None) == 3
     assert L.vda_readout(big, 2 * big, 3 * big, 4 * big, 4, 64, 2, 64, 16, 0, 5 * big, None) == 3
 

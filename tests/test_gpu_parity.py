@@ -53,17 +53,27 @@ def test_stats_stage(V, dtype, dk, dv):
     x = I.make_inputs(w)
     xo = oracle_inputs(w, x)
     d = device_inputs(w, x)
-    for splits in (1, 3):
-        _log(f"stats dtype={dtype} dk={dk} dv={dv} splits={splits}")
-        A_part, B_part = V.frame_stats(d["k"], d["v"], d["beta"], splits=splits)
+    # (tail_frames, splits): no split, every frame in 3 ranges, the last two
+    # frames in 3 ranges
+    for tail, splits in ((0, 1), (6, 3), (2, 3)):
+        _log(f"stats dtype={dtype} dk={dk} dv={dv} tail={tail} splits={splits}")
+        A_part, B_part = V.frame_stats(d["k"], d["v"], d["beta"], splits=splits, tail_frames=tail)
         torch.cuda.synchronize()
-        A = A_part.double().sum(0).cpu().numpy()
-        B = B_part.double().sum(0).cpu().numpy()
+        assert A_part.shape[0] == 6 + tail * (splits - 1)
+        A = V.fold_partials(A_part.double(), 6, tail, splits).view(2, 3, dk, dk).cpu().numpy()
+        B = V.fold_partials(B_part.double(), 6, tail, splits).view(2, 3, dv, dk).cpu().numpy()
         for h in range(2):
             As, Bs = O.head_statistics(xo["k"][h], xo["v"][h], xo["beta"][h])
             tol = 1e-5 if dtype == "f32" else 1e-2
             assert rel_max_err(A[h], As) < tol
             assert rel_max_err(B[h], Bs) < tol
+            if dtype == "bf16":  # off-diagonal 16 x 16 blocks: upper ones mirrored
+                for t in range(3):
+                    for i in range(dk // 16):
+                        for j in range(i + 1, dk // 16):
+                            blk = A[h, t, 16 * i:16 * i + 16, 16 * j:16 * j + 16]
+                            assert np.array_equal(A[h, t, 16 * j:16 * j + 16, 16 * i:16 * i + 16],
+                                                  blk.T)
 
 
 @pytest.mark.parametrize("dk", [32, 64, 128])
@@ -78,15 +88,28 @@ def test_inverse_stage(V, dk):
     beta[1] *= 10.0                      # stronger writes, larger condition number
     A = np.stack([O.frame_statistics(K[i], K[i][:, :1], beta[i])[0] for i in range(count)])
     expect = np.stack([O.frame_transition(A[i], np.zeros((1, dk)))[0] for i in range(count)])
-    for splits in (1, 2):
-        _log(f"inverse dk={dk} splits={splits}")
-        parts = np.stack([A / splits] * splits).astype(np.float32)
+    # (tail_frames, splits): no split, every frame in 2 ranges, the last
+    # three frames in 3 ranges.  Partial s >= 1 of split frame i is matrix
+    # i + s * tail.
+    for tail, splits in ((0, 1), (count, 2), (3, 3)):
+        _log(f"inverse dk={dk} tail={tail} splits={splits}")
+        split = np.arange(count) >= count - tail if splits > 1 else np.zeros(count, bool)
+        nparts = count + tail * (splits - 1) if splits > 1 else count
+        parts = np.empty((nparts, dk, dk), np.float32)
+        Bp = np.empty((nparts, 32, dk), np.float32)
+        Bsum = np.empty((count, 32, dk), np.float32)
+        for i in range(count):
+            n = splits if split[i] else 1
+            idx = [i] + [i + s * tail for s in range(1, n)]
+            for s, m in enumerate(idx):
+                parts[m] = A[i] / n
+                Bp[m] = float(s + 1)
+            Bsum[i] = float(sum(range(1, n + 1)))
         A_dev = to_device(parts, "f32")
-        Bp = np.stack([np.full((count, 32, dk), float(s + 1), np.float32) for s in range(splits)])
         B_dev = to_device(Bp, "f32")
-        Inv = V.frame_inverse(A_dev, B_dev)
+        Inv = V.frame_inverse(A_dev, B_dev, count=count, tail_frames=tail, splits=splits)
         torch.cuda.synchronize()
-        np.testing.assert_array_equal(B_dev[0].cpu().numpy(), Bp.sum(0))
+        np.testing.assert_array_equal(B_dev[:count].cpu().numpy(), Bsum)
         got = Inv.double().cpu().numpy()
         np.testing.assert_array_equal(got[0], np.eye(dk))
         for i in range(count):
@@ -331,11 +354,18 @@ def test_deterministic_and_guarded(V):
 
 def _staged_forward(V, d, exact_f32):
     """The forward pass through the stage entry points, with the library's
-    default split of the statistics step."""
-    A_part, B_part = V.frame_stats(d["k"], d["v"], d["beta"])
-    Inv = V.frame_inverse(A_part, B_part, Inv=A_part[0])
-    Sf, Sr = V.state_scan(Inv, B_part[0], exact_f32=exact_f32)
-    return V.readout(d["q"], Sf, Sr, d["gate"]), A_part.shape[0]
+    default split plan of the statistics step.  Returns the output and the
+    plan's split count."""
+    H, F, N, d_k = d["k"].shape
+    d_v = d["v"].shape[-1]
+    tail, splits = V.default_split_plan(F, N, H, d_k, d_v, exact_f32)
+    A_part, B_part = V.frame_stats(d["k"], d["v"], d["beta"], splits=splits, tail_frames=tail)
+    count = H * F
+    Inv = V.frame_inverse(A_part, B_part, count=count, tail_frames=tail, splits=splits,
+                          Inv=A_part[:count])
+    Sf, Sr = V.state_scan(Inv.view(H, F, d_k, d_k), B_part[:count].view(H, F, d_v, d_k),
+                          exact_f32=exact_f32)
+    return V.readout(d["q"], Sf, Sr, d["gate"]), splits
 
 
 def test_stages_compose_to_forward(V):
