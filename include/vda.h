@@ -175,7 +175,10 @@ int vda_frame_inverse(const float* A_part, float* B_part, int tail_frames, int s
  *     reverse  R_{F+1} = 0, R_t = (R_{t+1} + B_t) Inv_t,  S_rev[h][t] = R_{t+1}
  * (frames numbered 1..F here; array index t-1).  S_fwd, S_rev are
  * [H][F][d_v][d_k] fp32; Inv is [H][F][d_k][d_k] and must be symmetric (as
- * (I + A_t)^{-1} is): element Inv[k][j] is read from Inv[j][k].
+ * (I + A_t)^{-1} is): with is_f32 != 0 element Inv[k][j] is read from
+ * Inv[j][k]; with is_f32 == 0 only the 16 x 16 blocks on and above the
+ * diagonal are read and each block below is taken as the transpose of its
+ * mirror.
  * The state is fp32.  is_f32 != 0: fp32 matrix products.  is_f32 == 0 (the
  * bf16 storage path): each product operand is split into two bf16 parts
  * (hi + lo) and three bf16 matrix products are accumulated in fp32, about

@@ -73,6 +73,15 @@ __device__ __forceinline__ void store_b128(__amdgpu_buffer_rsrc_t r, uint32_t by
   __builtin_amdgcn_raw_buffer_store_b128(v, r, (int)byte_off, 0, 0);
 }
 
+// 16-byte store of streamed output (cache policy sc0 | nt | sc1: written
+// through at system scope, not kept).  An output much larger than the
+// caches is then written back while it is produced, instead of being left
+// dirty for the next kernel's reads to evict.
+__device__ __forceinline__ void store_b128_stream(__amdgpu_buffer_rsrc_t r, uint32_t byte_off,
+                                                  u32x4 v) {
+  __builtin_amdgcn_raw_buffer_store_b128(v, r, (int)byte_off, 0, 1 | 2 | 16);
+}
+
 // Workgroup-uniform integer kept in a scalar register.  Integer division by
 // a runtime value is expanded on the vector ALU; without this the compiler
 // may treat values derived from it (such as buffer descriptors) as varying

@@ -137,7 +137,7 @@ void readout_bf16_kernel(const uint16_t* __restrict__ Q, const float* __restrict
         const uint32_t b1 = pack_bf16x2(acc[2 * m + 1][2] * scale, acc[2 * m + 1][3] * scale);
         const auto s0 = __builtin_amdgcn_permlane16_swap(a0, b0, false, false);
         const auto s1 = __builtin_amdgcn_permlane16_swap(a1, b1, false, false);
-        store_b128(orsrc, off + m * 64u, u32x4{s0[0], s1[0], s0[1], s1[1]});
+        store_b128_stream(orsrc, off + m * 64u, u32x4{s0[0], s1[0], s0[1], s1[1]});
       }
     }
   }
