@@ -67,7 +67,7 @@ def kernel_bytes(w, heads=None):
 # Kernel of each stage, and the sources whose change makes counters taken
 # on it stale.
 KERNEL_OF = {"frame_stats": "stats_bf16_kernel", "frame_inverse": "inverse_kernel",
-             "state_scan": "scan_kernel", "readout": "readout_bf16_kernel"}
+             "state_scan": "scan_bf16_kernel", "readout": "readout_bf16_kernel"}
 SOURCE_OF = {"frame_stats": ("vda_stats.hip",),
              "frame_inverse": ("vda_inverse.hip", "vda_inverse_body.h"),
              "state_scan": ("vda_scan.hip",), "readout": ("vda_readout.hip",)}
