@@ -25,6 +25,14 @@ with no blocking, fusion or reordering beyond what the equations state:
       y = g * RMSNorm(o),  RMSNorm(o) = o / sqrt(mean_j o_j^2 + eps),
   over the d_v channels of one token of one head, no learnable weight.
 
+The full gather (the *_ex functions at the end) adds what the core leaves
+at its special values: the channel-wise decay alpha_t (S_bar_t =
+S_{t-1} Diag(alpha_t), Eq. 3a/5 and A.1), the text state S_T starting both
+scans at S_T / 2 (Eq. 1b), the local window [l_t, h_t] with the decay bridge
+of Eq. A.4, and, as a selectable rule, the frozen-state additive update of
+Eq. 3c with the 1/sqrt(U) key scaling the paper compares against (Section
+3.2, Appendix A.2).
+
 Index convention: the paper numbers frames 1..F; arrays here use 0..F-1, so
 array frame i is the paper's frame t = i + 1.
 
@@ -227,3 +235,133 @@ def frozen_state_update(S_bar, A, B, U: int | None = None) -> np.ndarray:
     if U is not None:
         A, B = A / U, B / np.sqrt(U)
     return S_bar @ (np.eye(A.shape[0]) - A) + B
+
+
+# ----------------------------------------------------------------------------
+# The full gather: decay, local window, text state; the frozen-state rule
+# ----------------------------------------------------------------------------
+#
+# Section 2.2 (Eq. 1a, 1b), Section 3.1 (Eq. 3c), Appendix A.1 (Eq. A.1),
+# Appendix A.3 (Eq. A.4) and Algorithm 1, steps 3-7.  The core functions
+# above are the special case alpha = 1, window = own frame, S_T = 0 and the
+# joint rule.
+
+RULES = ("joint", "frozen")
+
+
+def decayed_frame_update(S_prev, A, B, alpha=None, rule="joint", U=None):
+    """One frame of either rule from the entering state S_prev.
+
+    The decayed state is Sbar = S_prev Diag(alpha) (alpha per key channel,
+    None = 1).  'joint': Eq. 5, S = (Sbar + B)(I + A)^{-1} (so S = S_prev M + J
+    with M = Diag(alpha)(I + A)^{-1}, J = B (I + A)^{-1}, Eq. A.1).  'frozen':
+    Eq. 3c with the 1/sqrt(U) key scaling, S = Sbar (I - A/U) + B/sqrt(U).
+    """
+    S_bar = S_prev if alpha is None else S_prev * np.asarray(alpha)[None, :]
+    if rule == "joint":
+        return joint_frame_update(S_bar, A, B)
+    if rule == "frozen":
+        return frozen_state_update(S_bar, A, B, U)
+    raise ValueError(f"unknown rule {rule!r}")
+
+
+def scan_states_ex(As, Bs, S0, alphas=None, rule="joint", U=None):
+    """decayed_frame_update over frames 0..F-1 in order from S0.
+    Returns [F+1, d_v, d_k]; element j is the state after the first j frames."""
+    F = As.shape[0]
+    out = np.empty((F + 1,) + S0.shape)
+    out[0] = S0
+    for t in range(F):
+        a = None if alphas is None else alphas[t]
+        out[t + 1] = decayed_frame_update(out[t], As[t], Bs[t], a, rule, U)
+    return out
+
+
+def forward_states_ex(As, Bs, S0, alphas=None, rule="joint", U=None):
+    """P[j] = state through frames 1..j (paper numbering), P[0] = S0."""
+    return scan_states_ex(As, Bs, S0, alphas, rule, U)
+
+
+def reverse_states_ex(As, Bs, S0, alphas=None, rule="joint", U=None):
+    """R[j] = state through frames F..j (paper numbering) for j = 1..F,
+    R[F+1] = S0; R[0] unused (zero).  Each frame applies its own decay."""
+    F = Bs.shape[0]
+    a_rev = None if alphas is None else alphas[::-1]
+    rev = scan_states_ex(As[::-1], Bs[::-1], S0, a_rev, rule, U)
+    R = np.zeros((F + 2,) + S0.shape)
+    for j in range(1, F + 2):
+        R[j] = rev[F + 1 - j]
+    return R
+
+
+def local_windows(F: int, chunk: int = 1, radius: int = 0, offset: int = 0):
+    """Local Softmax window [l_t, h_t] of every interior frame t = 1..F.
+
+    Frames are grouped into chunks of `chunk` consecutive frames, counted
+    from `offset` positions before interior frame 1 (for example the leading
+    anchor frame); a query frame's window is its own chunk and `radius`
+    chunks on each side (Section 2.1: chunks of five latent frames, radius
+    one), clipped to the interior frames (Appendix A.3).  Returns a list of
+    (l_t, h_t) in paper numbering.
+    """
+    out = []
+    for t in range(1, F + 1):
+        c = (t - 1 + offset) // chunk
+        lo = (c - radius) * chunk - offset + 1
+        hi = (c + radius + 1) * chunk - offset
+        out.append((max(1, lo), min(F, hi)))
+    return out
+
+
+def gathered_states_ex(As, Bs, S_T=None, alphas=None, windows=None, rule="joint", U=None):
+    """Eq. A.4: S~_t = P_{l_t-1} Diag(prod_{r=l_t..t} alpha_r)
+                     + R_{h_t+1} Diag(prod_{r=t..h_t} alpha_r),
+    with both scans started from S_T / 2 (Eq. 1b).  windows: list of
+    (l_t, h_t) (default: the own frame).  Returns [F, d_v, d_k] (array frame
+    i is paper frame i + 1)."""
+    F, d_v, d_k = Bs.shape
+    S0 = np.zeros((d_v, d_k)) if S_T is None else 0.5 * np.asarray(S_T)
+    P = forward_states_ex(As, Bs, S0, alphas, rule, U)
+    R = reverse_states_ex(As, Bs, S0, alphas, rule, U)
+    if windows is None:
+        windows = [(t, t) for t in range(1, F + 1)]
+    out = np.empty((F, d_v, d_k))
+    for t in range(1, F + 1):
+        lo, hi = windows[t - 1]
+        df = np.ones(d_k)
+        dr = np.ones(d_k)
+        if alphas is not None:
+            for r in range(lo, t + 1):
+                df = df * alphas[r - 1]
+            for r in range(t, hi + 1):
+                dr = dr * alphas[r - 1]
+        out[t - 1] = P[lo - 1] * df[None, :] + R[hi + 1] * dr[None, :]
+    return out
+
+
+def head_forward_ex(q, k, v, beta, gate: float, alpha=None, S_T=None, windows=None,
+                    rule="joint", eps: float = RMS_EPS) -> np.ndarray:
+    """The full linear branch for one head problem (Algorithm 1, steps 3-7):
+    q, k [F,N,d_k], v [F,N,d_v], beta [F,N], alpha [F,d_k] or None, S_T
+    [d_v,d_k] or None, windows as in gathered_states_ex -> y [F,N,d_v]."""
+    if np.any(beta < 0):
+        raise ValueError("write strengths must be non-negative")
+    As, Bs = head_statistics(k, v, beta)
+    St = gathered_states_ex(As, Bs, S_T, alpha, windows, rule, U=k.shape[1])
+    y = np.empty(q.shape[:2] + (v.shape[2],))
+    for t in range(q.shape[0]):
+        y[t] = rmsnorm_gate(readout(St[t], q[t]), gate, eps)
+    return y
+
+
+def vda_forward_ex(q, k, v, beta, gate, alpha=None, S_T=None, chunk=1, radius=0, offset=0,
+                   rule="joint", eps: float = RMS_EPS) -> np.ndarray:
+    """All head problems: alpha [H,F,d_k] or None, S_T [H,d_v,d_k] or None,
+    one window layout for every head."""
+    H, F = q.shape[0], q.shape[1]
+    windows = local_windows(F, chunk, radius, offset)
+    return np.stack([
+        head_forward_ex(q[h], k[h], v[h], beta[h], float(gate[h]),
+                        None if alpha is None else alpha[h],
+                        None if S_T is None else S_T[h], windows, rule, eps)
+        for h in range(H)])

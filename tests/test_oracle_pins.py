@@ -407,6 +407,156 @@ def pin_sampled_matches_full():
     np.testing.assert_allclose(ys, y[frames, toks], rtol=1e-13, atol=1e-14)
 
 
+# ----------------------------------------------------------------------------
+# Pins of the full gather (decay, window, text state) and the frozen rule
+# ----------------------------------------------------------------------------
+
+def _random_alpha(rng, F, d_k, low=0.6):
+    return low + (1.0 - low) * rng.random((F, d_k))
+
+
+def pin_ex_reduces_to_core():
+    """alpha = 1, own-frame window, no text state, joint rule: the extended
+    operator is the core operator (itself pinned above)."""
+    rng = _rng(31)
+    q, k, v, beta = _random_clip(rng, F=6, N=7, d_k=5, d_v=4)
+    y = O.head_forward(q, k, v, beta, 0.7)
+    ye = O.head_forward_ex(q, k, v, beta, 0.7)
+    np.testing.assert_allclose(ye, y, rtol=1e-13, atol=1e-14)
+    yw = O.head_forward_ex(q, k, v, beta, 0.7, alpha=np.ones((6, 5)),
+                           windows=O.local_windows(6, 1, 0, 0))
+    np.testing.assert_allclose(yw, y, rtol=1e-13, atol=1e-14)
+
+
+def pin_decay_single_token_is_token_rule():
+    """With one token per frame the decayed joint update is the token-wise
+    delta rule of Eq. 2 with decay alpha and write strength
+    beta' = beta / (1 + beta |k|^2) (Sherman-Morrison), brute force per token."""
+    rng = _rng(32)
+    F, d_k, d_v = 6, 4, 3
+    keys = _unit_rows(rng.standard_normal((F, d_k))) * 1.3
+    vals = rng.standard_normal((F, d_v))
+    betas = rng.random(F)
+    alphas = _random_alpha(rng, F, d_k)
+    S0 = rng.standard_normal((d_v, d_k))
+    As = np.stack([betas[t] * np.outer(keys[t], keys[t]) for t in range(F)])
+    Bs = np.stack([betas[t] * np.outer(vals[t], keys[t]) for t in range(F)])
+    P = O.forward_states_ex(As, Bs, S0, alphas)
+    bprime = betas / (1.0 + betas * np.sum(keys * keys, axis=1))
+    for j in range(1, F + 1):
+        ref = O.token_delta_rule(S0, keys[:j], vals[:j], bprime[:j], alphas[:j])
+        np.testing.assert_allclose(P[j], ref, rtol=1e-11, atol=1e-12)
+
+
+def pin_bridge_is_scan_without_writes():
+    """Appendix A.3: the bridge decays the gathered state over the skipped
+    local frames without their writes.  So each side of S~_t equals a scan
+    that reaches frame t with the window's frames given zero writes (beta = 0
+    there: A = B = 0, each such frame only decays)."""
+    rng = _rng(33)
+    F, N, d_k, d_v = 11, 5, 4, 3
+    q, k, v, beta = _random_clip(rng, F=F, N=N, d_k=d_k, d_v=d_v)
+    alphas = _random_alpha(rng, F, d_k)
+    S_T = rng.standard_normal((d_v, d_k))
+    As, Bs = O.head_statistics(k, v, beta)
+    windows = O.local_windows(F, 3, 1, 1)
+    St = O.gathered_states_ex(As, Bs, S_T, alphas, windows)
+    for t in range(1, F + 1):
+        lo, hi = windows[t - 1]
+        Af, Bf = As.copy(), Bs.copy()
+        Af[lo - 1:], Bf[lo - 1:] = 0.0, 0.0           # no writes from frame l_t on
+        fwd = O.scan_states_ex(Af[:t], Bf[:t], 0.5 * S_T, alphas[:t])[t]
+        Ar, Br = As.copy(), Bs.copy()
+        Ar[:hi], Br[:hi] = 0.0, 0.0                   # no writes up to frame h_t
+        rev = O.scan_states_ex(Ar[t - 1:][::-1], Br[t - 1:][::-1], 0.5 * S_T,
+                               alphas[t - 1:][::-1])[F - t + 1]
+        np.testing.assert_allclose(St[t - 1], fwd + rev, rtol=1e-12, atol=1e-13)
+
+
+def pin_text_state_counted_once():
+    """Eq. 1b: with no writes (beta = 0) and alpha = 1 every frame reads
+    (S_T/2 + S_T/2) q = S_T q, for any window; with decay the two halves are
+    S_T/2 decayed over frames 1..t and over t..F (closed form)."""
+    rng = _rng(34)
+    F, N, d_k, d_v = 7, 3, 4, 5
+    q, k, v, _ = _random_clip(rng, F=F, N=N, d_k=d_k, d_v=d_v)
+    beta = np.zeros((F, N))
+    S_T = rng.standard_normal((d_v, d_k))
+    As, Bs = O.head_statistics(k, v, beta)
+    for windows in (None, O.local_windows(F, 2, 1, 0)):
+        St = O.gathered_states_ex(As, Bs, S_T, None, windows)
+        np.testing.assert_allclose(St, np.broadcast_to(S_T, St.shape), rtol=1e-14, atol=1e-14)
+    alphas = _random_alpha(rng, F, d_k)
+    St = O.gathered_states_ex(As, Bs, S_T, alphas, O.local_windows(F, 2, 1, 1))
+    for t in range(1, F + 1):
+        ref = 0.5 * S_T * np.prod(alphas[:t], axis=0)[None, :] \
+            + 0.5 * S_T * np.prod(alphas[t - 1:], axis=0)[None, :]
+        np.testing.assert_allclose(St[t - 1], ref, rtol=1e-13, atol=1e-14)
+
+
+def pin_frozen_rule_is_scaled_token_sum():
+    """Eq. 3a with every key scaled by 1/sqrt(U) (SANA-WM's scaling, Section
+    3.2): Sbar + sum_u beta_u (v_u - Sbar k'_u) k'_u^T with k' = k / sqrt(U),
+    summed token by token, is the frozen rule of Eq. 3c with A/U, B/sqrt(U)."""
+    rng = _rng(35)
+    K, V, beta = _random_frame(rng, U=9, d_k=5, d_v=4)
+    S_prev = rng.standard_normal((4, 5))
+    alpha = _random_alpha(rng, 1, 5)[0]
+    S_bar = S_prev * alpha[None, :]
+    Ks = K / np.sqrt(K.shape[0])
+    S = S_bar.copy()
+    for u in range(K.shape[0]):
+        S = S + beta[u] * np.outer(V[u] - S_bar @ Ks[u], Ks[u])
+    A, B = O.frame_statistics(K, V, beta)
+    got = O.decayed_frame_update(S_prev, A, B, alpha, rule="frozen", U=K.shape[0])
+    np.testing.assert_allclose(got, S, rtol=1e-12, atol=1e-13)
+
+
+def pin_frozen_rule_non_expansive_with_scaling():
+    """Appendix A.2: with unit keys and write strengths in [0, 1], the scaled
+    additive factor I - A/U has eigenvalues in [0, 1], so the frozen rule's
+    inherited-state transition does not expand (checked on differences of
+    entering states), while the unscaled factor I - A can (aligned keys)."""
+    rng = _rng(36)
+    U, d_k, d_v = 12, 4, 3
+    base = _unit_rows(rng.standard_normal(d_k))
+    K = _unit_rows(base[None, :] + 0.05 * rng.standard_normal((U, d_k)))
+    V = rng.standard_normal((U, d_v))
+    beta = 0.5 + 0.5 * rng.random(U)
+    A, B = O.frame_statistics(K, V, beta)
+    ev = np.linalg.eigvalsh(np.eye(d_k) - A / U)
+    assert ev.min() >= -1e-12 and ev.max() <= 1 + 1e-12
+    assert np.linalg.eigvalsh(np.eye(d_k) - A).min() < -1.0   # unscaled: expands
+    for _ in range(5):
+        S1, S2 = rng.standard_normal((2, d_v, d_k))
+        d1 = O.decayed_frame_update(S1, A, B, rule="frozen", U=U)
+        d2 = O.decayed_frame_update(S2, A, B, rule="frozen", U=U)
+        assert np.linalg.norm(d1 - d2) <= np.linalg.norm(S1 - S2) * (1 + 1e-12)
+
+
+def pin_local_windows_paper_layout():
+    """Section 2.1: chunks of five latent frames, each query chunk sees itself
+    and one chunk on each side, a 15-frame window away from the sequence
+    ends; every window holds its own frame and all frames of its chunk share
+    it; windows are clipped to the interior frames (Appendix A.3)."""
+    F = 40
+    w = O.local_windows(F, chunk=5, radius=1, offset=1)
+    for t in range(1, F + 1):
+        lo, hi = w[t - 1]
+        assert 1 <= lo <= t <= hi <= F
+        first = max(1, 5 * (t // 5))       # first interior frame of t's chunk
+        assert w[t - 1] == w[first - 1]
+        if lo > 1 and hi < F:
+            assert hi - lo + 1 == 15
+    # a brute-force membership check: frame r is in t's window iff their
+    # chunks differ by at most the radius
+    for t in range(1, F + 1):
+        lo, hi = w[t - 1]
+        inside = [r for r in range(1, F + 1) if abs(r // 5 - t // 5) <= 1]
+        assert (lo, hi) == (min(inside), max(inside))
+    assert O.local_windows(4, 1, 0, 0) == [(1, 1), (2, 2), (3, 3), (4, 4)]
+
+
 PINS = [f for name, f in sorted(globals().items()) if name.startswith("pin_")]
 
 
@@ -488,7 +638,54 @@ def _mut_rms_gate_inside(o, gate, eps=O.RMS_EPS):
     return og / np.sqrt(np.mean(og * og, axis=-1, keepdims=True) + eps)
 
 
+def _mut_decay_after_update(S_prev, A, B, alpha=None, rule="joint", U=None):
+    if rule == "joint":
+        S = O.joint_frame_update(S_prev, A, B)
+    else:
+        S = O.frozen_state_update(S_prev, A, B, U)
+    return S if alpha is None else S * np.asarray(alpha)[None, :]
+
+
+def _mut_frozen_unscaled(S_prev, A, B, alpha=None, rule="joint", U=None):
+    S_bar = S_prev if alpha is None else S_prev * np.asarray(alpha)[None, :]
+    if rule == "joint":
+        return O.joint_frame_update(S_bar, A, B)
+    return O.frozen_state_update(S_bar, A, B, None)
+
+
+def _mut_bridge_skips_own_decay(As, Bs, S_T=None, alphas=None, windows=None, rule="joint", U=None):
+    F, d_v, d_k = Bs.shape
+    S0 = np.zeros((d_v, d_k)) if S_T is None else 0.5 * np.asarray(S_T)
+    P = O.forward_states_ex(As, Bs, S0, alphas, rule, U)
+    R = O.reverse_states_ex(As, Bs, S0, alphas, rule, U)
+    windows = windows or [(t, t) for t in range(1, F + 1)]
+    out = np.empty((F, d_v, d_k))
+    for t in range(1, F + 1):
+        lo, hi = windows[t - 1]
+        df = np.ones(d_k) if alphas is None else np.prod(alphas[lo - 1:t - 1], axis=0)
+        dr = np.ones(d_k) if alphas is None else np.prod(alphas[t - 1:hi], axis=0)
+        out[t - 1] = P[lo - 1] * df[None, :] + R[hi + 1] * dr[None, :]
+    return out
+
+
+def _mut_text_state_not_halved(As, Bs, S_T=None, alphas=None, windows=None, rule="joint", U=None):
+    S2 = None if S_T is None else 2.0 * np.asarray(S_T)
+    return _ORIG_GATHER_EX(As, Bs, S2, alphas, windows, rule, U)
+
+
+def _mut_windows_ignore_offset(F, chunk=1, radius=0, offset=0):
+    return _ORIG_WINDOWS(F, chunk, radius, 0)
+
+
+_ORIG_GATHER_EX = O.gathered_states_ex
+_ORIG_WINDOWS = O.local_windows
+
 MUTANTS = [
+    ("decayed_frame_update", _mut_decay_after_update),
+    ("decayed_frame_update", _mut_frozen_unscaled),
+    ("gathered_states_ex", _mut_bridge_skips_own_decay),
+    ("gathered_states_ex", _mut_text_state_not_halved),
+    ("local_windows", _mut_windows_ignore_offset),
     ("frame_statistics", _mut_stats_no_beta),
     ("frame_statistics", _mut_stats_beta_squared),
     ("joint_frame_update", _mut_update_no_identity),
