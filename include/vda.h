@@ -107,6 +107,78 @@ int vda_forward_f32(const float* q, const float* k, const float* v,
                     float* out, hipStream_t stream);
 
 /* ------------------------------------------------------------------------- */
+/* The full operator: decay, local window, text state, and the frozen rule    */
+/* ------------------------------------------------------------------------- */
+
+/* Frame update rule. */
+typedef enum {
+  /* Eq. 5 (Sec. 3.2): S_t = (Sbar_t + B_t)(I + A_t)^{-1}, the VDA joint solve. */
+  VDA_RULE_JOINT = 0,
+  /* Eq. 3c (Sec. 3.1) with every key scaled by 1/sqrt(U), U = N tokens per
+   * frame (Sec. 3.2, App. A.2): S_t = Sbar_t (I - A_t / U) + B_t / sqrt(U),
+   * the frozen-state additive update the paper compares against. */
+  VDA_RULE_FROZEN_SCALED = 1
+} vda_rule;
+
+/*
+ * Options of vda_forward_ex.  A NULL pointer to this struct, or all fields at
+ * their defaults (rule 0, NULL pointers, chunk 1, radius 0, offset 0), give
+ * exactly vda_forward.
+ *  - rule: a vda_rule.
+ *  - alpha: NULL (alpha = 1) or a DEVICE pointer to [H][F][d_k] fp32 channel
+ *    decays in [0, 1] (16-byte aligned), one per frame and key channel:
+ *    Sbar_t = S_{t-1} Diag(alpha_t) (Eq. 5, A.1; Eq. 3a for the frozen rule),
+ *    and the decay bridge of Eq. A.4.  Values outside [0, 1] are not checked.
+ *  - text_state: NULL (zero) or a DEVICE pointer to [H][d_v][d_k] fp32 S_T:
+ *    both scans start from S_T / 2 (Eq. 1b).
+ *  - window_chunk, window_radius, window_offset: the local Softmax window of
+ *    each frame (Sec. 2.1; App. A.3).  Frames are grouped into chunks of
+ *    window_chunk >= 1 consecutive frames, counted from window_offset
+ *    (0 <= offset < chunk) positions before frame 0 (for example a leading
+ *    anchor frame).  Frame t's window [l_t, h_t] is its own chunk and
+ *    window_radius >= 0 chunks on each side, clipped to [0, F).  The paper's
+ *    setting is chunk 5, radius 1 (offset 1 with one leading anchor).
+ */
+typedef struct vda_options {
+  int rule;
+  const float* alpha;
+  const float* text_state;
+  int window_chunk;
+  int window_radius;
+  int window_offset;
+} vda_options;
+
+/*
+ * vda_forward_ex -- the linear branch of Algorithm 1, steps 3-7, with the
+ * options above (bf16 storage; otherwise as vda_forward).  Per head, with
+ * frames numbered 0..F-1 here:
+ *     P_0 = R_F = S_T / 2,
+ *     P_{j+1} = update(P_j, frame j),   R_j = update(R_{j+1}, frame j),
+ * where update applies the rule to Sbar = S Diag(alpha_j) with A_j, B_j (so
+ * P_j is the forward state after frames 0..j-1 and R_j the reverse state
+ * after frames F-1..j), and the gather of Eq. A.4 reads
+ *     S~_t = P_{l_t} Diag(prod_{r=l_t..t} alpha_r)
+ *          + R_{h_t+1} Diag(prod_{r=t..h_t} alpha_r),
+ *     out[t][u] = gate * RMSNorm(S~_t q[t][u]).  A window
+ * that covers the whole clip is evaluated as written (both sides read the
+ * decayed initial state); callers that bypass the linear branch in that case
+ * do so themselves.  The frozen rule never splits frames (its statistics are
+ * used directly), so its workspace has P = H*F.  Errors: VDA_ERR_UNSUPPORTED
+ * for an unknown rule, VDA_ERR_SIZE for invalid window fields, VDA_ERR_ALIGN,
+ * VDA_ERR_OVERLAP if out overlaps alpha or text_state.
+ */
+int vda_forward_ex(const void* q, const void* k, const void* v,
+                   const float* beta, const float* gate,
+                   int F, int N, int H, int d_k, int d_v,
+                   const vda_options* opts, void* out, hipStream_t stream);
+
+/* vda_forward_ex_f32 -- the same with fp32 storage (as vda_forward_f32). */
+int vda_forward_ex_f32(const float* q, const float* k, const float* v,
+                       const float* beta, const float* gate,
+                       int F, int N, int H, int d_k, int d_v,
+                       const vda_options* opts, float* out, hipStream_t stream);
+
+/* ------------------------------------------------------------------------- */
 /* Stage interface: the same kernels as vda_forward, one step per call, with  */
 /* caller-owned fp32 work buffers (all device pointers, 16-byte aligned).     */
 /* ------------------------------------------------------------------------- */

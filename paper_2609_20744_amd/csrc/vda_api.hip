@@ -193,33 +193,67 @@ Workspace workspace_layout(int F, int H, int d_k, int d_v, vda::SplitPlan plan) 
   return w;
 }
 
+// Options of the full operator, validated into *out; a null vda_options is
+// the core operator.
+int check_options(const vda_options* o, vda_options* out) {
+  vda_options d;
+  d.rule = VDA_RULE_JOINT;
+  d.alpha = nullptr;
+  d.text_state = nullptr;
+  d.window_chunk = 1;
+  d.window_radius = 0;
+  d.window_offset = 0;
+  if (o) d = *o;
+  if (d.rule != VDA_RULE_JOINT && d.rule != VDA_RULE_FROZEN_SCALED) return VDA_ERR_UNSUPPORTED;
+  if (d.window_chunk < 1 || d.window_radius < 0 || d.window_offset < 0 ||
+      d.window_offset >= d.window_chunk)
+    return VDA_ERR_SIZE;
+  if (!aligned(d.alpha, 16) || !aligned(d.text_state, 4)) return VDA_ERR_ALIGN;
+  *out = d;
+  return VDA_OK;
+}
+
 int forward_impl(bool is_f32, const void* q, const void* k, const void* v, const float* beta,
-                 const float* gate, int F, int N, int H, int d_k, int d_v, void* out,
-                 hipStream_t stream) {
+                 const float* gate, int F, int N, int H, int d_k, int d_v,
+                 const vda_options* opts, void* out, hipStream_t stream) {
   if (!q || !k || !v || !beta || !gate || !out) return VDA_ERR_NULL;
   int st = check_shape(F, N, H, d_k, d_v, true);
   if (st != VDA_OK) return st;
   if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 16) ||
       !aligned(beta, 4) || !aligned(gate, 4))
     return VDA_ERR_ALIGN;
+  vda_options o;
+  st = check_options(opts, &o);
+  if (st != VDA_OK) return st;
+  // The window arithmetic stays within 32 bits.
+  if ((long long)F + 2LL * (o.window_radius + 1) * o.window_chunk > 0x3fffffffLL) return VDA_ERR_SIZE;
   const size_t es = is_f32 ? 4 : 2;
   const size_t tok = (size_t)H * F * N;
   const Range ro = range_of(out, tok * d_v * es);
   if (overlaps(ro, range_of(q, tok * d_k * es)) || overlaps(ro, range_of(k, tok * d_k * es)) ||
       overlaps(ro, range_of(v, tok * d_v * es)) || overlaps(ro, range_of(beta, tok * 4)) ||
-      overlaps(ro, range_of(gate, (size_t)H * 4)))
+      overlaps(ro, range_of(gate, (size_t)H * 4)) ||
+      (o.alpha && overlaps(ro, range_of(o.alpha, (size_t)H * F * d_k * 4))) ||
+      (o.text_state && overlaps(ro, range_of(o.text_state, (size_t)H * d_v * d_k * 4))))
     return VDA_ERR_OVERLAP;
+  const bool frozen = o.rule == VDA_RULE_FROZEN_SCALED;
 
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return VDA_ERR_HIP;
   // Heads narrower than 32 channels run as zero-padded 32-channel heads; the
-  // padded q, k, v and output live after the state buffers.
+  // padded q, k, v, output, alpha and text state live after the state buffers.
   const int pk = padded_dim(d_k), pv = padded_dim(d_v);
-  const vda::SplitPlan plan = default_plan(dev, F, N, H, pk, pv, is_f32);
+  // The frozen rule reads the statistics directly, so its frames are not split.
+  const vda::SplitPlan plan =
+      frozen ? vda::SplitPlan{0, 1} : default_plan(dev, F, N, H, pk, pv, is_f32);
   const Workspace w = workspace_layout(F, H, pk, pv, plan);
   const size_t qk_pad = pk != d_k ? round_up(tok * pk * es, 256) : 0;
   const size_t v_pad = pv != d_v ? round_up(tok * pv * es, 256) : 0;
-  const size_t ws_bytes = round_up(w.total, 256) + 2 * qk_pad + 2 * v_pad;
+  const bool pad_any = pk != d_k || pv != d_v;
+  const size_t a_pad = pk != d_k && o.alpha ? round_up((size_t)H * F * pk * 4, 256) : 0;
+  const size_t t_pad = pad_any && o.text_state ? round_up((size_t)H * pv * pk * 4, 256) : 0;
+  const size_t t_tmp = pad_any && o.text_state ? round_up((size_t)H * d_v * pk * 4, 256) : 0;
+  const size_t ws_bytes = round_up(w.total, 256) + 2 * qk_pad + 2 * v_pad + a_pad + t_pad + t_tmp;
   const int wsi = acquire_workspace(dev, ws_bytes, stream);
   if (wsi < 0) return VDA_ERR_NOMEM;
   char* base = static_cast<char*>(workspace_ptr(dev, wsi));
@@ -233,6 +267,8 @@ int forward_impl(bool is_f32, const void* q, const void* k, const void* v, const
   const void* kx = k;
   const void* vx = v;
   void* ox = out;
+  const float* alpha_x = o.alpha;
+  const float* ts_x = o.text_state;
 
   hipError_t e = hipSuccess;
   if (qk_pad) {
@@ -250,15 +286,40 @@ int forward_impl(bool is_f32, const void* q, const void* k, const void* v, const
     vx = vp;
     ox = pad_base + 2 * qk_pad + v_pad;
   }
+  char* opt_base = pad_base + 2 * qk_pad + 2 * v_pad;
+  if (a_pad && e == hipSuccess) {  // alpha [H][F][d_k] -> [H][F][32]
+    float* ap = reinterpret_cast<float*>(opt_base);
+    e = vda::launch_pad_rows(o.alpha, ap, (long long)H * F, d_k * 4, pk * 4, stream);
+    alpha_x = ap;
+  }
+  if (t_pad && e == hipSuccess) {  // S_T [H][d_v][d_k] -> [H][d_v][pk] -> [H][pv][pk]
+    float* tt = reinterpret_cast<float*>(opt_base + a_pad);
+    float* tp = reinterpret_cast<float*>(opt_base + a_pad + t_tmp);
+    e = vda::launch_pad_rows(o.text_state, tt, (long long)H * d_v, d_k * 4, pk * 4, stream);
+    if (e == hipSuccess)
+      e = vda::launch_pad_rows(tt, tp, (long long)H, d_v * pk * 4, pv * pk * 4, stream);
+    ts_x = tp;
+  }
   if (e == hipSuccess)
     e = vda::launch_frame_stats(is_f32, kx, vx, beta, F, N, H, pk, pv, plan, A_part, B_part,
                                 stream);
-  if (e == hipSuccess)
+  if (e == hipSuccess && !frozen)
     e = vda::launch_frame_inverse(A_part, B_part, plan, (long long)H * F, pk, pv, Inv, stream);
+  vda::ScanOptions so;
+  so.frozen = frozen;
+  so.alpha = alpha_x;
+  so.text_state = ts_x;
+  so.tokens = N;
   if (e == hipSuccess)
-    e = vda::launch_state_scan(is_f32, Inv, B_part, F, H, pk, pv, S_fwd, S_rev, stream);
+    e = vda::launch_state_scan(is_f32, frozen ? A_part : Inv, B_part, F, H, pk, pv, so, S_fwd,
+                               S_rev, stream);
+  vda::GatherOptions go;
+  go.alpha = alpha_x;
+  go.chunk = o.window_chunk;
+  go.radius = o.window_radius;
+  go.offset = o.window_offset;
   if (e == hipSuccess)
-    e = vda::launch_readout(is_f32, qx, S_fwd, S_rev, gate, F, N, H, pk, pv, d_v, ox, stream);
+    e = vda::launch_readout(is_f32, qx, S_fwd, S_rev, gate, F, N, H, pk, pv, d_v, go, ox, stream);
   if (e == hipSuccess && ox != out)
     e = vda::launch_unpad_rows(ox, out, (long long)tok, (int)(pv * es), (int)(d_v * es), stream);
   const hipError_t ef = release_workspace(dev, wsi, stream);
@@ -287,13 +348,25 @@ const char* vda_status_string(int status) {
 
 int vda_forward(const void* q, const void* k, const void* v, const float* beta, const float* gate,
                 int F, int N, int H, int d_k, int d_v, void* out, hipStream_t stream) {
-  return forward_impl(false, q, k, v, beta, gate, F, N, H, d_k, d_v, out, stream);
+  return forward_impl(false, q, k, v, beta, gate, F, N, H, d_k, d_v, nullptr, out, stream);
 }
 
 int vda_forward_f32(const float* q, const float* k, const float* v, const float* beta,
                     const float* gate, int F, int N, int H, int d_k, int d_v, float* out,
                     hipStream_t stream) {
-  return forward_impl(true, q, k, v, beta, gate, F, N, H, d_k, d_v, out, stream);
+  return forward_impl(true, q, k, v, beta, gate, F, N, H, d_k, d_v, nullptr, out, stream);
+}
+
+int vda_forward_ex(const void* q, const void* k, const void* v, const float* beta,
+                   const float* gate, int F, int N, int H, int d_k, int d_v,
+                   const vda_options* opts, void* out, hipStream_t stream) {
+  return forward_impl(false, q, k, v, beta, gate, F, N, H, d_k, d_v, opts, out, stream);
+}
+
+int vda_forward_ex_f32(const float* q, const float* k, const float* v, const float* beta,
+                       const float* gate, int F, int N, int H, int d_k, int d_v,
+                       const vda_options* opts, float* out, hipStream_t stream) {
+  return forward_impl(true, q, k, v, beta, gate, F, N, H, d_k, d_v, opts, out, stream);
 }
 
 int vda_default_split_plan(int F, int N, int H, int d_k, int d_v, int is_f32, int* tail_frames,
@@ -385,8 +458,8 @@ int vda_state_scan(const float* Inv, const float* B, int F, int H, int d_k, int 
   if (overlaps(rf, rr) || overlaps(rf, ri) || overlaps(rf, rb) || overlaps(rr, ri) ||
       overlaps(rr, rb))
     return VDA_ERR_OVERLAP;
-  return hip_status(
-      vda::launch_state_scan(is_f32 != 0, Inv, B, F, H, d_k, d_v, S_fwd, S_rev, stream));
+  return hip_status(vda::launch_state_scan(is_f32 != 0, Inv, B, F, H, d_k, d_v, vda::ScanOptions(),
+                                           S_fwd, S_rev, stream));
 }
 
 int vda_readout(const void* q, const float* S_fwd, const float* S_rev, const float* gate, int F,
@@ -405,7 +478,7 @@ int vda_readout(const void* q, const float* S_fwd, const float* S_rev, const flo
       overlaps(ro, range_of(S_rev, fh * d_v * d_k * 4)) || overlaps(ro, range_of(gate, H * 4)))
     return VDA_ERR_OVERLAP;
   return hip_status(vda::launch_readout(is_f32 != 0, q, S_fwd, S_rev, gate, F, N, H, d_k, d_v,
-                                        d_v, out, stream));
+                                        d_v, vda::GatherOptions(), out, stream));
 }
 
 }  // extern "C"

@@ -36,17 +36,35 @@ hipError_t launch_frame_inverse(const float* A_part, float* B_part, SplitPlan pl
                                 long long count, int d_k, int d_v, float* Inv,
                                 hipStream_t stream);
 
+// Options of the scans beyond the core (defaults: the core scan).
+struct ScanOptions {
+  bool frozen = false;                // Eq. 3c with 1/sqrt(U) scaling; Mat holds A_t
+  const float* alpha = nullptr;       // [H][F][d_k] channel decay, or null (1)
+  const float* text_state = nullptr;  // [H][d_v][d_k] S_T (both scans start at S_T/2), or null
+  int tokens = 0;                     // U, tokens per frame (frozen rule)
+};
+
 // Steps a3/a4, Eq. A.1: forward and reverse state scans (exact fp32 products,
-// or split-bf16 products with fp32 accumulation).
-hipError_t launch_state_scan(bool exact_f32, const float* Inv, const float* Bm, int F, int H,
-                             int d_k, int d_v, float* S_fwd, float* S_rev, hipStream_t stream);
+// or split-bf16 products with fp32 accumulation).  Mat is Inv_t (joint rule)
+// or A_t (frozen rule), symmetric.
+hipError_t launch_state_scan(bool exact_f32, const float* Mat, const float* Bm, int F, int H,
+                             int d_k, int d_v, const ScanOptions& o, float* S_fwd, float* S_rev,
+                             hipStream_t stream);
+
+// Options of the gather beyond the core (defaults: own frame, no decay).
+struct GatherOptions {
+  const float* alpha = nullptr;  // [H][F][d_k] channel decay, or null (1)
+  int chunk = 1;                 // local window: frames per chunk,
+  int radius = 0;                // chunks on each side,
+  int offset = 0;                // and chunk position of frame 0
+};
 
 // Steps a5-a7, Eq. A.4 / 1a / 1c: gather, readout, RMSNorm and gate.
 // d_v_norm: the number of channels RMSNorm averages over (d_v, or fewer
 // when the trailing value channels are zero padding).
 hipError_t launch_readout(bool is_f32, const void* q, const float* S_fwd, const float* S_rev,
                           const float* gate, int F, int N, int H, int d_k, int d_v,
-                          int d_v_norm, void* out, hipStream_t stream);
+                          int d_v_norm, const GatherOptions& g, void* out, hipStream_t stream);
 
 // Row-wise channel padding (zero fill) and its inverse, in 16-byte pieces.
 hipError_t launch_pad_rows(const void* src, void* dst, long long rows, int src_bytes,

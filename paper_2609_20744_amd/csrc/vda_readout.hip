@@ -18,12 +18,46 @@
 namespace vda {
 namespace {
 
+// Local window [lo, hi] of frame f (0-based, clipped to [0, F)): the frame's
+// chunk of `chunk` frames (counted from `offset` positions before frame 0)
+// and `radius` chunks on each side (Eq. A.4's [l_t, h_t]).
+struct Window {
+  int lo, hi;
+};
+
+__device__ __forceinline__ Window local_window(int f, int F, int chunk, int radius, int offset) {
+  const int c = (f + offset) / chunk;
+  const int lo = (c - radius) * chunk - offset;
+  const int hi = (c + radius + 1) * chunk - offset - 1;
+  return Window{max(0, lo), min(F - 1, hi)};
+}
+
+// Decay bridge factors of Eq. A.4 for key channels j .. j + W - 1 of head h:
+// df = prod_{r = lo..f} alpha_r, dr = prod_{r = f..hi} alpha_r.
+template <int W>
+__device__ __forceinline__ void bridge_decay(const float* alpha, int h, int F, int DKr, int j,
+                                             int f, Window w, float (&df)[W], float (&dr)[W]) {
+#pragma unroll
+  for (int c = 0; c < W; ++c) df[c] = dr[c] = 1.0f;
+  if (alpha == nullptr) return;
+  const float* a = alpha + (size_t)h * F * DKr + j;
+  for (int r = w.lo; r <= w.hi; ++r) {
+#pragma unroll
+    for (int c = 0; c < W; ++c) {
+      const float x = a[(size_t)r * DKr + c];
+      if (r <= f) df[c] *= x;
+      if (r >= f) dr[c] *= x;
+    }
+  }
+}
+
 template <int DK, int DV>
 __global__ __launch_bounds__(kThreads, 2)
 void readout_bf16_kernel(const uint16_t* __restrict__ Q, const float* __restrict__ S_fwd,
                          const float* __restrict__ S_rev, const float* __restrict__ gate,
                          int F, int N, int chunks, int tokens_per_chunk, unsigned nwg,
-                         float inv_norm, uint16_t* __restrict__ out) {
+                         float inv_norm, const float* __restrict__ alpha, int wchunk,
+                         int wradius, int woffset, uint16_t* __restrict__ out) {
   constexpr int SLD = DK + 8;  // bf16 row stride of S~ in LDS
   constexpr int MB = DV / 16;  // 16-row blocks of S~ (output channels)
   constexpr int KB = DK / 32;  // 32-wide k steps
@@ -44,8 +78,17 @@ void readout_bf16_kernel(const uint16_t* __restrict__ Q, const float* __restrict
   const int lg = lane >> 4;
 
   {
-    const float* sf = S_fwd + (size_t)fh * (DV * DK);
-    const float* sr = S_rev + (size_t)fh * (DV * DK);
+    // Gather (Eq. A.4): the forward state entering the frame's local window
+    // and the reverse state leaving it, each decayed across the skipped
+    // frames (the own frame only, with alpha = 1, in the core operator).
+    const int h = (int)(fh / F), f = (int)(fh % F);
+    const Window w = local_window(f, F, wchunk, wradius, woffset);
+    const float* sf = S_fwd + ((size_t)h * F + w.lo) * (DV * DK);
+    const float* sr = S_rev + ((size_t)h * F + w.hi) * (DV * DK);
+    // This thread's columns are the same in every iteration below.
+    static_assert((kThreads * 4) % DK == 0, "fixed columns per thread");
+    float df[4], dr[4];
+    bridge_decay<4>(alpha, h, F, DK, (tid * 4) % DK, f, w, df, dr);
     // Fully unrolled (a compile-time trip count; DV * DK is a multiple of
     // kThreads * 4), so all of a thread's loads are in flight together.
     static_assert((DV * DK) % (kThreads * 4) == 0, "state size");
@@ -56,7 +99,8 @@ void readout_bf16_kernel(const uint16_t* __restrict__ Q, const float* __restrict
       const float4 b = *reinterpret_cast<const float4*>(sr + idx);
       const int i = idx / DK, j = idx % DK;
       *reinterpret_cast<uint2*>(&st[i * SLD + j]) =
-          make_uint2(pack_bf16x2(a.x + b.x, a.y + b.y), pack_bf16x2(a.z + b.z, a.w + b.w));
+          make_uint2(pack_bf16x2(a.x * df[0] + b.x * dr[0], a.y * df[1] + b.y * dr[1]),
+                     pack_bf16x2(a.z * df[2] + b.z * dr[2], a.w * df[3] + b.w * dr[3]));
     }
   }
   lds_barrier();
@@ -150,6 +194,7 @@ __global__ __launch_bounds__(kThreads)
 void readout_f32_kernel(const float* __restrict__ Q, const float* __restrict__ S_fwd,
                         const float* __restrict__ S_rev, const float* __restrict__ gate,
                         int F, int N, int chunks, int tokens_per_chunk, float inv_norm,
+                        const float* __restrict__ alpha, int wchunk, int wradius, int woffset,
                         float* __restrict__ out) {
   constexpr int SLD = DK + 1;
   constexpr int VPT = DV / 16;  // output channels per thread
@@ -163,10 +208,16 @@ void readout_f32_kernel(const float* __restrict__ Q, const float* __restrict__ S
   const float g = gate[fh / F];
   const int tid = threadIdx.x;
 
-  const float* sf = S_fwd + (size_t)fh * (DV * DK);
-  const float* sr = S_rev + (size_t)fh * (DV * DK);
+  // Gather (Eq. A.4), as in readout_bf16_kernel.
+  const int h = (int)(fh / F), f = (int)(fh % F);
+  const Window w = local_window(f, F, wchunk, wradius, woffset);
+  const float* sf = S_fwd + ((size_t)h * F + w.lo) * (DV * DK);
+  const float* sr = S_rev + ((size_t)h * F + w.hi) * (DV * DK);
+  static_assert(kThreads % DK == 0, "fixed column per thread");
+  float df[1], dr[1];
+  bridge_decay<1>(alpha, h, F, DK, tid % DK, f, w, df, dr);
   for (int idx = tid; idx < DV * DK; idx += kThreads)
-    st[(idx / DK) * SLD + idx % DK] = sf[idx] + sr[idx];
+    st[(idx / DK) * SLD + idx % DK] = sf[idx] * df[0] + sr[idx] * dr[0];
 
   const int tok = tid >> 4;  // token within the group of 16
   const int part = tid & 15;
@@ -211,8 +262,8 @@ inline int readout_chunks(long long fh_count, int N) {
 
 template <int DK, int DV>
 hipError_t launch_readout_t(bool is_f32, const void* q, const float* S_fwd, const float* S_rev,
-                            const float* gate, int F, int N, int H, int d_v_norm, void* out,
-                            hipStream_t stream) {
+                            const float* gate, int F, int N, int H, int d_v_norm,
+                            const GatherOptions& go, void* out, hipStream_t stream) {
   const float inv_norm = 1.0f / (float)d_v_norm;
   const long long fh_count = (long long)H * F;
   const int chunks = readout_chunks(fh_count, N);
@@ -222,11 +273,12 @@ hipError_t launch_readout_t(bool is_f32, const void* q, const float* S_fwd, cons
   if (is_f32)
     hipLaunchKernelGGL((readout_f32_kernel<DK, DV>), grid, dim3(kThreads), 0, stream,
                        static_cast<const float*>(q), S_fwd, S_rev, gate, F, N, chunks, tpc,
-                       inv_norm, static_cast<float*>(out));
+                       inv_norm, go.alpha, go.chunk, go.radius, go.offset, static_cast<float*>(out));
   else
     hipLaunchKernelGGL((readout_bf16_kernel<DK, DV>), grid, dim3(kThreads), 0, stream,
                        static_cast<const uint16_t*>(q), S_fwd, S_rev, gate, F, N, chunks, tpc,
-                       (unsigned)(fh_count * chunks), inv_norm, static_cast<uint16_t*>(out));
+                       (unsigned)(fh_count * chunks), inv_norm, go.alpha, go.chunk, go.radius,
+                       go.offset, static_cast<uint16_t*>(out));
   return hipGetLastError();
 }
 
@@ -234,10 +286,10 @@ hipError_t launch_readout_t(bool is_f32, const void* q, const float* S_fwd, cons
 
 hipError_t launch_readout(bool is_f32, const void* q, const float* S_fwd, const float* S_rev,
                           const float* gate, int F, int N, int H, int d_k, int d_v, int d_v_norm,
-                          void* out, hipStream_t stream) {
-#define VDA_READOUT_CASE(DKV, DVV)                                                         \
-  if (d_k == DKV && d_v == DVV)                                                            \
-    return launch_readout_t<DKV, DVV>(is_f32, q, S_fwd, S_rev, gate, F, N, H, d_v_norm, out, \
+                          const GatherOptions& go, void* out, hipStream_t stream) {
+#define VDA_READOUT_CASE(DKV, DVV)                                                            \
+  if (d_k == DKV && d_v == DVV)                                                               \
+    return launch_readout_t<DKV, DVV>(is_f32, q, S_fwd, S_rev, gate, F, N, H, d_v_norm, go, out, \
                                       stream);
   VDA_READOUT_CASE(32, 32) VDA_READOUT_CASE(32, 64) VDA_READOUT_CASE(32, 128)
   VDA_READOUT_CASE(64, 32) VDA_READOUT_CASE(64, 64) VDA_READOUT_CASE(64, 128)

@@ -38,15 +38,18 @@ __device__ __forceinline__ void split_bf16x8(const float (&x)[8], bf16x8& hi, bf
   }
 }
 
-template <int DK, bool EXACT_F32>
+// The exact fp32 scan (fp32 storage path); DECAY and FROZEN as described at
+// scan_bf16_kernel below.
+template <int DK, bool FROZEN, bool DECAY>
 __global__ __launch_bounds__(kThreads)
-void scan_kernel(const float* __restrict__ Inv, const float* __restrict__ Bm,
-                 int F, int DV, unsigned nwg,
-                 float* __restrict__ S_fwd, float* __restrict__ S_rev) {
+void scan_f32_kernel(const float* __restrict__ Mat, const float* __restrict__ Bm,
+                     const float* __restrict__ alpha, const float* __restrict__ text_state,
+                     int F, int DV, unsigned nwg, float inv_u, float inv_sqrt_u,
+                     float* __restrict__ S_fwd, float* __restrict__ S_rev) {
   constexpr int XLD = DK + 4;        // LDS row stride (floats)
   constexpr int NB = DK / 16;        // 16-column output slices
   constexpr int NBW = (NB + 3) / 4;  // slices per wave
-  constexpr int KL = DK / 4;         // k values per lane and slice
+  constexpr int KL = DK / 4;         // k values per lane and slice (k = lg * KL + s)
   constexpr int E = DK / 16;         // state elements per thread in the row-wise phase
   static_assert(E % 2 == 0, "float2 granularity");
   // Row-wise accesses in 16-byte pieces where the row slice allows: fewer
@@ -54,6 +57,7 @@ void scan_kernel(const float* __restrict__ Inv, const float* __restrict__ Bm,
   // outstanding-load counter can track precisely.
   constexpr int VW = E % 4 == 0 ? 4 : 2;
   __shared__ __align__(16) float xs[2][16 * XLD];
+  __shared__ __align__(16) float alds[DECAY ? DK : 4];  // alpha of the coming step
 
   const int nrb = DV / 16;
   const unsigned L = xcd_grouped_id(blockIdx.x, nwg);
@@ -72,45 +76,47 @@ void scan_kernel(const float* __restrict__ Inv, const float* __restrict__ Bm,
   const int pr = tid >> 4;
   const int pc = (tid & 15) * E;
 
-  for (int i = tid; i < 16 * XLD; i += kThreads) xs[0][i] = 0.f;
+  const size_t mat_b = (size_t)DV * DK;  // one B / state matrix
+  for (int i = tid; i < 16 * XLD; i += kThreads) {
+    const int r = i / XLD, c = i % XLD;
+    xs[0][i] = text_state != nullptr && c < DK
+                   ? 0.5f * text_state[(size_t)hb * mat_b + (size_t)(rb * 16 + r) * DK + c]
+                   : 0.f;
+  }
 
   float* Sout = dir == 0 ? S_fwd : S_rev;
-  const size_t mat_b = (size_t)DV * DK;  // one B / state matrix
   const size_t row_off = (size_t)(rb * 16 + pr) * DK + pc;
-  // Entering states of this head, [F][d_v][d_k]: a range-checked buffer, so
-  // the padded steps past the last frame store nothing.
   const __amdgpu_buffer_rsrc_t srsrc =
       make_rsrc(Sout + (size_t)hb * F * mat_b, (uint32_t)(F * mat_b * sizeof(float)));
+  const __amdgpu_buffer_rsrc_t brsrc =
+      make_rsrc(Bm + (size_t)hb * F * mat_b, (uint32_t)(F * mat_b * sizeof(float)));
+  const __amdgpu_buffer_rsrc_t arsrc =
+      make_rsrc(DECAY ? alpha + (size_t)hb * F * DK : Bm, DECAY ? (uint32_t)(F * DK * 4) : 0u);
 
   auto frame_of = [&](int step) { return dir == 0 ? step : F - 1 - step; };
 
-  // k indices held by this lane for the MFMA, in order:
-  //   exact fp32 (16x16x4, k = lg*KL + s):           lg*KL .. lg*KL + KL-1
-  //   split bf16 (16x16x32, k = ks*32 + 8*lg + e):   ks*32 + 8*lg .. +7, ks = 0..DK/32-1
-  auto kidx = [&](int s) {
-    return EXACT_F32 ? lg * KL + s : (s / 8) * 32 + 8 * lg + (s % 8);
-  };
-
-  // Operands of the next kPrefetch frames are in flight in a register ring:
-  // slot d holds frame step0 + d, refilled with frame step0 + d + kPrefetch
-  // once consumed.  A deeper ring no longer fits in the vector registers; the
-  // compiler then parks slots in accumulation registers and must wait for
-  // each load before copying it there, which drains the ring.
+  // Operands of the next two frames are in flight in a register ring: slot
+  // d holds frame step0 + d, refilled with frame step0 + d + 2 once
+  // consumed.  A deeper ring no longer fits in the vector registers.
   constexpr int kPrefetch = 2;
   float ops[kPrefetch][NBW][KL];
   float bs[kPrefetch][E];
-  auto load_ops = [&](int step, float (&op)[NBW][KL], float (&bb)[E]) {
-    const size_t fh = (size_t)hb * F + frame_of(step);
-    const float* inv = Inv + fh * (DK * DK);
+  u32x4 al[kPrefetch];  // alpha, columns 4 tid .. 4 tid + 3 (threads tid < DK / 4)
+  auto load_ops = [&](int step, float (&op)[NBW][KL], float (&bb)[E], u32x4& av) {
+    const int frame = frame_of(step);
+    const int bframe = FROZEN ? frame_of(step - 1) : frame;
+    const bool bin = (unsigned)bframe < (unsigned)F;
+    const size_t fh = (size_t)hb * F + frame;
+    const float* mat = Mat + fh * (DK * DK);
 #pragma unroll
     for (int m = 0; m < NBW; ++m) {
       const int nb = wave + 4 * m;
       if (NB >= 4 || nb < NB) {  // compile-time true unless d_k = 32
-        // Inv[k][nb*16 + li] == Inv[nb*16 + li][k]
-        const float* row = inv + (size_t)(nb * 16 + li) * DK;
+        // Mat[k][nb*16 + li] == Mat[nb*16 + li][k] (symmetric)
+        const float* row = mat + (size_t)(nb * 16 + li) * DK;
 #pragma unroll
         for (int s = 0; s < KL; s += 4) {
-          const float4 v = *reinterpret_cast<const float4*>(row + kidx(s));
+          const float4 v = *reinterpret_cast<const float4*>(row + lg * KL + s);
           op[m][s] = v.x;
           op[m][s + 1] = v.y;
           op[m][s + 2] = v.z;
@@ -118,128 +124,107 @@ void scan_kernel(const float* __restrict__ Inv, const float* __restrict__ Bm,
         }
       }
     }
-    const float* src = Bm + fh * mat_b + row_off;
 #pragma unroll
     for (int e = 0; e < E; e += VW) {
+      const uint32_t off =
+          bin ? (uint32_t)(((size_t)bframe * mat_b + row_off + e) * 4u) : kOutOfRange;
       if constexpr (VW == 4) {
-        const float4 x = *reinterpret_cast<const float4*>(src + e);
-        bb[e] = x.x;
-        bb[e + 1] = x.y;
-        bb[e + 2] = x.z;
-        bb[e + 3] = x.w;
+        const u32x4 x =
+            __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(brsrc, (int)off, 0, 0));
+#pragma unroll
+        for (int v = 0; v < 4; ++v) bb[e + v] = __uint_as_float(x[v]);
       } else {
-        const float2 x = *reinterpret_cast<const float2*>(src + e);
-        bb[e] = x.x;
-        bb[e + 1] = x.y;
+        const u32x2 x =
+            __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(brsrc, (int)off, 0, 0));
+        bb[e] = __uint_as_float(x[0]);
+        bb[e + 1] = __uint_as_float(x[1]);
       }
+    }
+    if constexpr (DECAY) {
+      const uint32_t off = tid < DK / 4 ? (uint32_t)(frame * DK + 4 * tid) * 4u : kOutOfRange;
+      av = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(arsrc, (int)off, 0, 0));
     }
   };
 
-  // Issue the ring in slot order (pinned against rescheduling) so slot 0 is
-  // the oldest load on loop entry.
 #pragma unroll
   for (int d = 0; d < kPrefetch; ++d) {
-    load_ops(min(d, F - 1), ops[d], bs[d]);
+    load_ops(min(d, F - 1), ops[d], bs[d], al[d]);
     __builtin_amdgcn_sched_barrier(0);
   }
+  if constexpr (DECAY) {
+    if (tid < DK / 4) reinterpret_cast<u32x4*>(alds)[tid] = al[0];
+  }
 
-  // The step count is padded to a multiple of the ring depth; padded steps
-  // (step >= F) read a clamped frame and their stores are dropped, so the
-  // loop body has no early exit.
   int cur = 0;
   for (int step0 = 0; step0 < F; step0 += kPrefetch) {
 #pragma unroll
     for (int d = 0; d < kPrefetch; ++d) {
       const int step = step0 + d;
-      // Frame index within the head; past the end it is out of the buffer
-      // range (>= F forward, negative and so huge as unsigned in reverse).
       const int frame = dir == 0 ? step : F - 1 - step;
       lds_barrier();  // xs[cur] holds the entering state
       {
         float* x = &xs[cur][pr * XLD + pc];
         const uint32_t off = (uint32_t)((size_t)(unsigned)frame * mat_b + row_off) * 4u;
 #pragma unroll
+        for (int e = 0; e < E; ++e) {
+          if constexpr (FROZEN) x[e] += bs[d][e] * inv_sqrt_u;  // previous frame's write
+        }
+#pragma unroll
         for (int e = 0; e < E; e += VW) {
           if constexpr (VW == 4) {
-            float4 v = *reinterpret_cast<float4*>(x + e);
+            const float4 v = *reinterpret_cast<float4*>(x + e);
             store_b128(srsrc, off + e * 4u,
                        u32x4{__float_as_uint(v.x), __float_as_uint(v.y), __float_as_uint(v.z),
                              __float_as_uint(v.w)});
-            v.x += bs[d][e];
-            v.y += bs[d][e + 1];
-            v.z += bs[d][e + 2];
-            v.w += bs[d][e + 3];
-            *reinterpret_cast<float4*>(x + e) = v;
           } else {
-            float2 v = *reinterpret_cast<float2*>(x + e);
+            const float2 v = *reinterpret_cast<float2*>(x + e);
             store_b64(srsrc, off + e * 4u, make_uint2(__float_as_uint(v.x), __float_as_uint(v.y)));
-            v.x += bs[d][e];
-            v.y += bs[d][e + 1];
-            *reinterpret_cast<float2*>(x + e) = v;
           }
+        }
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          float v = x[e];
+          if constexpr (DECAY) v *= alds[pc + e];
+          if constexpr (!FROZEN) v += bs[d][e];
+          x[e] = v;
         }
       }
       lds_barrier();
+      if constexpr (DECAY) {  // alpha of the next step (this step's reads are done)
+        if (tid < DK / 4) reinterpret_cast<u32x4*>(alds)[tid] = al[(d + 1) % kPrefetch];
+      }
       if (NB >= 4 || wave < NB) {
-        // A-operand: row li of the block at this lane's k indices.
+        // A-operand: row li of the block at k = lg * KL + s.
         float a[KL];
-        const float* xr = &xs[cur][li * XLD];
+        const float* xr = &xs[cur][li * XLD + lg * KL];
 #pragma unroll
         for (int s = 0; s < KL; s += 4) {
-          const float4 v = *reinterpret_cast<const float4*>(xr + kidx(s));
+          const float4 v = *reinterpret_cast<const float4*>(xr + s);
           a[s] = v.x;
           a[s + 1] = v.y;
           a[s + 2] = v.z;
           a[s + 3] = v.w;
         }
-        if constexpr (EXACT_F32) {
 #pragma unroll
-          for (int m = 0; m < NBW; ++m) {
-            const int nb = wave + 4 * m;
-            if (NB >= 4 || nb < NB) {
-              floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+        for (int m = 0; m < NBW; ++m) {
+          const int nb = wave + 4 * m;
+          if (NB >= 4 || nb < NB) {
+            floatx4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-              for (int s = 0; s < KL; ++s)
-                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[s], ops[d][m][s], acc, 0, 0, 0);
-#pragma unroll
-              for (int i = 0; i < 4; ++i) xs[cur ^ 1][(lg * 4 + i) * XLD + nb * 16 + li] = acc[i];
+            for (int s = 0; s < KL; ++s) {
+              float b = ops[d][m][s];
+              if constexpr (FROZEN)  // I - A / U
+                b = (lg * KL + s == nb * 16 + li ? 1.0f : 0.0f) - b * inv_u;
+              acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[s], b, acc, 0, 0, 0);
             }
-          }
-        } else {
-          constexpr int KB = DK / 32;
-          bf16x8 ahi[KB], alo[KB];
 #pragma unroll
-          for (int kb = 0; kb < KB; ++kb) {
-            float t[8];
-#pragma unroll
-            for (int e = 0; e < 8; ++e) t[e] = a[kb * 8 + e];
-            split_bf16x8(t, ahi[kb], alo[kb]);
-          }
-#pragma unroll
-          for (int m = 0; m < NBW; ++m) {
-            const int nb = wave + 4 * m;
-            if (NB >= 4 || nb < NB) {
-              floatx4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-              for (int kb = 0; kb < KB; ++kb) {
-                float t[8];
-#pragma unroll
-                for (int e = 0; e < 8; ++e) t[e] = ops[d][m][kb * 8 + e];
-                bf16x8 bhi, blo;
-                split_bf16x8(t, bhi, blo);
-                acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(alo[kb], bhi, acc, 0, 0, 0);
-                acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi[kb], blo, acc, 0, 0, 0);
-                acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi[kb], bhi, acc, 0, 0, 0);
-              }
-#pragma unroll
-              for (int i = 0; i < 4; ++i) xs[cur ^ 1][(lg * 4 + i) * XLD + nb * 16 + li] = acc[i];
-            }
+            for (int i = 0; i < 4; ++i) xs[cur ^ 1][(lg * 4 + i) * XLD + nb * 16 + li] = acc[i];
           }
         }
       }
       // Always refill (past the end: a clamped, unused frame) so no branch
       // hides the loads from the wait-count bookkeeping.
-      load_ops(min(step + kPrefetch, F - 1), ops[d], bs[d]);
+      load_ops(min(step + kPrefetch, F - 1), ops[d], bs[d], al[d]);
       cur ^= 1;
     }
   }
@@ -361,18 +346,33 @@ __device__ __forceinline__ void scan_mfma_phase(const float* __restrict__ xs_cur
 // block (kb, nb) (four 4-byte reads).  With a row stride of 132 floats the
 // two lane groups of each 32-lane LDS pass then fall on distinct banks in
 // both kinds of read.
-template <int DK>
+//
+// Options of the full operator (template switches, so the core path carries
+// none of their work):
+//   DECAY  - the entering state is decayed, Sbar = S Diag(alpha_t), before
+//            the frame's write (Eq. 5 / A.1 with alpha); alpha_t reaches the
+//            row-wise phase through a small LDS row written one step ahead.
+//   FROZEN - the frozen-state additive rule with 1/sqrt(U) key scaling,
+//            S_t = Sbar_t (I - A_t / U) + B_t / sqrt(U) (Eq. 3c): the staged
+//            matrix is I - A_t / U, built from A_t on the way into LDS, and
+//            the write B_t / sqrt(U) is added after the product, that is at
+//            the start of the next step (B is loaded one frame late), so the
+//            state kept between steps is S_t - B_t / sqrt(U).
+// Both scans may start from a text state: S_T / 2 (Eq. 1b).
+template <int DK, bool FROZEN, bool DECAY>
 __global__ __launch_bounds__(kThreads)
-void scan_bf16_kernel(const float* __restrict__ Inv, const float* __restrict__ Bm, int F,
-                      int DV, unsigned nwg, float* __restrict__ S_fwd,
-                      float* __restrict__ S_rev) {
+void scan_bf16_kernel(const float* __restrict__ Mat, const float* __restrict__ Bm,
+                      const float* __restrict__ alpha, const float* __restrict__ text_state,
+                      int F, int DV, unsigned nwg, float inv_u, float inv_sqrt_u,
+                      float* __restrict__ S_fwd, float* __restrict__ S_rev) {
   constexpr int XLD = DK + 4;        // LDS row stride (floats)
   constexpr int VW = DK >= 64 ? 4 : 2;  // floats per access in the row-wise phase
   constexpr int NG = DK / (16 * VW);    // accesses per thread in the row-wise phase
   using U = UpperChunks<DK>;
   constexpr int CPT = U::per_thread;
-  __shared__ __align__(16) float ivs[(DK + 1) * XLD];  // Inv_t image, plus a dummy row
+  __shared__ __align__(16) float ivs[(DK + 1) * XLD];  // matrix image, plus a dummy row
   __shared__ __align__(16) float xs[2][16 * XLD];
+  __shared__ __align__(16) float alds[DECAY ? DK : 4];  // alpha of the coming step
 
   const int nrb = DV / 16;
   const unsigned L = xcd_grouped_id(blockIdx.x, nwg);
@@ -392,15 +392,26 @@ void scan_bf16_kernel(const float* __restrict__ Inv, const float* __restrict__ B
   const int pr = tid >> 4;
   const int pc = (tid & 15) * VW;
 
-  for (int i = tid; i < 16 * XLD; i += kThreads) xs[0][i] = 0.f;
+  const size_t mat_b = (size_t)DV * DK;  // one B / state matrix
+  // Initial state: S_T / 2 (rows of this block), or zero.
+  for (int i = tid; i < 16 * XLD; i += kThreads) {
+    const int r = i / XLD, c = i % XLD;
+    xs[0][i] = text_state != nullptr && c < DK
+                   ? 0.5f * text_state[(size_t)hb * mat_b + (size_t)(rb * 16 + r) * DK + c]
+                   : 0.f;
+  }
 
   float* Sout = dir == 0 ? S_fwd : S_rev;
-  const size_t mat_b = (size_t)DV * DK;  // one B / state matrix
   const size_t row_off = (size_t)(rb * 16 + pr) * DK + pc;
   // Entering states of this head, [F][d_v][d_k]: a range-checked buffer, so
   // the padded steps past the last frame store nothing.
   const __amdgpu_buffer_rsrc_t srsrc =
       make_rsrc(Sout + (size_t)hb * F * mat_b, (uint32_t)(F * mat_b * sizeof(float)));
+  // B of this head, range-checked (frames outside [0, F) read as zero).
+  const __amdgpu_buffer_rsrc_t brsrc =
+      make_rsrc(Bm + (size_t)hb * F * mat_b, (uint32_t)(F * mat_b * sizeof(float)));
+  const __amdgpu_buffer_rsrc_t arsrc =
+      make_rsrc(DECAY ? alpha + (size_t)hb * F * DK : Bm, DECAY ? (uint32_t)(F * DK * 4) : 0u);
 
   auto frame_of = [&](int step) { return dir == 0 ? step : F - 1 - step; };
 
@@ -423,14 +434,20 @@ void scan_bf16_kernel(const float* __restrict__ Inv, const float* __restrict__ B
   // indices only).
   u32x4 ir0[CPT], ir1[CPT];
   float bs0[NG][VW], bs1[NG][VW];
-  auto load_step = [&](int step, u32x4 (&ir)[CPT], float (&bb)[NG][VW]) {
-    const size_t fh = (size_t)hb * F + frame_of(step);
-    // B rows first (they are needed earlier in the step than Inv_t), and
-    // both through buffer loads, which the compiler keeps in program order.
-    const __amdgpu_buffer_rsrc_t brsrc = make_rsrc(Bm + fh * mat_b, (uint32_t)(mat_b * 4));
+  u32x4 al0, al1;  // alpha_t, columns 4 tid .. 4 tid + 3 (threads tid < DK / 4)
+  auto load_step = [&](int step, u32x4 (&ir)[CPT], float (&bb)[NG][VW], u32x4& al) {
+    const int frame = frame_of(step);
+    // The write added in this step: B of this frame (joint rule) or of the
+    // previous one (frozen rule; none before the first frame).
+    const int bframe = FROZEN ? frame_of(step - 1) : frame;
+    const bool bin = (unsigned)bframe < (unsigned)F;
+    // B rows first (they are needed earlier in the step than the matrix),
+    // and everything through buffer loads, which the compiler keeps in
+    // program order.
 #pragma unroll
     for (int g = 0; g < NG; ++g) {
-      const uint32_t off = (uint32_t)(row_off + g * 16 * VW) * 4u;
+      const uint32_t off =
+          bin ? (uint32_t)(((size_t)bframe * mat_b + row_off + g * 16 * VW) * 4u) : kOutOfRange;
       if constexpr (VW == 4) {
         const u32x4 x =
             __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(brsrc, (int)off, 0, 0));
@@ -443,48 +460,92 @@ void scan_bf16_kernel(const float* __restrict__ Inv, const float* __restrict__ B
         bb[g][1] = __uint_as_float(x[1]);
       }
     }
-    const __amdgpu_buffer_rsrc_t irsrc = make_rsrc(Inv + fh * (DK * DK), DK * DK * 4u);
+    if constexpr (DECAY) {
+      const uint32_t off = tid < DK / 4 ? (uint32_t)(frame * DK + 4 * tid) * 4u : kOutOfRange;
+      al = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(arsrc, (int)off, 0, 0));
+    }
+    const size_t fh = (size_t)hb * F + frame;
+    const __amdgpu_buffer_rsrc_t irsrc = make_rsrc(Mat + fh * (DK * DK), DK * DK * 4u);
 #pragma unroll
     for (int e = 0; e < CPT; ++e)
       ir[e] = __builtin_bit_cast(
           u32x4, __builtin_amdgcn_raw_buffer_load_b128(irsrc, (int)goff[e], 0, 0));
   };
 
+  // The staged matrix: Inv_t as loaded (joint rule), or I - A_t / U from the
+  // loaded A_t (frozen rule).
+  auto stage = [&](const u32x4 (&ir)[CPT]) {
+#pragma unroll
+    for (int e = 0; e < CPT; ++e) {
+      u32x4 w = ir[e];
+      if constexpr (FROZEN) {
+        const int elem = (int)(goff[e] / 4u);
+        const int row = elem / DK, col = elem % DK;
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+          w[c] = __float_as_uint((row == col + c ? 1.0f : 0.0f) - __uint_as_float(w[c]) * inv_u);
+      }
+      reinterpret_cast<u32x4*>(ivs)[loff[e]] = w;
+    }
+  };
+
   int cur = 0;
-  auto step_body = [&](int step, u32x4 (&ir)[CPT], float (&bb)[NG][VW]) {
+  auto step_body = [&](int step, u32x4 (&ir)[CPT], float (&bb)[NG][VW], u32x4& al,
+                       const u32x4& al_next) {
     // Frame index within the head; past the end it is out of the buffer
     // range (>= F forward, negative and so huge as unsigned in reverse).
     const int frame = dir == 0 ? step : F - 1 - step;
-    lds_barrier();  // xs[cur] holds the entering state; the last Inv image is consumed
-#pragma unroll
-    for (int e = 0; e < CPT; ++e) reinterpret_cast<u32x4*>(ivs)[loff[e]] = ir[e];
+    lds_barrier();  // xs[cur] holds the entering state; the last matrix image is consumed
+    stage(ir);
     {
       const uint32_t off = (uint32_t)((size_t)(unsigned)frame * mat_b + row_off) * 4u;
 #pragma unroll
       for (int g = 0; g < NG; ++g) {
         float* x = &xs[cur][pr * XLD + pc + g * 16 * VW];
+        float v[VW];
         if constexpr (VW == 4) {
-          floatx4& xv = reinterpret_cast<floatx4*>(xs[cur])[(pr * XLD + pc + g * 16 * VW) / 4];
-          floatx4 v = xv;
+          const floatx4 xv = reinterpret_cast<const floatx4*>(xs[cur])[(pr * XLD + pc + g * 16 * VW) / 4];
+#pragma unroll
+          for (int c = 0; c < 4; ++c) v[c] = xv[c];
+        } else {
+          const float2 xv = *reinterpret_cast<const float2*>(x);
+          v[0] = xv.x;
+          v[1] = xv.y;
+        }
+        if constexpr (FROZEN) {  // the previous frame's write, B / sqrt(U)
+#pragma unroll
+          for (int c = 0; c < VW; ++c) v[c] += bb[g][c] * inv_sqrt_u;
+        }
+        if constexpr (VW == 4)
           store_b128(srsrc, off + g * 64u * VW,
                      u32x4{__float_as_uint(v[0]), __float_as_uint(v[1]), __float_as_uint(v[2]),
                            __float_as_uint(v[3])});
+        else
+          store_b64(srsrc, off + g * 64u * VW, make_uint2(__float_as_uint(v[0]), __float_as_uint(v[1])));
+        if constexpr (DECAY) {
 #pragma unroll
-          for (int c = 0; c < 4; ++c) v[c] += bb[g][c];
-          xv = v;
-        } else {
-          float2 v = *reinterpret_cast<float2*>(x);
-          store_b64(srsrc, off + g * 64u * VW, make_uint2(__float_as_uint(v.x), __float_as_uint(v.y)));
-          v.x += bb[g][0];
-          v.y += bb[g][1];
-          *reinterpret_cast<float2*>(x) = v;
+          for (int c = 0; c < VW; ++c) v[c] *= alds[pc + g * 16 * VW + c];
         }
+        if constexpr (!FROZEN) {
+#pragma unroll
+          for (int c = 0; c < VW; ++c) v[c] += bb[g][c];
+        }
+        if constexpr (VW == 4)
+          reinterpret_cast<floatx4*>(xs[cur])[(pr * XLD + pc + g * 16 * VW) / 4] =
+              floatx4{v[0], v[1], v[2], v[3]};
+        else
+          *reinterpret_cast<float2*>(x) = make_float2(v[0], v[1]);
       }
     }
     lds_barrier();
+    // alpha of the next step, read by its row-wise phase (after the next
+    // barrier); this step's reads of alds are complete.
+    if constexpr (DECAY) {
+      if (tid < DK / 4) reinterpret_cast<u32x4*>(alds)[tid] = al_next;
+    }
     // Always refill (past the end: a clamped, unused frame) so no branch
     // hides the loads from the wait-count bookkeeping.
-    load_step(min(step + 2, F - 1), ir, bb);
+    load_step(min(step + 2, F - 1), ir, bb, al);
     switch (wave) {  // wave-uniform
       case 0: scan_mfma_phase<DK, 0>(xs[cur], xs[cur ^ 1], ivs, li, lg); break;
       case 1: scan_mfma_phase<DK, 1>(xs[cur], xs[cur ^ 1], ivs, li, lg); break;
@@ -496,40 +557,57 @@ void scan_bf16_kernel(const float* __restrict__ Inv, const float* __restrict__ B
 
   // Issue the ring in slot order (pinned against rescheduling) so slot 0 is
   // the oldest load on loop entry.
-  load_step(0, ir0, bs0);
+  load_step(0, ir0, bs0, al0);
   __builtin_amdgcn_sched_barrier(0);
-  load_step(min(1, F - 1), ir1, bs1);
+  load_step(min(1, F - 1), ir1, bs1, al1);
   __builtin_amdgcn_sched_barrier(0);
+  if constexpr (DECAY) {  // alpha of step 0
+    if (tid < DK / 4) reinterpret_cast<u32x4*>(alds)[tid] = al0;
+  }
   // The step count is padded to an even number; a padded step (step >= F)
   // reads a clamped frame and its stores are dropped, so the loop body has
   // no early exit.
   for (int step0 = 0; step0 < F; step0 += 2) {
-    step_body(step0, ir0, bs0);
-    step_body(step0 + 1, ir1, bs1);
+    step_body(step0, ir0, bs0, al0, al1);
+    step_body(step0 + 1, ir1, bs1, al1, al0);
   }
 }
 
-template <int DK>
-hipError_t launch_scan_t(bool exact_f32, const float* Inv, const float* Bm, int F, int H, int d_v,
-                         float* S_fwd, float* S_rev, hipStream_t stream) {
+template <int DK, bool FROZEN, bool DECAY>
+hipError_t launch_scan_v(bool exact_f32, const float* Mat, const float* Bm, int F, int H, int d_v,
+                         const ScanOptions& o, float* S_fwd, float* S_rev, hipStream_t stream) {
   const unsigned nwg = (unsigned)H * 2u * (unsigned)(d_v / 16);
+  const float inv_u = FROZEN ? 1.0f / (float)o.tokens : 0.0f;
+  const float inv_sqrt_u = FROZEN ? 1.0f / sqrtf((float)o.tokens) : 0.0f;
   if (exact_f32)
-    hipLaunchKernelGGL((scan_kernel<DK, true>), dim3(nwg), dim3(kThreads), 0, stream, Inv, Bm, F,
-                       d_v, nwg, S_fwd, S_rev);
+    hipLaunchKernelGGL((scan_f32_kernel<DK, FROZEN, DECAY>), dim3(nwg), dim3(kThreads), 0, stream,
+                       Mat, Bm, o.alpha, o.text_state, F, d_v, nwg, inv_u, inv_sqrt_u, S_fwd, S_rev);
   else
-    hipLaunchKernelGGL((scan_bf16_kernel<DK>), dim3(nwg), dim3(kThreads), 0, stream, Inv, Bm, F,
-                       d_v, nwg, S_fwd, S_rev);
+    hipLaunchKernelGGL((scan_bf16_kernel<DK, FROZEN, DECAY>), dim3(nwg), dim3(kThreads), 0, stream,
+                       Mat, Bm, o.alpha, o.text_state, F, d_v, nwg, inv_u, inv_sqrt_u, S_fwd, S_rev);
   return hipGetLastError();
+}
+
+template <int DK>
+hipError_t launch_scan_t(bool exact_f32, const float* Mat, const float* Bm, int F, int H, int d_v,
+                         const ScanOptions& o, float* S_fwd, float* S_rev, hipStream_t stream) {
+  const bool decay = o.alpha != nullptr;
+  if (o.frozen)
+    return decay ? launch_scan_v<DK, true, true>(exact_f32, Mat, Bm, F, H, d_v, o, S_fwd, S_rev, stream)
+                 : launch_scan_v<DK, true, false>(exact_f32, Mat, Bm, F, H, d_v, o, S_fwd, S_rev, stream);
+  return decay ? launch_scan_v<DK, false, true>(exact_f32, Mat, Bm, F, H, d_v, o, S_fwd, S_rev, stream)
+               : launch_scan_v<DK, false, false>(exact_f32, Mat, Bm, F, H, d_v, o, S_fwd, S_rev, stream);
 }
 
 }  // namespace
 
-hipError_t launch_state_scan(bool exact_f32, const float* Inv, const float* Bm, int F, int H,
-                             int d_k, int d_v, float* S_fwd, float* S_rev, hipStream_t stream) {
+hipError_t launch_state_scan(bool exact_f32, const float* Mat, const float* Bm, int F, int H,
+                             int d_k, int d_v, const ScanOptions& o, float* S_fwd, float* S_rev,
+                             hipStream_t stream) {
   switch (d_k) {
-    case 32: return launch_scan_t<32>(exact_f32, Inv, Bm, F, H, d_v, S_fwd, S_rev, stream);
-    case 64: return launch_scan_t<64>(exact_f32, Inv, Bm, F, H, d_v, S_fwd, S_rev, stream);
-    case 128: return launch_scan_t<128>(exact_f32, Inv, Bm, F, H, d_v, S_fwd, S_rev, stream);
+    case 32: return launch_scan_t<32>(exact_f32, Mat, Bm, F, H, d_v, o, S_fwd, S_rev, stream);
+    case 64: return launch_scan_t<64>(exact_f32, Mat, Bm, F, H, d_v, o, S_fwd, S_rev, stream);
+    case 128: return launch_scan_t<128>(exact_f32, Mat, Bm, F, H, d_v, o, S_fwd, S_rev, stream);
     default: return hipErrorInvalidValue;
   }
 }

@@ -25,6 +25,9 @@ come from ``default_rng([seed, H_total])``.  Draw order inside a head: q, k,
 v (float32 normals), beta logits, then the optional zero mask and duplicate
 picks.  q, k, v are rounded to the storage type with round-to-nearest-even
 (bf16) or kept as float32.
+
+For the full operator: channel decays alpha uniform in [0.6, 1] and a text
+state S_T with N(0, 1) / 2 entries, each from its own salted stream.
 """
 from __future__ import annotations
 
@@ -204,6 +207,21 @@ def make_inputs(w: Workload, heads=None) -> dict:
             fill(item)
     out["gate"] = gates(w)[list(hs)]
     return out
+
+
+def make_decay(w: Workload, low: float = 0.6, salt: int = 101) -> np.ndarray:
+    """Channel decays alpha [H_total][F][d_k] float32, uniform in [low, 1]
+    (Proposition 1's range, 0 <= alpha <= 1), from default_rng([seed, salt])."""
+    rng = np.random.default_rng([w.seed, salt])
+    a = low + (1.0 - low) * rng.random((w.heads, w.F, w.d_k))
+    return a.astype(np.float32)
+
+
+def make_text_state(w: Workload, scale: float = 0.5, salt: int = 102) -> np.ndarray:
+    """A text state S_T [H_total][d_v][d_k] float32, scale * N(0, 1), from
+    default_rng([seed, salt])."""
+    rng = np.random.default_rng([w.seed, salt])
+    return (scale * rng.standard_normal((w.heads, w.d_v, w.d_k))).astype(np.float32)
 
 
 def as_float64(x: np.ndarray, dtype: str) -> np.ndarray:

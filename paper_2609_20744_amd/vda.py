@@ -35,10 +35,21 @@ STATUS_NAMES = {0: "VDA_OK", 1: "VDA_ERR_NULL", 2: "VDA_ERR_SIZE", 3: "VDA_ERR_U
 _P = ctypes.c_void_p
 _I = ctypes.c_int
 
+class VdaOptions(ctypes.Structure):
+    """struct vda_options (include/vda.h)."""
+    _fields_ = [("rule", ctypes.c_int), ("alpha", ctypes.c_void_p),
+                ("text_state", ctypes.c_void_p), ("window_chunk", ctypes.c_int),
+                ("window_radius", ctypes.c_int), ("window_offset", ctypes.c_int)]
+
+
+RULES = {"joint": 0, "frozen": 1}
+
 _SIGNATURES = {
     "vda_status_string": (ctypes.c_char_p, [_I]),
     "vda_forward": (_I, [_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _P, _P]),
     "vda_forward_f32": (_I, [_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _P, _P]),
+    "vda_forward_ex": (_I, [_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _P, _P, _P]),
+    "vda_forward_ex_f32": (_I, [_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _P, _P, _P]),
     "vda_default_split_plan": (_I, [_I, _I, _I, _I, _I, _I, _P, _P]),
     "vda_frame_stats": (_I, [_P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _P, _P, _P]),
     "vda_frame_inverse": (_I, [_P, _P, _I, _I, _I, _I, _I, _P, _P]),
@@ -135,8 +146,14 @@ def _shape(q, k, v, beta, gate=None):
     return lead, F, N, H, d_k, d_v
 
 
-def forward(q, k, v, beta, gate, out=None, stream=None):
-    """VDA forward (vda_forward for bf16 tensors, vda_forward_f32 for fp32)."""
+def forward(q, k, v, beta, gate, out=None, stream=None, alpha=None, text_state=None,
+            window=None, rule="joint"):
+    """VDA forward (vda_forward for bf16 tensors, vda_forward_f32 for fp32).
+
+    With any of the full-operator options it calls vda_forward_ex(_f32):
+    alpha [..., F, d_k] fp32 channel decays, text_state [..., d_v, d_k] fp32
+    S_T, window = (chunk, radius, offset) of the local window, and rule
+    'joint' (Eq. 5) or 'frozen' (Eq. 3c with 1/sqrt(U) key scaling)."""
     torch = _torch()
     dt = q.dtype
     if dt not in (torch.bfloat16, torch.float32):
@@ -155,10 +172,32 @@ def forward(q, k, v, beta, gate, out=None, stream=None):
         _require(out, "out", dt, dev)
         if tuple(out.shape) != lead + (F, N, d_v):
             raise ValueError(f"out shape {tuple(out.shape)} must be {lead + (F, N, d_v)}")
-    fn = lib.vda_forward if dt == torch.bfloat16 else lib.vda_forward_f32
+    if alpha is None and text_state is None and window is None and rule == "joint":
+        fn = lib.vda_forward if dt == torch.bfloat16 else lib.vda_forward_f32
+        with torch.cuda.device(dev):
+            st = fn(q.data_ptr(), k.data_ptr(), v.data_ptr(), beta.data_ptr(), gate.data_ptr(),
+                    F, N, H, d_k, d_v, out.data_ptr(), _stream_ptr(dev, stream))
+        _check(st, fn.__name__)
+        return out
+    if rule not in RULES:
+        raise ValueError(f"rule must be one of {sorted(RULES)}")
+    if alpha is not None:
+        _require(alpha, "alpha", torch.float32, dev)
+        if tuple(alpha.shape) != lead + (F, d_k):
+            raise ValueError(f"alpha shape {tuple(alpha.shape)} must be {lead + (F, d_k)}")
+    if text_state is not None:
+        _require(text_state, "text_state", torch.float32, dev)
+        if tuple(text_state.shape) != lead + (d_v, d_k):
+            raise ValueError(f"text_state shape {tuple(text_state.shape)} must be "
+                             f"{lead + (d_v, d_k)}")
+    chunk, radius, offset = (1, 0, 0) if window is None else (int(x) for x in window)
+    opts = VdaOptions(RULES[rule], alpha.data_ptr() if alpha is not None else None,
+                      text_state.data_ptr() if text_state is not None else None,
+                      chunk, radius, offset)
+    fn = lib.vda_forward_ex if dt == torch.bfloat16 else lib.vda_forward_ex_f32
     with torch.cuda.device(dev):
         st = fn(q.data_ptr(), k.data_ptr(), v.data_ptr(), beta.data_ptr(), gate.data_ptr(),
-                F, N, H, d_k, d_v, out.data_ptr(), _stream_ptr(dev, stream))
+                F, N, H, d_k, d_v, ctypes.byref(opts), out.data_ptr(), _stream_ptr(dev, stream))
     _check(st, fn.__name__)
     return out
 

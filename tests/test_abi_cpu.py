@@ -14,7 +14,7 @@ def test_exports_every_declared_symbol():
     names = vda.header_functions()
     assert set(names) >= {"vda_forward", "vda_forward_f32", "vda_status_string", "vda_frame_stats",
                           "vda_frame_inverse", "vda_state_scan", "vda_readout",
-                          "vda_default_split_plan"}
+                          "vda_default_split_plan", "vda_forward_ex", "vda_forward_ex_f32"}
     for n in names:
         assert hasattr(vda.lib, n), n
     assert set(names) == set(vda._SIGNATURES)
@@ -109,3 +109,29 @@ def test_single_hip_runtime_loaded():
     maps = open(f"/proc/{os.getpid()}/maps").read()
     libs = {l.split()[-1] for l in maps.splitlines() if "libamdhip64" in l}
     assert len(libs) == 1, libs
+
+
+def test_forward_ex_validation():
+    import ctypes
+    big = 1 << 32
+    L = vda.lib
+
+    def ex(opts, out=6 * big, d_k=64, d_v=64):
+        return L.vda_forward_ex(big, 2 * big, 3 * big, 4 * big, 5 * big, 4, 64, 2, d_k, d_v,
+                                None if opts is None else ctypes.byref(opts), out, None)
+
+    def opts(rule=0, alpha=None, ts=None, chunk=1, radius=0, offset=0):
+        return vda.VdaOptions(rule, alpha, ts, chunk, radius, offset)
+
+    assert ex(opts(rule=2)) == 3                        # unknown rule
+    assert ex(opts(chunk=0)) == 2
+    assert ex(opts(radius=-1)) == 2
+    assert ex(opts(chunk=5, offset=5)) == 2             # offset must be < chunk
+    assert ex(opts(alpha=7 * big + 8)) == 4             # alpha 16-byte aligned
+    assert ex(opts(ts=7 * big + 2)) == 4
+    # out overlapping alpha or the text state
+    assert ex(opts(alpha=7 * big), out=7 * big + 64) == 5
+    assert ex(opts(ts=8 * big), out=8 * big - 64) == 5
+    assert ex(opts(), d_k=48) == 3
+    assert L.vda_forward_ex(None, 2 * big, 3 * big, 4 * big, 5 * big, 4, 64, 2, 64, 64, None,
+                            6 * big, None) == 1
