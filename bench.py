@@ -362,6 +362,32 @@ def main() -> int:
                      "unit": "GB/s", "frac": ach / PEAK_HBM_GBS,
                      "traffic": measured_traffic(w.name, dominant)},
     }
+    # 3. The full operator (vda_forward_ex) on the same workload, with every
+    #    option: channel decay, text state, the paper's local window (chunks
+    #    of five frames, radius one, one leading anchor), for both rules.
+    #    Reported beside the headline, not as it.
+    alpha = dev(I.make_decay(w), "f32")
+    text_state = dev(I.make_text_state(w), "f32")
+    full = {}
+    for rule in ("joint", "frozen"):
+        def fwd_ex():
+            vda.forward(q, k, v, beta, gate, out=out, alpha=alpha, text_state=text_state,
+                        window=(5, 1, 1), rule=rule)
+        for _ in range(max(2, args.warmup)):
+            fwd_ex()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(K):
+            fwd_ex()
+        e1.record()
+        torch.cuda.synchronize()
+        ms_ex = e0.elapsed_time(e1) / K
+        full[f"{rule}_decay_text_window"] = {"ms_per_step": ms_ex,
+                                             "tokens_per_s": w.tokens / (ms_ex / 1e3)}
+        print(f"[bench] vda_forward_ex ({rule}, all options): {ms_ex:.4f} ms/step",
+              file=sys.stderr, flush=True)
+    result["full_operator"] = full
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
         result["cpu_baseline"] = cpu_baseline(w, args.cpu_budget)
