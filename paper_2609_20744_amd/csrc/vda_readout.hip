@@ -61,7 +61,9 @@ void readout_bf16_kernel(const uint16_t* __restrict__ Q, const float* __restrict
   constexpr int SLD = DK + 8;  // bf16 row stride of S~ in LDS
   constexpr int MB = DV / 16;  // 16-row blocks of S~ (output channels)
   constexpr int KB = DK / 32;  // 32-wide k steps
+  constexpr int OLD = DV + 8;  // bf16 row stride of the output staging tiles
   __shared__ __align__(16) uint16_t st[DV * SLD];
+  __shared__ __align__(16) uint16_t otile[4 * 16 * OLD];  // one 16-token tile per wave
 
   // The chunks of one frame read the same two states: keep them on one XCD.
   const unsigned L = xcd_grouped_id(blockIdx.x, nwg);
@@ -165,23 +167,23 @@ void readout_bf16_kernel(const uint16_t* __restrict__ Q, const float* __restrict
       ss += __shfl_xor(ss, 16);
       ss += __shfl_xor(ss, 32);
       const float scale = g / sqrtf(ss * inv_norm + kRmsEps);
-      // 16-byte stores: for each pair of row blocks (2m, 2m+1), lane groups
-      // 2p and 2p+1 (lanes l and l ^ 16) swap one 4-channel piece with
-      // v_permlane16_swap, after which lane group 2p holds channels
-      // 32m + 8p .. +7 of block 2m's rows and lane group 2p+1 the same
-      // channels of block 2m+1 (+16).  Each store then writes 64 contiguous
-      // bytes of each of 16 token rows.
-      const uint32_t off =
-          ((uint32_t)(ng + li) * DV + (lg & 1) * 16 + (lg >> 1) * 8) * 2u;
+      // Stores of whole token rows: the group's outputs (16 tokens x DV,
+      // bf16) go through this wave's LDS tile, then each store instruction
+      // writes 64 / (DV / 8) consecutive token rows, one contiguous run of
+      // up to 1 KB.
+      uint16_t* tile = otile + wave * (16 * OLD);
 #pragma unroll
-      for (int m = 0; m < MB / 2; ++m) {
-        const uint32_t a0 = pack_bf16x2(acc[2 * m][0] * scale, acc[2 * m][1] * scale);
-        const uint32_t a1 = pack_bf16x2(acc[2 * m][2] * scale, acc[2 * m][3] * scale);
-        const uint32_t b0 = pack_bf16x2(acc[2 * m + 1][0] * scale, acc[2 * m + 1][1] * scale);
-        const uint32_t b1 = pack_bf16x2(acc[2 * m + 1][2] * scale, acc[2 * m + 1][3] * scale);
-        const auto s0 = __builtin_amdgcn_permlane16_swap(a0, b0, false, false);
-        const auto s1 = __builtin_amdgcn_permlane16_swap(a1, b1, false, false);
-        store_b128_stream(orsrc, off + m * 64u, u32x4{s0[0], s1[0], s0[1], s1[1]});
+      for (int mb = 0; mb < MB; ++mb)
+        *reinterpret_cast<uint2*>(&tile[li * OLD + mb * 16 + 4 * lg]) =
+            make_uint2(pack_bf16x2(acc[mb][0] * scale, acc[mb][1] * scale),
+                       pack_bf16x2(acc[mb][2] * scale, acc[mb][3] * scale));
+      constexpr int CPR = DV / 8;     // 16-byte chunks per token row
+      constexpr int RPI = 64 / CPR;   // token rows per store instruction
+#pragma unroll
+      for (int r0 = 0; r0 < 16; r0 += RPI) {
+        const int tok = r0 + lane / CPR, ch = lane % CPR;
+        const u32x4 v = *reinterpret_cast<const u32x4*>(&tile[tok * OLD + ch * 8]);
+        store_b128_stream(orsrc, ((uint32_t)(ng + tok) * DV + ch * 8) * 2u, v);
       }
     }
   }
