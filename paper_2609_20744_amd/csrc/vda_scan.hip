@@ -261,39 +261,40 @@ __device__ __forceinline__ void upper_chunk(int f, int& row, int& col) {
 // Matrix-core phase of one scan step for wave W (a template, so that which
 // operand halves are read along rows and which down columns is fixed at
 // compile time and no branch separates the LDS reads): out = x Inv_t for
-// this wave's 16-column slices, x being the 16 x d_k block in LDS (row
-// stride XLD) and Inv_t the upper-triangle image.
+// this wave's 16-column slices.  x, the 16 x d_k block, comes already split
+// into bf16 hi and lo planes (row stride PLD); Inv_t is the upper-triangle
+// image (row stride XLD).  Even and odd k steps accumulate separately, which
+// halves the chain of dependent matrix products.
 template <int DK, int W>
-__device__ __forceinline__ void scan_mfma_phase(const float* __restrict__ xs_cur,
+__device__ __forceinline__ void scan_mfma_phase(const uint16_t* __restrict__ xhi,
+                                                const uint16_t* __restrict__ xlo,
                                                 float* __restrict__ xs_next,
                                                 const float* __restrict__ ivs, int li, int lg) {
   constexpr int XLD = DK + 4;
+  constexpr int PLD = DK + 8;
   constexpr int NB = DK / 16;
   constexpr int NBW = (NB + 3) / 4;
   constexpr int KB = DK / 32;
   if constexpr (W >= NB) {
     return;  // d_k = 32: two slices, waves 2 and 3 idle
   } else {
-    // A-operand: row li of the block at this lane's k values.
+    // A-operand: row li of the block at k = 32 ks + 4 lg + e, 32 ks + 16 + 4 lg + e.
     bf16x8 ahi[KB], alo[KB];
-    const floatx4* xr = reinterpret_cast<const floatx4*>(xs_cur) + (li * XLD + 4 * lg) / 4;
 #pragma unroll
     for (int ks = 0; ks < KB; ++ks) {
-      float t[8];
-      const floatx4 v0 = xr[8 * ks];
-      const floatx4 v1 = xr[8 * ks + 4];
-#pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        t[c] = v0[c];
-        t[4 + c] = v1[c];
-      }
-      split_bf16x8(t, ahi[ks], alo[ks]);
+      const int o = li * PLD + 32 * ks + 4 * lg;
+      const u32x2 h0 = *reinterpret_cast<const u32x2*>(&xhi[o]);
+      const u32x2 h1 = *reinterpret_cast<const u32x2*>(&xhi[o + 16]);
+      const u32x2 l0 = *reinterpret_cast<const u32x2*>(&xlo[o]);
+      const u32x2 l1 = *reinterpret_cast<const u32x2*>(&xlo[o + 16]);
+      ahi[ks] = __builtin_bit_cast(bf16x8, u32x4{h0[0], h0[1], h1[0], h1[1]});
+      alo[ks] = __builtin_bit_cast(bf16x8, u32x4{l0[0], l0[1], l1[0], l1[1]});
     }
 #pragma unroll
     for (int m = 0; m < NBW; ++m) {
       const int nb = W + 4 * m;
       if (nb < NB) {
-        floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+        floatx4 acc[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
 #pragma unroll
         for (int ks = 0; ks < KB; ++ks) {
           // B-operand: Inv[k][16 nb + li] at this lane's k values, in two
@@ -314,12 +315,14 @@ __device__ __forceinline__ void scan_mfma_phase(const float* __restrict__ xs_cur
           }
           bf16x8 bhi, blo;
           split_bf16x8(t, bhi, blo);
-          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(alo[ks], bhi, acc, 0, 0, 0);
-          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi[ks], blo, acc, 0, 0, 0);
-          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi[ks], bhi, acc, 0, 0, 0);
+          floatx4& a = acc[ks & 1];
+          a = __builtin_amdgcn_mfma_f32_16x16x32_bf16(alo[ks], bhi, a, 0, 0, 0);
+          a = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi[ks], blo, a, 0, 0, 0);
+          a = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi[ks], bhi, a, 0, 0, 0);
         }
 #pragma unroll
-        for (int i = 0; i < 4; ++i) xs_next[(lg * 4 + i) * XLD + nb * 16 + li] = acc[i];
+        for (int i = 0; i < 4; ++i)
+          xs_next[(lg * 4 + i) * XLD + nb * 16 + li] = acc[0][i] + acc[1][i];
       }
     }
   }
@@ -370,8 +373,10 @@ void scan_bf16_kernel(const float* __restrict__ Mat, const float* __restrict__ B
   constexpr int NG = DK / (16 * VW);    // accesses per thread in the row-wise phase
   using U = UpperChunks<DK>;
   constexpr int CPT = U::per_thread;
+  constexpr int PLD = DK + 8;        // bf16 row stride of the split planes
   __shared__ __align__(16) float ivs[(DK + 1) * XLD];  // matrix image, plus a dummy row
   __shared__ __align__(16) float xs[2][16 * XLD];
+  __shared__ __align__(16) uint16_t xsp[2][16 * PLD];   // bf16 hi / lo planes of the block
   __shared__ __align__(16) float alds[DECAY ? DK : 4];  // alpha of the coming step
 
   const int nrb = DV / 16;
@@ -530,11 +535,24 @@ void scan_bf16_kernel(const float* __restrict__ Mat, const float* __restrict__ B
 #pragma unroll
           for (int c = 0; c < VW; ++c) v[c] += bb[g][c];
         }
-        if constexpr (VW == 4)
-          reinterpret_cast<floatx4*>(xs[cur])[(pr * XLD + pc + g * 16 * VW) / 4] =
-              floatx4{v[0], v[1], v[2], v[3]};
-        else
-          *reinterpret_cast<float2*>(x) = make_float2(v[0], v[1]);
+        // The product's A-operand, split once here into bf16 hi and lo
+        // (instead of by each of the four waves).
+        uint32_t hw[VW / 2], lw[VW / 2];
+#pragma unroll
+        for (int c = 0; c < VW; c += 2) {
+          const uint32_t h = pack_bf16x2(v[c], v[c + 1]);
+          hw[c / 2] = h;
+          lw[c / 2] = pack_bf16x2(v[c] - bf16_lo(h), v[c + 1] - bf16_hi(h));
+        }
+        const int po = pr * PLD + pc + g * 16 * VW;
+        if constexpr (VW == 4) {
+          *reinterpret_cast<u32x2*>(&xsp[0][po]) = u32x2{hw[0], hw[1]};
+          *reinterpret_cast<u32x2*>(&xsp[1][po]) = u32x2{lw[0], lw[1]};
+        } else {
+          *reinterpret_cast<uint32_t*>(&xsp[0][po]) = hw[0];
+          *reinterpret_cast<uint32_t*>(&xsp[1][po]) = lw[0];
+        }
+        (void)x;
       }
     }
     lds_barrier();
@@ -547,10 +565,10 @@ void scan_bf16_kernel(const float* __restrict__ Mat, const float* __restrict__ B
     // hides the loads from the wait-count bookkeeping.
     load_step(min(step + 2, F - 1), ir, bb, al);
     switch (wave) {  // wave-uniform
-      case 0: scan_mfma_phase<DK, 0>(xs[cur], xs[cur ^ 1], ivs, li, lg); break;
-      case 1: scan_mfma_phase<DK, 1>(xs[cur], xs[cur ^ 1], ivs, li, lg); break;
-      case 2: scan_mfma_phase<DK, 2>(xs[cur], xs[cur ^ 1], ivs, li, lg); break;
-      default: scan_mfma_phase<DK, 3>(xs[cur], xs[cur ^ 1], ivs, li, lg); break;
+      case 0: scan_mfma_phase<DK, 0>(xsp[0], xsp[1], xs[cur ^ 1], ivs, li, lg); break;
+      case 1: scan_mfma_phase<DK, 1>(xsp[0], xsp[1], xs[cur ^ 1], ivs, li, lg); break;
+      case 2: scan_mfma_phase<DK, 2>(xsp[0], xsp[1], xs[cur ^ 1], ivs, li, lg); break;
+      default: scan_mfma_phase<DK, 3>(xsp[0], xsp[1], xs[cur ^ 1], ivs, li, lg); break;
     }
     cur ^= 1;
   };
