@@ -67,10 +67,10 @@ def kernel_bytes(w, heads=None):
 # Kernel of each stage, and the sources whose change makes counters taken
 # on it stale.
 KERNEL_OF = {"frame_stats": "stats_bf16_kernel", "frame_inverse": "inverse_kernel",
-             "state_scan": "scan_bf16_kernel", "readout": "readout_bf16_kernel"}
+             "state_scan": "scan_tiled_kernel", "readout": "readout_bf16_kernel"}
 SOURCE_OF = {"frame_stats": ("vda_stats.hip",),
              "frame_inverse": ("vda_inverse.hip", "vda_inverse_body.h"),
-             "state_scan": ("vda_scan.hip",), "readout": ("vda_readout.hip",)}
+             "state_scan": ("vda_scan_tiled.hip",), "readout": ("vda_readout.hip",)}
 
 
 def source_hash(stage: str) -> str:
@@ -297,9 +297,11 @@ def main() -> int:
                 lambda: vda.frame_stats(k[sl], v[sl], beta[sl], splits=sp, tail_frames=tail,
                                         A_part=A_part, B_part=B_part),
                 lambda: vda.frame_inverse(A_part, B_part, count=c, tail_frames=tail, splits=sp,
-                                          Inv=Inv),
-                lambda: vda.state_scan(Inv.view(-1, F, dk, dk), B_part[:c].view(-1, F, dv, dk),
-                                       S_fwd, S_rev, exact_f32=(w.dtype == "f32")),
+                                          Inv=Inv, tiles=(w.dtype != "f32")),
+                (lambda: vda.state_scan(Inv.view(-1, F, dk, dk), B_part[:c].view(-1, F, dv, dk),
+                                        S_fwd, S_rev, exact_f32=True)) if w.dtype == "f32" else
+                (lambda: vda.state_scan_tiles(Inv.view(-1, F, dk * dk),
+                                              B_part[:c].view(-1, F, dv, dk), S_fwd, S_rev)),
                 lambda: vda.readout(q[sl], S_fwd, S_rev, gate[sl], out=out[sl]),
             )
             for fn in launches:

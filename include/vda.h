@@ -30,6 +30,8 @@
  *    H counts independent head problems (batch folded in: H = B * heads).
  *  - Supported head dimensions: d_k, d_v in {32, 64, 128} for every entry
  *    point, and also 16 for vda_forward / vda_forward_f32.  F, N, H >= 1.
+ *    Offsets are 32-bit: H*F*64, N*d*4 and F*d*d*4 (d the larger of d_k and
+ *    d_v, at least 32) must each stay below 2^31 (else VDA_ERR_SIZE).
  *  - q, k, v, out and the fp32 work buffers must be 16-byte aligned; beta and
  *    gate 4-byte aligned.  out must not overlap any input.
  *  - Every call is asynchronous on `stream` (0 = the null stream): it
@@ -76,7 +78,8 @@ const char* vda_status_string(int status);
  * bf16 storage for q, k, v (inputs) and out (output, round-to-nearest-even).
  * Frame statistics and the readout run on bf16 matrix cores with fp32
  * accumulation; (I + A_t)^{-1}, the recurrent states and the epilogue are
- * fp32, and the state products use split-bf16 operands (see vda_state_scan).
+ * fp32, and the state products use split-bf16 operands (vda_frame_inverse_tiles
+ * and vda_state_scan_tiles are its steps a2-a4).
  * Workspace of (P*(d_k*d_k + d_v*d_k) + 2*H*F*d_v*d_k)*4 bytes, with
  * P = H*F + T*(S-1) partials of the plan (T, S) = vda_default_split_plan(F,
  * N, H, d_k, d_v, is_f32) (P = H*F when S == 1), comes from a per-device cache of
@@ -259,6 +262,46 @@ int vda_frame_inverse(const float* A_part, float* B_part, int tail_frames, int s
 int vda_state_scan(const float* Inv, const float* B,
                    int F, int H, int d_k, int d_v, int is_f32,
                    float* S_fwd, float* S_rev, hipStream_t stream);
+
+/*
+ * Split-bf16 operand tiles.  The bf16 storage path passes each inverse
+ * Inv_t (d_k x d_k, symmetric) from step a2 to the state scan pre-split for
+ * the scan's bf16 matrix products: every element x is stored as
+ * hi = bf16(x) and lo = bf16(x - hi) (round-to-nearest-even), in the order
+ * in which the scan's matrix instructions take them.  One frame's tiles fill
+ * d_k*d_k*4 bytes (the size of the fp32 matrix): two planes (p = 0: hi,
+ * p = 1: lo) of d_k*d_k bf16 values, plane p at byte p*d_k*d_k*2.  Within a
+ * plane, for nb < d_k/16, ks < d_k/32, lane < 64 and e < 8, the value at
+ * bf16 index ((nb*(d_k/32) + ks)*64 + lane)*8 + e is element [k][n] of
+ * Inv_t with
+ *     n = 16*nb + lane % 16,
+ *     k = 32*ks + 4*(lane / 16) + e        for e < 4,
+ *     k = 32*ks + 16 + 4*(lane / 16) + e - 4  for e >= 4.
+ */
+
+/*
+ * vda_frame_inverse_tiles -- step a2 as vda_frame_inverse (same arguments,
+ * checks, split plan, in-place rule and B folding), with each inverse written
+ * as split-bf16 operand tiles (above) instead of an fp32 matrix.  Inv_tiles
+ * is count * d_k*d_k*4 bytes.  This is the inverse vda_forward runs with
+ * bf16 storage (joint rule).
+ */
+int vda_frame_inverse_tiles(const float* A_part, float* B_part, int tail_frames, int splits,
+                            int count, int d_k, int d_v, void* Inv_tiles, hipStream_t stream);
+
+/*
+ * vda_state_scan_tiles -- steps a3 and a4 as vda_state_scan with
+ * is_f32 == 0 (same recurrence, zero initial state, outputs and split-bf16
+ * products with fp32 accumulation and fp32 state), reading each Inv_t from
+ * split-bf16 operand tiles: Inv_tiles is [H][F] frames of d_k*d_k*4 bytes
+ * (vda_frame_inverse_tiles writes them).  Element [k][n] of each tile set is
+ * used as Inv_t[k][n] (no symmetry is assumed).  This is the scan
+ * vda_forward runs with bf16 storage (joint rule).  Errors as
+ * vda_state_scan.
+ */
+int vda_state_scan_tiles(const void* Inv_tiles, const float* B,
+                         int F, int H, int d_k, int d_v,
+                         float* S_fwd, float* S_rev, hipStream_t stream);
 
 /*
  * vda_readout -- steps a5-a7, Eq. A.4 (own-frame window), Eq. 1a and Eq. 1c:

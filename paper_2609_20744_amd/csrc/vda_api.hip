@@ -46,9 +46,11 @@ int check_shape(int F, int N, int H, int d_k, int d_v, bool forward = false) {
               : !(supported_dim(d_k) && supported_dim(d_v)))
     return VDA_ERR_UNSUPPORTED;
   if ((long long)H * F * 64 > 0x7fffffffLL) return VDA_ERR_SIZE;
-  // Byte offsets within one frame of one head are 32-bit.
+  // Byte offsets within one frame of one head, and within one head's
+  // per-frame matrices, are 32-bit.
   const int dmax = padded_dim(d_k > d_v ? d_k : d_v);
   if ((long long)N * dmax * 4 > 0x7fffffffLL) return VDA_ERR_SIZE;
+  if ((long long)F * dmax * dmax * 4 > 0x7fffffffLL) return VDA_ERR_SIZE;
   return VDA_OK;
 }
 
@@ -303,16 +305,21 @@ int forward_impl(bool is_f32, const void* q, const void* k, const void* v, const
   if (e == hipSuccess)
     e = vda::launch_frame_stats(is_f32, kx, vx, beta, F, N, H, pk, pv, plan, A_part, B_part,
                                 stream);
+  // With bf16 storage the joint rule's inverse is written as split-bf16
+  // operand tiles for the state scan.
+  const bool tiled = !is_f32 && !frozen;
   if (e == hipSuccess && !frozen)
-    e = vda::launch_frame_inverse(A_part, B_part, plan, (long long)H * F, pk, pv, Inv, stream);
+    e = vda::launch_frame_inverse(A_part, B_part, plan, (long long)H * F, pk, pv, tiled, Inv,
+                                  stream);
   vda::ScanOptions so;
   so.frozen = frozen;
   so.alpha = alpha_x;
   so.text_state = ts_x;
   so.tokens = N;
   if (e == hipSuccess)
-    e = vda::launch_state_scan(is_f32, frozen ? A_part : Inv, B_part, F, H, pk, pv, so, S_fwd,
-                               S_rev, stream);
+    e = tiled ? vda::launch_state_scan_tiled(Inv, B_part, F, H, pk, pv, so, S_fwd, S_rev, stream)
+              : vda::launch_state_scan(is_f32, frozen ? A_part : Inv, B_part, F, H, pk, pv, so,
+                                       S_fwd, S_rev, stream);
   vda::GatherOptions go;
   go.alpha = alpha_x;
   go.chunk = o.window_chunk;
@@ -382,6 +389,10 @@ int vda_default_split_plan(int F, int N, int H, int d_k, int d_v, int is_f32, in
   return VDA_OK;
 }
 
+}  // extern "C"
+
+namespace {
+
 // Shared checks of a split plan over `count` frames of N tokens.
 int check_plan(long long count, int N, int tail_frames, int splits) {
   if (splits < 1) return VDA_ERR_SIZE;
@@ -392,6 +403,10 @@ int check_plan(long long count, int N, int tail_frames, int splits) {
   if (vda::stats_workgroups(count, p) > 0x7fffffffLL) return VDA_ERR_SIZE;
   return VDA_OK;
 }
+
+}  // namespace
+
+extern "C" {
 
 int vda_frame_stats(const void* k, const void* v, const float* beta, int F, int N, int H,
                     int d_k, int d_v, int tail_frames, int splits, int is_f32, float* A_part,
@@ -419,8 +434,12 @@ int vda_frame_stats(const void* k, const void* v, const float* beta, int F, int 
                                             A_part, B_part, stream));
 }
 
-int vda_frame_inverse(const float* A_part, float* B_part, int tail_frames, int splits, int count,
-                      int d_k, int d_v, float* Inv, hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+int frame_inverse(const float* A_part, float* B_part, int tail_frames, int splits, int count,
+                  int d_k, int d_v, bool tiled, float* Inv, hipStream_t stream) {
   if (!A_part || !Inv || (splits > 1 && !B_part)) return VDA_ERR_NULL;
   if (count < 1 || (long long)count * 64 > 0x7fffffffLL) return VDA_ERR_SIZE;
   // N is not known here; any split count the statistics step accepted is fine.
@@ -441,11 +460,14 @@ int vda_frame_inverse(const float* A_part, float* B_part, int tail_frames, int s
     const Range rb = range_of(B_part, parts * d_v * d_k * 4);
     if (overlaps(rb, ri) || overlaps(rb, ra)) return VDA_ERR_OVERLAP;
   }
-  return hip_status(vda::launch_frame_inverse(A_part, B_part, plan, count, d_k, d_v, Inv, stream));
+  return hip_status(
+      vda::launch_frame_inverse(A_part, B_part, plan, count, d_k, d_v, tiled, Inv, stream));
 }
 
-int vda_state_scan(const float* Inv, const float* B, int F, int H, int d_k, int d_v, int is_f32,
-                   float* S_fwd, float* S_rev, hipStream_t stream) {
+// Checks of the state-scan stage entry points (matrix operand of d_k*d_k*4
+// bytes per frame in either layout).
+int check_scan(const void* Inv, const float* B, int F, int H, int d_k, int d_v, float* S_fwd,
+               float* S_rev) {
   if (!Inv || !B || !S_fwd || !S_rev) return VDA_ERR_NULL;
   int st = check_shape(F, 1, H, d_k, d_v);
   if (st != VDA_OK) return st;
@@ -458,8 +480,38 @@ int vda_state_scan(const float* Inv, const float* B, int F, int H, int d_k, int 
   if (overlaps(rf, rr) || overlaps(rf, ri) || overlaps(rf, rb) || overlaps(rr, ri) ||
       overlaps(rr, rb))
     return VDA_ERR_OVERLAP;
+  return VDA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int vda_frame_inverse(const float* A_part, float* B_part, int tail_frames, int splits, int count,
+                      int d_k, int d_v, float* Inv, hipStream_t stream) {
+  return frame_inverse(A_part, B_part, tail_frames, splits, count, d_k, d_v, false, Inv, stream);
+}
+
+int vda_frame_inverse_tiles(const float* A_part, float* B_part, int tail_frames, int splits,
+                            int count, int d_k, int d_v, void* Inv_tiles, hipStream_t stream) {
+  return frame_inverse(A_part, B_part, tail_frames, splits, count, d_k, d_v, true,
+                       static_cast<float*>(Inv_tiles), stream);
+}
+
+int vda_state_scan(const float* Inv, const float* B, int F, int H, int d_k, int d_v, int is_f32,
+                   float* S_fwd, float* S_rev, hipStream_t stream) {
+  const int st = check_scan(Inv, B, F, H, d_k, d_v, S_fwd, S_rev);
+  if (st != VDA_OK) return st;
   return hip_status(vda::launch_state_scan(is_f32 != 0, Inv, B, F, H, d_k, d_v, vda::ScanOptions(),
                                            S_fwd, S_rev, stream));
+}
+
+int vda_state_scan_tiles(const void* Inv_tiles, const float* B, int F, int H, int d_k, int d_v,
+                         float* S_fwd, float* S_rev, hipStream_t stream) {
+  const int st = check_scan(Inv_tiles, B, F, H, d_k, d_v, S_fwd, S_rev);
+  if (st != VDA_OK) return st;
+  return hip_status(vda::launch_state_scan_tiled(Inv_tiles, B, F, H, d_k, d_v, vda::ScanOptions(),
+                                                 S_fwd, S_rev, stream));
 }
 
 int vda_readout(const void* q, const float* S_fwd, const float* S_rev, const float* gate, int F,

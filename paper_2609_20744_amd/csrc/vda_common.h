@@ -50,6 +50,24 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, ui
                                            0x00020000);
 }
 
+// Split-bf16 operand tiles of a d_k x d_k fp32 matrix X (the inverse
+// (I + A_t)^{-1} on the bf16 storage path, written by the inverse and read
+// by the state scan).  The scan's product x X of a 16-row block x on
+// v_mfma_f32_16x16x32_bf16 takes, for output columns 16 nb .. 16 nb + 15
+// and k step ks, one 8-element B-operand per lane (li, lg) =
+// (lane % 16, lane / 16):
+//     X[32 ks + 4 lg + r][16 nb + li] for r < 4, then
+//     X[32 ks + 16 + 4 lg + r][16 nb + li] for r < 4
+// (the k order the scan uses in both operands).  Each operand is stored as
+// its bf16 part hi = RNE(x) in plane 0 and lo = RNE(x - hi) in plane 1, so
+// one wave's operand of one (nb, ks) tile is 1 KB of contiguous memory.  The
+// layout has d_k * d_k * 4 bytes, as many as the fp32 matrix.
+__host__ __device__ constexpr uint32_t operand_tile_offset(int dk, int plane, int nb, int ks,
+                                                           int lane) {
+  return (uint32_t)plane * (uint32_t)(dk * dk * 2) +
+         ((uint32_t)(nb * (dk / 32) + ks) * 64u + (uint32_t)lane) * 16u;
+}
+
 typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 

@@ -1,6 +1,8 @@
 // Step a2 as a stand-alone kernel: Inv_t = (I + A_t)^{-1} for every frame
 // of every head (Eq. 5), one workgroup per matrix.  The algorithm is
-// described in vda_inverse_body.h.
+// described in vda_inverse_body.h.  The result is written as an fp32
+// matrix, or (TILED, for the split-bf16 state scan) as split-bf16 operand
+// tiles (operand_tile_offset).
 #include "vda_common.h"
 #include "vda_inverse_body.h"
 #include "vda_launch.h"
@@ -8,8 +10,12 @@
 namespace vda {
 namespace {
 
-template <int DK>
+// Three workgroups per SIMD (the registers of the tiled store would
+// otherwise push it to two), so one matrix's serial pivot work hides behind
+// the others' products.
+template <int DK, bool TILED>
 __global__ __launch_bounds__(64 * (DK / 16 < 4 ? DK / 16 : 4))
+__attribute__((amdgpu_waves_per_eu(3)))
 void inverse_kernel(const float* A_part, unsigned first_split, int plan_splits, unsigned extra,
                     size_t part_stride,
                     float* Inv,  // may alias A_part (in place)
@@ -30,13 +36,13 @@ void inverse_kernel(const float* A_part, unsigned first_split, int plan_splits, 
   const size_t base = (size_t)blockIdx.x * (DK * DK);
   // Frames from first_split on were split into plan_splits token ranges.
   const int splits = blockIdx.x >= first_split ? plan_splits : 1;
-  inv::invert_matrix<DK>(A_part, splits, part_stride, base, Inv, &piv[0][0][0], tid);
+  inv::invert_matrix<DK, TILED>(A_part, splits, part_stride, base, Inv, &piv[0][0][0], tid);
 }
 
 }  // namespace
 
 hipError_t launch_frame_inverse(const float* A_part, float* B_part, SplitPlan plan,
-                                long long count, int d_k, int d_v, float* Inv,
+                                long long count, int d_k, int d_v, bool tiled, float* Inv,
                                 hipStream_t stream) {
   const int splits = plan.splits > 1 && plan.tail > 0 ? plan.splits : 1;
   const unsigned first_split = splits > 1 ? (unsigned)(count - plan.tail) : (unsigned)count;
@@ -49,16 +55,28 @@ hipError_t launch_frame_inverse(const float* A_part, float* B_part, SplitPlan pl
   const dim3 grid((unsigned)count + extra);
   switch (d_k) {
     case 32:
-      hipLaunchKernelGGL(inverse_kernel<32>, grid, dim3(64 * 2), 0, stream, A_part, first_split,
-                         splits, extra, part_stride, Inv, B_part, b_mat, b_stride);
+      if (tiled)
+        hipLaunchKernelGGL((inverse_kernel<32, true>), grid, dim3(64 * 2), 0, stream, A_part,
+                           first_split, splits, extra, part_stride, Inv, B_part, b_mat, b_stride);
+      else
+        hipLaunchKernelGGL((inverse_kernel<32, false>), grid, dim3(64 * 2), 0, stream, A_part,
+                           first_split, splits, extra, part_stride, Inv, B_part, b_mat, b_stride);
       break;
     case 64:
-      hipLaunchKernelGGL(inverse_kernel<64>, grid, dim3(64 * 4), 0, stream, A_part, first_split,
-                         splits, extra, part_stride, Inv, B_part, b_mat, b_stride);
+      if (tiled)
+        hipLaunchKernelGGL((inverse_kernel<64, true>), grid, dim3(64 * 4), 0, stream, A_part,
+                           first_split, splits, extra, part_stride, Inv, B_part, b_mat, b_stride);
+      else
+        hipLaunchKernelGGL((inverse_kernel<64, false>), grid, dim3(64 * 4), 0, stream, A_part,
+                           first_split, splits, extra, part_stride, Inv, B_part, b_mat, b_stride);
       break;
     case 128:
-      hipLaunchKernelGGL(inverse_kernel<128>, grid, dim3(64 * 4), 0, stream, A_part, first_split,
-                         splits, extra, part_stride, Inv, B_part, b_mat, b_stride);
+      if (tiled)
+        hipLaunchKernelGGL((inverse_kernel<128, true>), grid, dim3(64 * 4), 0, stream, A_part,
+                           first_split, splits, extra, part_stride, Inv, B_part, b_mat, b_stride);
+      else
+        hipLaunchKernelGGL((inverse_kernel<128, false>), grid, dim3(64 * 4), 0, stream, A_part,
+                           first_split, splits, extra, part_stride, Inv, B_part, b_mat, b_stride);
       break;
     default:
       return hipErrorInvalidValue;

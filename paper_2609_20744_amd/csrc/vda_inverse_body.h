@@ -90,7 +90,7 @@ __device__ __forceinline__ void invert_pivot_block(float (&d)[4], int li, int lg
 // The elimination for the block rows of wave WV (rows WV, WV + W, ...); a
 // template on the wave so that every row-dependent condition is resolved at
 // compile time.  All W waves of the workgroup take the same NB barriers.
-template <int DK, int WV>
+template <int DK, int WV, bool TILED>
 __device__ __forceinline__ void invert_rows(const float* A_part, int splits, size_t part_stride,
                                             size_t base, float* Inv, float (*piv)[DK / 16][64 * 4],
                                             int lane) {
@@ -220,13 +220,36 @@ __device__ __forceinline__ void invert_rows(const float* A_part, int splits, siz
     }
   }
 
+  if constexpr (TILED) {
+    // Split-bf16 operand tiles (operand_tile_offset): block (i, j) at lane
+    // (li, lg) holds X[16i + 4lg + r][16j + li], which is half i % 2 of that
+    // lane's B-operand of tile (nb = j, ks = i / 2), so every lane writes
+    // its own 8-byte halves with no exchange.
+    char* t0 = reinterpret_cast<char*>(Inv + base);
 #pragma unroll
-  for (int q = 0; q < RPW; ++q) {
-    const int i = WV + W * q;
+    for (int q = 0; q < RPW; ++q) {
+      const int i = WV + W * q;
 #pragma unroll
-    for (int j = 0; j < NB; ++j)
-      *reinterpret_cast<float4*>(Inv + base + (size_t)(16 * j + li) * DK + 16 * i + 4 * lg) =
-          make_float4(acc[q][j][0], acc[q][j][1], acc[q][j][2], acc[q][j][3]);
+      for (int j = 0; j < NB; ++j) {
+        const floatx4 a = acc[q][j];
+        const uint32_t h01 = pack_bf16x2(a[0], a[1]);
+        const uint32_t h23 = pack_bf16x2(a[2], a[3]);
+        const uint32_t l01 = pack_bf16x2(a[0] - bf16_lo(h01), a[1] - bf16_hi(h01));
+        const uint32_t l23 = pack_bf16x2(a[2] - bf16_lo(h23), a[3] - bf16_hi(h23));
+        char* t = t0 + operand_tile_offset(DK, 0, j, i / 2, lane) + (i & 1) * 8;
+        *reinterpret_cast<uint2*>(t) = make_uint2(h01, h23);
+        *reinterpret_cast<uint2*>(t + (size_t)DK * DK * 2) = make_uint2(l01, l23);
+      }
+    }
+  } else {
+#pragma unroll
+    for (int q = 0; q < RPW; ++q) {
+      const int i = WV + W * q;
+#pragma unroll
+      for (int j = 0; j < NB; ++j)
+        *reinterpret_cast<float4*>(Inv + base + (size_t)(16 * j + li) * DK + 16 * i + 4 * lg) =
+            make_float4(acc[q][j][0], acc[q][j][1], acc[q][j][2], acc[q][j][3]);
+    }
   }
 }
 
@@ -267,8 +290,9 @@ __device__ __forceinline__ void fold_b_partials(float* b0, int splits, size_t b_
 // (any further waves only take part in the barriers); `piv` is
 // 2 * (d_k/16) * 256 floats of LDS.  The matrix is the sum of `splits`
 // partials at A_part + s * part_stride + base; the result goes to Inv + base
-// (which may alias the first partial).
-template <int DK>
+// (which may alias the first partial): an fp32 d_k x d_k matrix, or with
+// TILED the split-bf16 operand tiles of the same size in bytes.
+template <int DK, bool TILED>
 __device__ __forceinline__ void invert_matrix(const float* A_part, int splits, size_t part_stride,
                                               size_t base, float* Inv, float* piv_lds, int tid) {
   constexpr int NB = DK / 16;
@@ -281,10 +305,10 @@ __device__ __forceinline__ void invert_matrix(const float* A_part, int splits, s
     return;
   }
   switch (wave) {
-    case 0: invert_rows<DK, 0>(A_part, splits, part_stride, base, Inv, piv, lane); break;
-    case 1: invert_rows<DK, 1 % W>(A_part, splits, part_stride, base, Inv, piv, lane); break;
-    case 2: invert_rows<DK, 2 % W>(A_part, splits, part_stride, base, Inv, piv, lane); break;
-    default: invert_rows<DK, 3 % W>(A_part, splits, part_stride, base, Inv, piv, lane); break;
+    case 0: invert_rows<DK, 0, TILED>(A_part, splits, part_stride, base, Inv, piv, lane); break;
+    case 1: invert_rows<DK, 1 % W, TILED>(A_part, splits, part_stride, base, Inv, piv, lane); break;
+    case 2: invert_rows<DK, 2 % W, TILED>(A_part, splits, part_stride, base, Inv, piv, lane); break;
+    default: invert_rows<DK, 3 % W, TILED>(A_part, splits, part_stride, base, Inv, piv, lane); break;
   }
 }
 

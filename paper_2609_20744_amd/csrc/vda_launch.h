@@ -30,10 +30,11 @@ hipError_t launch_frame_stats(bool is_f32, const void* k, const void* v, const f
                               int F, int N, int H, int d_k, int d_v, SplitPlan plan,
                               float* A_part, float* B_part, hipStream_t stream);
 
-// Step a2, Eq. 5: Inv = (I + sum of A partials)^{-1}; also folds the B
-// partials of every split frame into its first partial.
+// Step a2, Eq. 5: Inv = (I + sum of A partials)^{-1} (fp32 matrices, or
+// split-bf16 operand tiles when `tiled`); also folds the B partials of every
+// split frame into its first partial.
 hipError_t launch_frame_inverse(const float* A_part, float* B_part, SplitPlan plan,
-                                long long count, int d_k, int d_v, float* Inv,
+                                long long count, int d_k, int d_v, bool tiled, float* Inv,
                                 hipStream_t stream);
 
 // Options of the scans beyond the core (defaults: the core scan).
@@ -50,6 +51,13 @@ struct ScanOptions {
 hipError_t launch_state_scan(bool exact_f32, const float* Mat, const float* Bm, int F, int H,
                              int d_k, int d_v, const ScanOptions& o, float* S_fwd, float* S_rev,
                              hipStream_t stream);
+
+// Steps a3/a4 for the joint rule on the bf16 storage path, with Inv_t given
+// as split-bf16 operand tiles (operand_tile_offset); alpha and the text
+// state of `o` apply, `o.frozen` must be false.
+hipError_t launch_state_scan_tiled(const void* Inv_tiles, const float* Bm, int F, int H, int d_k,
+                                   int d_v, const ScanOptions& o, float* S_fwd, float* S_rev,
+                                   hipStream_t stream);
 
 // Options of the gather beyond the core (defaults: own frame, no decay).
 struct GatherOptions {

@@ -1,0 +1,319 @@
+// Steps a3/a4 on the bf16 storage path for the joint rule: the forward and
+// reverse state scans of Eq. A.1 (Algorithm 1 step 5),
+//     P_t = (P_{t-1} Diag(alpha_t) + B_t) Inv_t,
+//     R_t = (R_{t+1} Diag(alpha_t) + B_t) Inv_t,
+// from S_T / 2 (Eq. 1b) or zero, with alpha = 1 unless a decay is given.
+// The entering state of every frame (P_{t-1} forward, R_{t+1} reverse) is
+// stored for the readout.
+//
+// Work split as in the other scans: one workgroup per (head, direction,
+// 16-row block of the state); the rows of the state evolve independently,
+// and the block stays in LDS across all F frames.  The difference is how
+// Inv_t reaches the matrix cores: the inverse step wrote it as split-bf16
+// operand tiles (operand_tile_offset), in exactly the lane order of the
+// B-operands of v_mfma_f32_16x16x32_bf16.  Each wave loads the tiles of its
+// own 16-column output slices straight into registers, one contiguous 1 KB
+// piece per load instruction, two frames ahead of use.  No LDS image of
+// Inv_t, no per-step split of it and no barrier for it remain on the serial
+// path, which is now the row-wise update (entering state out, decay, B_t in,
+// split into bf16 hi / lo), one barrier, the matrix products and another
+// barrier.
+//
+// Products: the state operand x is split into hi = bf16(x) and
+// lo = bf16(x - hi) once per step, and hi*hi + hi*lo + lo*hi runs on the
+// bf16 matrix cores with fp32 accumulation (about 16 mantissa bits per
+// operand; relative error ~1e-5 per step, which the non-expansive frame maps
+// of Prop. 1 keep from growing along the scan).
+#include "vda_common.h"
+#include "vda_launch.h"
+
+namespace vda {
+namespace {
+
+template <int DK>
+struct TiledDims {
+  static constexpr int NB = DK / 16;           // 16-column output slices
+  static constexpr int NBW = (NB + 3) / 4;     // slices per wave
+  static constexpr int KB = DK / 32;           // 32-wide k steps
+  static constexpr int XLD = DK + 4;           // fp32 state row stride (floats)
+  static constexpr int PLD = DK + 8;           // bf16 plane row stride (elements)
+  static constexpr int VW = DK >= 64 ? 4 : 2;  // floats per access in the row-wise phase
+  static constexpr int NG = DK / (16 * VW);    // accesses per thread in the row-wise phase
+};
+
+// Matrix-core phase of one step for wave W: xs_next = x Inv_t for this
+// wave's output slices nb = W, W + 4, ..., with x from the bf16 hi / lo
+// planes and Inv_t from the register tiles t[m][ks][plane].  Even and odd k
+// steps accumulate separately (two shorter dependency chains).
+template <int DK, int W>
+__device__ __forceinline__ void tiled_mfma_phase(
+    const uint16_t* __restrict__ xhi, const uint16_t* __restrict__ xlo,
+    float* __restrict__ xs_next,
+    const u32x4 (&t)[TiledDims<DK>::NBW][TiledDims<DK>::KB][2], int li, int lg) {
+  using D = TiledDims<DK>;
+  if constexpr (W >= D::NB) {
+    return;  // d_k = 32: two slices, waves 2 and 3 idle
+  } else {
+    // A-operand: row li of the block at k = 32 ks + 4 lg + e, 32 ks + 16 + 4 lg + e.
+    bf16x8 ahi[D::KB], alo[D::KB];
+#pragma unroll
+    for (int ks = 0; ks < D::KB; ++ks) {
+      const int o = li * D::PLD + 32 * ks + 4 * lg;
+      const u32x2 h0 = *reinterpret_cast<const u32x2*>(&xhi[o]);
+      const u32x2 h1 = *reinterpret_cast<const u32x2*>(&xhi[o + 16]);
+      const u32x2 l0 = *reinterpret_cast<const u32x2*>(&xlo[o]);
+      const u32x2 l1 = *reinterpret_cast<const u32x2*>(&xlo[o + 16]);
+      ahi[ks] = __builtin_bit_cast(bf16x8, u32x4{h0[0], h0[1], h1[0], h1[1]});
+      alo[ks] = __builtin_bit_cast(bf16x8, u32x4{l0[0], l0[1], l1[0], l1[1]});
+    }
+#pragma unroll
+    for (int m = 0; m < D::NBW; ++m) {
+      const int nb = W + 4 * m;
+      if (nb < D::NB) {
+        floatx4 acc[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
+#pragma unroll
+        for (int ks = 0; ks < D::KB; ++ks) {
+          const bf16x8 bhi = __builtin_bit_cast(bf16x8, t[m][ks][0]);
+          const bf16x8 blo = __builtin_bit_cast(bf16x8, t[m][ks][1]);
+          floatx4& a = acc[ks & 1];
+          a = __builtin_amdgcn_mfma_f32_16x16x32_bf16(alo[ks], bhi, a, 0, 0, 0);
+          a = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi[ks], blo, a, 0, 0, 0);
+          a = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi[ks], bhi, a, 0, 0, 0);
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          xs_next[(lg * 4 + i) * D::XLD + nb * 16 + li] = acc[0][i] + acc[1][i];
+      }
+    }
+  }
+}
+
+template <int DK, bool DECAY>
+__global__ __launch_bounds__(kThreads)
+void scan_tiled_kernel(const uint16_t* __restrict__ Invt, const float* __restrict__ Bm,
+                       const float* __restrict__ alpha, const float* __restrict__ text_state,
+                       int F, int DV, unsigned nwg, float* __restrict__ S_fwd,
+                       float* __restrict__ S_rev) {
+  using D = TiledDims<DK>;
+  constexpr int XLD = D::XLD, PLD = D::PLD, VW = D::VW, NG = D::NG;
+  constexpr int NBW = D::NBW, KB = D::KB;
+  __shared__ __align__(16) float xs[2][16 * XLD];
+  __shared__ __align__(16) uint16_t xsp[2][16 * PLD];   // bf16 hi / lo planes of the block
+  __shared__ __align__(16) float alds[DECAY ? DK : 4];  // alpha of the coming step
+
+  const int nrb = DV / 16;
+  const unsigned L = xcd_grouped_id(blockIdx.x, nwg);
+  const int rb = L % nrb;
+  const unsigned chain = L / nrb;
+  const int dir = chain & 1;
+  const unsigned hb = chain >> 1;
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (scalar)
+  const int li = lane & 15;
+  const int lg = lane >> 4;
+
+  // Row-wise phase role: row pr of the block; access g covers columns
+  // pc + g * 16 * VW .. + VW - 1 (16 consecutive lanes on one contiguous run).
+  const int pr = tid >> 4;
+  const int pc = (tid & 15) * VW;
+
+  const size_t mat_b = (size_t)DV * DK;  // one B / state matrix
+  // Initial state: S_T / 2 (rows of this block), or zero.
+  for (int i = tid; i < 16 * XLD; i += kThreads) {
+    const int r = i / XLD, c = i % XLD;
+    xs[0][i] = text_state != nullptr && c < DK
+                   ? 0.5f * text_state[(size_t)hb * mat_b + (size_t)(rb * 16 + r) * DK + c]
+                   : 0.f;
+  }
+
+  float* Sout = dir == 0 ? S_fwd : S_rev;
+  const size_t row_off = (size_t)(rb * 16 + pr) * DK + pc;
+  // Entering states of this head, [F][d_v][d_k]: a range-checked buffer, so
+  // the padded step past the last frame stores nothing.
+  const __amdgpu_buffer_rsrc_t srsrc =
+      make_rsrc(Sout + (size_t)hb * F * mat_b, (uint32_t)(F * mat_b * sizeof(float)));
+  // B of this head, range-checked (frames outside [0, F) read as zero).
+  const __amdgpu_buffer_rsrc_t brsrc =
+      make_rsrc(Bm + (size_t)hb * F * mat_b, (uint32_t)(F * mat_b * sizeof(float)));
+  const __amdgpu_buffer_rsrc_t arsrc =
+      make_rsrc(DECAY ? alpha + (size_t)hb * F * DK : Bm, DECAY ? (uint32_t)(F * DK * 4) : 0u);
+  // Operand tiles of this head's frames, [F][d_k * d_k * 4 bytes].
+  const __amdgpu_buffer_rsrc_t trsrc =
+      make_rsrc(Invt + (size_t)hb * F * (DK * DK * 2), (uint32_t)F * (uint32_t)(DK * DK * 4));
+
+  // This wave's tile offsets within a frame (out of range for the slices of
+  // idle waves at d_k = 32).
+  uint32_t toff[NBW][KB][2];
+#pragma unroll
+  for (int m = 0; m < NBW; ++m) {
+    const int nb = wave + 4 * m;
+#pragma unroll
+    for (int ks = 0; ks < KB; ++ks)
+#pragma unroll
+      for (int p = 0; p < 2; ++p)
+        toff[m][ks][p] = nb < D::NB ? operand_tile_offset(DK, p, nb, ks, lane) : kOutOfRange;
+  }
+
+  auto frame_of = [&](int step) { return dir == 0 ? step : F - 1 - step; };
+
+  // Two-frame register ring, as separately named arrays (compile-time
+  // indices only).
+  u32x4 t0[NBW][KB][2], t1[NBW][KB][2];
+  float bs0[NG][VW], bs1[NG][VW];
+  u32x4 al0, al1;  // alpha_t, columns 4 tid .. 4 tid + 3 (threads tid < DK / 4)
+  auto load_step = [&](int step, u32x4 (&t)[NBW][KB][2], float (&bb)[NG][VW], u32x4& al) {
+    const int frame = frame_of(step);
+    // B rows first (they are needed earlier in the step than the tiles),
+    // and everything through buffer loads, which the compiler keeps in
+    // program order.
+#pragma unroll
+    for (int g = 0; g < NG; ++g) {
+      const uint32_t off = (uint32_t)(((size_t)frame * mat_b + row_off + g * 16 * VW) * 4u);
+      if constexpr (VW == 4) {
+        const u32x4 x =
+            __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(brsrc, (int)off, 0, 0));
+#pragma unroll
+        for (int v = 0; v < 4; ++v) bb[g][v] = __uint_as_float(x[v]);
+      } else {
+        const u32x2 x =
+            __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(brsrc, (int)off, 0, 0));
+        bb[g][0] = __uint_as_float(x[0]);
+        bb[g][1] = __uint_as_float(x[1]);
+      }
+    }
+    if constexpr (DECAY) {
+      const uint32_t off = tid < DK / 4 ? (uint32_t)(frame * DK + 4 * tid) * 4u : kOutOfRange;
+      al = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(arsrc, (int)off, 0, 0));
+    }
+    const uint32_t fbase = (uint32_t)frame * (uint32_t)(DK * DK * 4);
+#pragma unroll
+    for (int m = 0; m < NBW; ++m)
+#pragma unroll
+      for (int ks = 0; ks < KB; ++ks)
+#pragma unroll
+        for (int p = 0; p < 2; ++p) {
+          const uint32_t o = toff[m][ks][p];
+          t[m][ks][p] = __builtin_bit_cast(
+              u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                         trsrc, (int)(o == kOutOfRange ? kOutOfRange : fbase + o), 0, 0));
+        }
+  };
+
+  int cur = 0;
+  auto step_body = [&](int step, u32x4 (&t)[NBW][KB][2], float (&bb)[NG][VW], u32x4& al,
+                       const u32x4& al_next) {
+    // Frame index within the head; past the end it is out of the buffer
+    // range (>= F forward, negative and so huge as unsigned in reverse).
+    const int frame = dir == 0 ? step : F - 1 - step;
+    lds_barrier();  // xs[cur] holds the entering state; last step's plane reads are done
+    {
+      const uint32_t off = (uint32_t)((size_t)(unsigned)frame * mat_b + row_off) * 4u;
+#pragma unroll
+      for (int g = 0; g < NG; ++g) {
+        const int xo = pr * XLD + pc + g * 16 * VW;
+        float v[VW];
+        if constexpr (VW == 4) {
+          const floatx4 xv = reinterpret_cast<const floatx4*>(xs[cur])[xo / 4];
+#pragma unroll
+          for (int c = 0; c < 4; ++c) v[c] = xv[c];
+          store_b128(srsrc, off + g * 64u * VW,
+                     u32x4{__float_as_uint(v[0]), __float_as_uint(v[1]), __float_as_uint(v[2]),
+                           __float_as_uint(v[3])});
+        } else {
+          const float2 xv = *reinterpret_cast<const float2*>(&xs[cur][xo]);
+          v[0] = xv.x;
+          v[1] = xv.y;
+          store_b64(srsrc, off + g * 64u * VW, make_uint2(__float_as_uint(v[0]), __float_as_uint(v[1])));
+        }
+        if constexpr (DECAY) {
+#pragma unroll
+          for (int c = 0; c < VW; ++c) v[c] *= alds[pc + g * 16 * VW + c];
+        }
+#pragma unroll
+        for (int c = 0; c < VW; ++c) v[c] += bb[g][c];
+        // The product's A-operand, split once here into bf16 hi and lo.
+        uint32_t hw[VW / 2], lw[VW / 2];
+#pragma unroll
+        for (int c = 0; c < VW; c += 2) {
+          const uint32_t h = pack_bf16x2(v[c], v[c + 1]);
+          hw[c / 2] = h;
+          lw[c / 2] = pack_bf16x2(v[c] - bf16_lo(h), v[c + 1] - bf16_hi(h));
+        }
+        const int po = pr * PLD + pc + g * 16 * VW;
+        if constexpr (VW == 4) {
+          *reinterpret_cast<u32x2*>(&xsp[0][po]) = u32x2{hw[0], hw[1]};
+          *reinterpret_cast<u32x2*>(&xsp[1][po]) = u32x2{lw[0], lw[1]};
+        } else {
+          *reinterpret_cast<uint32_t*>(&xsp[0][po]) = hw[0];
+          *reinterpret_cast<uint32_t*>(&xsp[1][po]) = lw[0];
+        }
+      }
+    }
+    lds_barrier();
+    // alpha of the next step, read by its row-wise phase (after the next
+    // barrier); this step's reads of alds are complete.
+    if constexpr (DECAY) {
+      if (tid < DK / 4) reinterpret_cast<u32x4*>(alds)[tid] = al_next;
+    }
+    switch (wave) {  // wave-uniform
+      case 0: tiled_mfma_phase<DK, 0>(xsp[0], xsp[1], xs[cur ^ 1], t, li, lg); break;
+      case 1: tiled_mfma_phase<DK, 1>(xsp[0], xsp[1], xs[cur ^ 1], t, li, lg); break;
+      case 2: tiled_mfma_phase<DK, 2>(xsp[0], xsp[1], xs[cur ^ 1], t, li, lg); break;
+      default: tiled_mfma_phase<DK, 3>(xsp[0], xsp[1], xs[cur ^ 1], t, li, lg); break;
+    }
+    // Refill this slot with the frame two steps on, once its tiles are
+    // consumed (past the end: a clamped, unused frame), always, so no branch
+    // hides the loads from the wait-count bookkeeping.
+    load_step(min(step + 2, F - 1), t, bb, al);
+    cur ^= 1;
+  };
+
+  // Issue the ring in slot order (pinned against rescheduling) so slot 0 is
+  // the oldest load on loop entry.
+  load_step(0, t0, bs0, al0);
+  __builtin_amdgcn_sched_barrier(0);
+  load_step(min(1, F - 1), t1, bs1, al1);
+  __builtin_amdgcn_sched_barrier(0);
+  if constexpr (DECAY) {  // alpha of step 0
+    if (tid < DK / 4) reinterpret_cast<u32x4*>(alds)[tid] = al0;
+  }
+  // The step count is padded to an even number; a padded step (step >= F)
+  // reads a clamped frame and its stores are dropped, so the loop body has
+  // no early exit.
+  for (int step0 = 0; step0 < F; step0 += 2) {
+    step_body(step0, t0, bs0, al0, al1);
+    step_body(step0 + 1, t1, bs1, al1, al0);
+  }
+}
+
+template <int DK>
+hipError_t launch_tiled_t(const void* Invt, const float* Bm, int F, int H, int d_v,
+                          const ScanOptions& o, float* S_fwd, float* S_rev, hipStream_t stream) {
+  const unsigned nwg = (unsigned)H * 2u * (unsigned)(d_v / 16);
+  const uint16_t* t = static_cast<const uint16_t*>(Invt);
+  if (o.alpha != nullptr)
+    hipLaunchKernelGGL((scan_tiled_kernel<DK, true>), dim3(nwg), dim3(kThreads), 0, stream, t, Bm,
+                       o.alpha, o.text_state, F, d_v, nwg, S_fwd, S_rev);
+  else
+    hipLaunchKernelGGL((scan_tiled_kernel<DK, false>), dim3(nwg), dim3(kThreads), 0, stream, t, Bm,
+                       o.alpha, o.text_state, F, d_v, nwg, S_fwd, S_rev);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_state_scan_tiled(const void* Inv_tiles, const float* Bm, int F, int H, int d_k,
+                                   int d_v, const ScanOptions& o, float* S_fwd, float* S_rev,
+                                   hipStream_t stream) {
+  if (o.frozen) return hipErrorInvalidValue;
+  switch (d_k) {
+    case 32: return launch_tiled_t<32>(Inv_tiles, Bm, F, H, d_v, o, S_fwd, S_rev, stream);
+    case 64: return launch_tiled_t<64>(Inv_tiles, Bm, F, H, d_v, o, S_fwd, S_rev, stream);
+    case 128: return launch_tiled_t<128>(Inv_tiles, Bm, F, H, d_v, o, S_fwd, S_rev, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace vda

@@ -53,7 +53,9 @@ _SIGNATURES = {
     "vda_default_split_plan": (_I, [_I, _I, _I, _I, _I, _I, _P, _P]),
     "vda_frame_stats": (_I, [_P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _P, _P, _P]),
     "vda_frame_inverse": (_I, [_P, _P, _I, _I, _I, _I, _I, _P, _P]),
+    "vda_frame_inverse_tiles": (_I, [_P, _P, _I, _I, _I, _I, _I, _P, _P]),
     "vda_state_scan": (_I, [_P, _P, _I, _I, _I, _I, _I, _P, _P, _P]),
+    "vda_state_scan_tiles": (_I, [_P, _P, _I, _I, _I, _I, _P, _P, _P]),
     "vda_readout": (_I, [_P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _P, _P]),
 }
 
@@ -261,12 +263,15 @@ def frame_stats(k, v, beta, splits=None, tail_frames=None, A_part=None, B_part=N
 
 
 def frame_inverse(A_part, B_part=None, count=None, tail_frames=0, splits=1, Inv=None,
-                  stream=None):
+                  stream=None, tiles=False):
     """Step a2 (vda_frame_inverse): Inv [count, d_k, d_k] = (I + sum of each
     frame's A partials)^-1, fp32, under the split plan that made the partials
     (A_part [P, d_k, d_k]; count defaults to P when splits == 1).  With
     splits > 1 each frame's B partials ([P, d_v, d_k]) are folded in place into
-    B_part[frame]."""
+    B_part[frame].  tiles=True (vda_frame_inverse_tiles) writes each inverse
+    as split-bf16 operand tiles instead: Inv is then [count, 2, d_k * d_k]
+    bfloat16 (hi plane, lo plane; the layout of include/vda.h), or any
+    buffer of the same size in bytes."""
     torch = _torch()
     d_k = A_part.shape[-1]
     if count is None:
@@ -277,13 +282,15 @@ def frame_inverse(A_part, B_part=None, count=None, tail_frames=0, splits=1, Inv=
     if splits > 1 and B_part is None:
         raise ValueError("B_part is required when there is more than one split")
     if Inv is None:
-        Inv = torch.empty((count, d_k, d_k), dtype=torch.float32, device=A_part.device)
+        Inv = (torch.empty((count, 2, d_k * d_k), dtype=torch.bfloat16, device=A_part.device)
+               if tiles else
+               torch.empty((count, d_k, d_k), dtype=torch.float32, device=A_part.device))
+    fn = lib.vda_frame_inverse_tiles if tiles else lib.vda_frame_inverse
     with torch.cuda.device(A_part.device):
-        st = lib.vda_frame_inverse(A_part.data_ptr(),
-                                   B_part.data_ptr() if B_part is not None else None,
-                                   int(tail_frames), int(splits), int(count), d_k, d_v,
-                                   Inv.data_ptr(), _stream_ptr(A_part.device, stream))
-    _check(st, "vda_frame_inverse")
+        st = fn(A_part.data_ptr(), B_part.data_ptr() if B_part is not None else None,
+                int(tail_frames), int(splits), int(count), d_k, d_v, Inv.data_ptr(),
+                _stream_ptr(A_part.device, stream))
+    _check(st, fn.__name__)
     return Inv
 
 
@@ -304,6 +311,27 @@ def state_scan(Inv, B, S_fwd=None, S_rev=None, exact_f32=False, stream=None):
                                 int(bool(exact_f32)), S_fwd.data_ptr(), S_rev.data_ptr(),
                                 _stream_ptr(dev, stream))
     _check(st, "vda_state_scan")
+    return S_fwd, S_rev
+
+
+def state_scan_tiles(Inv_tiles, B, S_fwd=None, S_rev=None, stream=None):
+    """Steps a3/a4 from split-bf16 operand tiles (vda_state_scan_tiles), the
+    kernel vda_forward runs with bf16 storage.  Inv_tiles: [H, F, ...] with
+    d_k * d_k * 4 bytes per frame (as written by frame_inverse(tiles=True));
+    B [H, F, d_v, d_k] fp32."""
+    torch = _torch()
+    H, F, d_v, d_k = B.shape
+    dev = B.device
+    if Inv_tiles.numel() * Inv_tiles.element_size() != H * F * d_k * d_k * 4:
+        raise ValueError("Inv_tiles must hold d_k * d_k * 4 bytes per frame")
+    if S_fwd is None:
+        S_fwd = torch.empty((H, F, d_v, d_k), dtype=torch.float32, device=dev)
+    if S_rev is None:
+        S_rev = torch.empty((H, F, d_v, d_k), dtype=torch.float32, device=dev)
+    with torch.cuda.device(dev):
+        st = lib.vda_state_scan_tiles(Inv_tiles.data_ptr(), B.data_ptr(), F, H, d_k, d_v,
+                                      S_fwd.data_ptr(), S_rev.data_ptr(), _stream_ptr(dev, stream))
+    _check(st, "vda_state_scan_tiles")
     return S_fwd, S_rev
 
 

@@ -12,8 +12,9 @@ import pytest
 
 import oracle.vda_oracle as O
 from paper_2609_20744_amd import inputs as I
-from vda_testutil import (TOL_BF16, TOL_F32, device_inputs, from_device, oracle_inputs,
-                          oracle_sampled, rel_max_err, sample_positions, to_device, tol_for)
+from vda_testutil import (TOL_BF16, TOL_F32, device_inputs, from_device, from_operand_tiles,
+                          oracle_inputs, oracle_sampled, rel_max_err, sample_positions, to_device,
+                          to_operand_tiles, tol_for)
 
 pytestmark = pytest.mark.gpu
 
@@ -115,6 +116,22 @@ def test_inverse_stage(V, dk):
         for i in range(count):
             cond = np.linalg.cond(np.eye(dk) + A[i])
             assert rel_max_err(got[i], expect[i]) < 2e-6 * cond, (i, cond)
+        # The same inverse as split-bf16 operand tiles: element [k][n] of the
+        # tiles is the computed inverse, whose fp32 form is stored transposed
+        # (the two agree up to the inverse's rounding asymmetry), split into
+        # bf16 hi + lo exactly as torch's RNE casts do on the CPU.
+        A_dev = to_device(parts, "f32")
+        B_dev = to_device(Bp, "f32")
+        T = V.frame_inverse(A_dev, B_dev, count=count, tail_frames=tail, splits=splits,
+                            tiles=True)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(B_dev[:count].cpu().numpy(), Bsum)
+        T_exp = to_operand_tiles(np.swapaxes(Inv.cpu().numpy(), -1, -2))
+        assert torch.equal(T.cpu().view(torch.int16), T_exp.view(torch.int16))
+        gt = from_operand_tiles(T, dk)
+        for i in range(count):
+            cond = np.linalg.cond(np.eye(dk) + A[i])
+            assert rel_max_err(gt[i], expect[i]) < 2e-6 * cond + 2e-5, (i, cond)
     # in place onto the partial buffer
     A_dev = to_device(A[None].astype(np.float32), "f32")
     V.frame_inverse(A_dev, Inv=A_dev[0])
@@ -153,6 +170,14 @@ def test_scan_stage(V, dk, dv):
         _log(f"  exact_f32={exact}: fwd {ef:.2e} rev {er:.2e}")
         assert ef < tol and er < tol
         assert np.all(Sf[:, 0].cpu().numpy() == 0) and np.all(Sr[:, -1].cpu().numpy() == 0)
+    # The scan vda_forward runs with bf16 storage: Inv_t as split-bf16 tiles.
+    Sf, Sr = V.state_scan_tiles(to_operand_tiles(Inv).cuda(), to_device(Bm.astype(np.float32), "f32"))
+    torch.cuda.synchronize()
+    ef = rel_max_err(Sf.double().cpu().numpy(), P_exp)
+    er = rel_max_err(Sr.double().cpu().numpy(), R_exp)
+    _log(f"  tiles: fwd {ef:.2e} rev {er:.2e}")
+    assert ef < 1e-4 and er < 1e-4
+    assert np.all(Sf[:, 0].cpu().numpy() == 0) and np.all(Sr[:, -1].cpu().numpy() == 0)
 
 
 @pytest.mark.parametrize("dk,dv", [(64, 128), (128, 128)])
@@ -177,14 +202,19 @@ def test_scan_many_workgroups_per_cu(V, dk, dv):
     for t in range(F - 2, -1, -1):
         R_exp[:, t] = (R_exp[:, t + 1] + B64[:, t + 1]) @ I64[:, t + 1]
     Id, Bd = to_device(Inv, "f32"), to_device(Bm, "f32")
-    for exact, tol in ((True, 1e-5), (False, 1e-4)):
-        Sf, Sr = V.state_scan(Id, Bd, exact_f32=exact)
-        Sf2, Sr2 = V.state_scan(Id, Bd, exact_f32=exact)
+    Td = to_operand_tiles(Inv).cuda()
+    for kind, tol in (("exact_f32", 1e-5), ("split", 1e-4), ("tiles", 1e-4)):
+        if kind == "tiles":
+            Sf, Sr = V.state_scan_tiles(Td, Bd)
+            Sf2, Sr2 = V.state_scan_tiles(Td, Bd)
+        else:
+            Sf, Sr = V.state_scan(Id, Bd, exact_f32=kind == "exact_f32")
+            Sf2, Sr2 = V.state_scan(Id, Bd, exact_f32=kind == "exact_f32")
         torch.cuda.synchronize()
         assert torch.equal(Sf, Sf2) and torch.equal(Sr, Sr2)
         ef = rel_max_err(Sf.double().cpu().numpy(), P_exp)
         er = rel_max_err(Sr.double().cpu().numpy(), R_exp)
-        _log(f"  exact_f32={exact}: fwd {ef:.2e} rev {er:.2e}")
+        _log(f"  {kind}: fwd {ef:.2e} rev {er:.2e}")
         assert ef < tol and er < tol
 
 
@@ -361,10 +391,14 @@ def _staged_forward(V, d, exact_f32):
     tail, splits = V.default_split_plan(F, N, H, d_k, d_v, exact_f32)
     A_part, B_part = V.frame_stats(d["k"], d["v"], d["beta"], splits=splits, tail_frames=tail)
     count = H * F
+    # With bf16 storage the inverse goes to the scan as split-bf16 tiles.
     Inv = V.frame_inverse(A_part, B_part, count=count, tail_frames=tail, splits=splits,
-                          Inv=A_part[:count])
-    Sf, Sr = V.state_scan(Inv.view(H, F, d_k, d_k), B_part[:count].view(H, F, d_v, d_k),
-                          exact_f32=exact_f32)
+                          Inv=A_part[:count], tiles=not exact_f32)
+    if exact_f32:
+        Sf, Sr = V.state_scan(Inv.view(H, F, d_k, d_k), B_part[:count].view(H, F, d_v, d_k),
+                              exact_f32=True)
+    else:
+        Sf, Sr = V.state_scan_tiles(Inv.view(H, F, d_k * d_k), B_part[:count].view(H, F, d_v, d_k))
     return V.readout(d["q"], Sf, Sr, d["gate"]), splits
 
 

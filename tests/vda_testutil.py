@@ -70,3 +70,39 @@ def oracle_sampled(w, xo: dict, h_local: int, toks) -> tuple[np.ndarray, np.ndar
     y = O.head_forward_sampled(xo["q"][h_local], xo["k"][h_local], xo["v"][h_local],
                                xo["beta"][h_local], float(xo["gate"][h_local]), frames, tk)
     return y, frames, tk
+
+
+def operand_tile_index(dk: int):
+    """(k, n) of every bf16 position of one plane of the split-bf16 operand
+    tile layout (include/vda.h): plane position i holds element [k[i]][n[i]]."""
+    NB, KB = dk // 16, dk // 32
+    nb, ks, lane, e = np.meshgrid(np.arange(NB), np.arange(KB), np.arange(64), np.arange(8),
+                                  indexing="ij")
+    k = 32 * ks + 4 * (lane // 16) + np.where(e < 4, e, 12 + e)
+    n = 16 * nb + lane % 16
+    return k.ravel(), n.ravel()
+
+
+def to_operand_tiles(X: np.ndarray):
+    """fp32 matrices [..., d_k, d_k] -> torch bfloat16 [..., 2, d_k*d_k] in
+    the tile layout: plane 0 = bf16(x), plane 1 = bf16(x - hi) (torch's
+    round-to-nearest-even casts, on the CPU)."""
+    import torch
+    dk = X.shape[-1]
+    k, n = operand_tile_index(dk)
+    vals = torch.from_numpy(np.ascontiguousarray(X[..., k, n], dtype=np.float32))
+    hi = vals.to(torch.bfloat16)
+    lo = (vals - hi.float()).to(torch.bfloat16)
+    return torch.stack([hi, lo], dim=-2).contiguous()
+
+
+def from_operand_tiles(T, dk: int) -> np.ndarray:
+    """Tile layout [..., 2, d_k*d_k] (torch bfloat16, any device) -> float64
+    matrices hi + lo [..., d_k, d_k]."""
+    import torch
+    t = T.cpu().to(torch.float64).numpy()
+    vals = t[..., 0, :] + t[..., 1, :]
+    k, n = operand_tile_index(dk)
+    X = np.zeros(t.shape[:-2] + (dk, dk))
+    X[..., k, n] = vals
+    return X
