@@ -25,6 +25,11 @@ with no blocking, fusion or reordering beyond what the equations state:
       y = g * RMSNorm(o),  RMSNorm(o) = o / sqrt(mean_j o_j^2 + eps),
   over the d_v channels of one token of one head, no learnable weight.
 
+The chunk-wise scans (chunk_map, chunk_boundary_states) compose each chunk
+of the window grid into one affine map of Eq. A.1 and scan the chunk
+sequence (Section 4); they give the states at chunk boundaries, which equal
+the frame-by-frame scans' states there.
+
 The full gather (the *_ex functions at the end) adds what the core leaves
 at its special values: the channel-wise decay alpha_t (S_bar_t =
 S_{t-1} Diag(alpha_t), Eq. 3a/5 and A.1), the text state S_T starting both
@@ -365,3 +370,60 @@ def vda_forward_ex(q, k, v, beta, gate, alpha=None, S_T=None, chunk=1, radius=0,
                         None if alpha is None else alpha[h],
                         None if S_T is None else S_T[h], windows, rule, eps)
         for h in range(H)])
+
+
+# ----------------------------------------------------------------------------
+# Chunk-wise scans (Section 4): each chunk of frames composed into one affine
+# map (Eq. A.1), then the chunk sequence scanned in both directions
+# ----------------------------------------------------------------------------
+
+def chunk_ranges(F: int, chunk: int, offset: int = 0):
+    """The chunks of the local-window grid (Section 2.1, as in local_windows):
+    `chunk` consecutive frames counted from `offset` positions before array
+    frame 0, clipped to the clip.  Returns (first, last) array frame indices
+    (inclusive) of every non-empty chunk, in frame order."""
+    out = []
+    c = 0
+    while c * chunk - offset <= F - 1:
+        lo = max(0, c * chunk - offset)
+        hi = min(F - 1, (c + 1) * chunk - offset - 1)
+        if hi >= lo:
+            out.append((lo, hi))
+        c += 1
+    return out
+
+
+def chunk_map(As, Bs, frames, alphas=None):
+    """Eq. A.1 composed over array frames `frames`, applied in the order
+    given (the scan order): the map S_in -> S_out of the joint rule is
+    S_out = S_in M + J with, frame by frame, M <- M M_t and J <- J M_t + J_t
+    (M_t = Diag(alpha_t)(I + A_t)^{-1}, J_t = B_t (I + A_t)^{-1})."""
+    d_k, d_v = As.shape[1], Bs.shape[1]
+    M = np.eye(d_k)
+    J = np.zeros((d_v, d_k))
+    for t in frames:
+        Mt, Jt = frame_transition(As[t], Bs[t], None if alphas is None else alphas[t])
+        M = M @ Mt
+        J = J @ Mt + Jt
+    return M, J
+
+
+def chunk_boundary_states(As, Bs, S0, chunk: int, offset: int = 0, alphas=None):
+    """Both scans over the chunk sequence (joint rule), from S0 each.
+    Returns (Pb, Rb), one entry per chunk of chunk_ranges: Pb[c] is the
+    forward state entering chunk c (after every earlier frame), Rb[c] the
+    reverse state entering it from the right (after every later frame)."""
+    ranges = chunk_ranges(Bs.shape[0], chunk, offset)
+    Pb, Rb = [], [None] * len(ranges)
+    P = np.array(S0, dtype=np.float64)
+    for lo, hi in ranges:
+        Pb.append(P)
+        M, J = chunk_map(As, Bs, range(lo, hi + 1), alphas)
+        P = P @ M + J
+    R = np.array(S0, dtype=np.float64)
+    for c in range(len(ranges) - 1, -1, -1):
+        lo, hi = ranges[c]
+        Rb[c] = R
+        M, J = chunk_map(As, Bs, range(hi, lo - 1, -1), alphas)
+        R = R @ M + J
+    return Pb, Rb

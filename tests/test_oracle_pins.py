@@ -557,6 +557,46 @@ def pin_local_windows_paper_layout():
     assert O.local_windows(4, 1, 0, 0) == [(1, 1), (2, 2), (3, 3), (4, 4)]
 
 
+def pin_chunk_ranges_tile_the_window_grid():
+    """Section 2.1 / Section 4: the chunks of the window grid, clipped to the
+    clip, cover every frame once, in order, and two frames share a chunk
+    exactly when they share a radius-0 window.  Hand-derived layout: 12
+    frames in chunks of 5 after one leading anchor are frames 0-3, 4-8 and
+    9-11 (array numbering)."""
+    assert O.chunk_ranges(12, 5, 1) == [(0, 3), (4, 8), (9, 11)]
+    assert O.chunk_ranges(10, 5, 0) == [(0, 4), (5, 9)]
+    assert O.chunk_ranges(3, 5, 4) == [(0, 0), (1, 2)]
+    assert O.chunk_ranges(4, 1, 0) == [(0, 0), (1, 1), (2, 2), (3, 3)]
+    for F, chunk, offset in ((1, 3, 0), (7, 3, 2), (36, 5, 1), (40, 5, 0), (13, 4, 3)):
+        ranges = O.chunk_ranges(F, chunk, offset)
+        frames = [t for lo, hi in ranges for t in range(lo, hi + 1)]
+        assert frames == list(range(F))
+        assert all(hi - lo + 1 <= chunk for lo, hi in ranges)
+        own = O.local_windows(F, chunk, 0, offset)      # paper numbering
+        for lo, hi in ranges:
+            for t in range(lo, hi + 1):
+                assert own[t] == (lo + 1, hi + 1)
+
+
+def pin_chunk_scan_matches_frame_scan():
+    """Section 4, chunk-wise scans: composing each chunk into S_out = S_in M
+    + J (Eq. A.1) and scanning the chunk sequence gives, at every chunk
+    boundary and in both directions, the states of the frame-by-frame scans
+    (with decay and a text state)."""
+    rng = _rng(31)
+    q, k, v, beta = _random_clip(rng, F=11, N=5, d_k=4, d_v=3)
+    As, Bs = O.head_statistics(k, v, beta)
+    alphas = _random_alpha(rng, 11, 4)
+    S0 = 0.5 * rng.standard_normal((3, 4))
+    P = O.forward_states_ex(As, Bs, S0, alphas)
+    R = O.reverse_states_ex(As, Bs, S0, alphas)
+    for chunk, offset in ((5, 1), (3, 0), (4, 2), (11, 0), (1, 0)):
+        Pb, Rb = O.chunk_boundary_states(As, Bs, S0, chunk, offset, alphas)
+        for c, (lo, hi) in enumerate(O.chunk_ranges(11, chunk, offset)):
+            np.testing.assert_allclose(Pb[c], P[lo], rtol=1e-11, atol=1e-12)
+            np.testing.assert_allclose(Rb[c], R[hi + 2], rtol=1e-11, atol=1e-12)
+
+
 PINS = [f for name, f in sorted(globals().items()) if name.startswith("pin_")]
 
 
@@ -677,8 +717,23 @@ def _mut_windows_ignore_offset(F, chunk=1, radius=0, offset=0):
     return _ORIG_WINDOWS(F, chunk, radius, 0)
 
 
+def _mut_chunk_map_wrong_order(As, Bs, frames, alphas=None):
+    d_k, d_v = As.shape[1], Bs.shape[1]
+    M, J = np.eye(d_k), np.zeros((d_v, d_k))
+    for t in frames:
+        Mt, Jt = O.frame_transition(As[t], Bs[t], None if alphas is None else alphas[t])
+        M = Mt @ M
+        J = J @ Mt + Jt
+    return M, J
+
+
+def _mut_chunk_ranges_unclipped(F, chunk, offset=0):
+    return [(lo, min(F - 1, lo + chunk - 1)) for lo, _ in _ORIG_CHUNK_RANGES(F, chunk, offset)]
+
+
 _ORIG_GATHER_EX = O.gathered_states_ex
 _ORIG_WINDOWS = O.local_windows
+_ORIG_CHUNK_RANGES = O.chunk_ranges
 
 MUTANTS = [
     ("decayed_frame_update", _mut_decay_after_update),
@@ -686,6 +741,8 @@ MUTANTS = [
     ("gathered_states_ex", _mut_bridge_skips_own_decay),
     ("gathered_states_ex", _mut_text_state_not_halved),
     ("local_windows", _mut_windows_ignore_offset),
+    ("chunk_map", _mut_chunk_map_wrong_order),
+    ("chunk_ranges", _mut_chunk_ranges_unclipped),
     ("frame_statistics", _mut_stats_no_beta),
     ("frame_statistics", _mut_stats_beta_squared),
     ("joint_frame_update", _mut_update_no_identity),
