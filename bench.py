@@ -145,6 +145,39 @@ def pmc_summary(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, copy_gib, 
             "write_factor": f_write, "kernels": kernels}
 
 
+def scan_paths(vda, torch, H, F, dk, dv, chunk, offset, K):
+    """Time the frame-by-frame and the chunk-wise scans of one shape on
+    synthetic inverses (I + G G^T / d_k)^{-1}, written as operand tiles by the
+    library's inverse, and random B."""
+    g = torch.Generator(device="cuda").manual_seed(11)
+    G = torch.randn((H * F, dk, dk), device="cuda", generator=g) / dk ** 0.5
+    A = torch.bmm(G, G.transpose(1, 2).contiguous())
+    T = vda.frame_inverse(A, tiles=True).view(H, F, -1)
+    B = torch.randn((H, F, dv, dk), device="cuda", generator=g)
+    Sf = torch.zeros((H, F, dv, dk), device="cuda")
+    Sr = torch.zeros_like(Sf)
+    work = torch.empty((vda.chunked_workspace(F, H, dk, dv, chunk, offset),), dtype=torch.uint8,
+                       device="cuda")
+    runs = {"frame_scan_ms": lambda: vda.state_scan_tiles(T, B, Sf, Sr),
+            "chunk_scan_ms": lambda: vda.state_scan_chunked(T, B, chunk, offset, S_fwd=Sf,
+                                                            S_rev=Sr, work=work)}
+    out = {"heads": H, "frames": F, "d_k": dk, "d_v": dv, "chunk": chunk, "offset": offset}
+    for name, fn in runs.items():
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(K):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        out[name] = e0.elapsed_time(e1) / K
+    print(f"[bench] scans H={H} F={F}: frame by frame {out['frame_scan_ms']:.4f} ms, "
+          f"chunk-wise {out['chunk_scan_ms']:.4f} ms", file=sys.stderr, flush=True)
+    return out
+
+
 def cpu_baseline(w, budget_s: float = 20.0) -> dict:
     """Time the fp64 oracle on whole heads of the same workload until about
     budget_s of CPU work, and scale to the full job's tokens/s."""
@@ -390,6 +423,12 @@ def main() -> int:
         print(f"[bench] vda_forward_ex ({rule}, all options): {ms_ex:.4f} ms/step",
               file=sys.stderr, flush=True)
     result["full_operator"] = full
+    # 4. The two scan paths of a chunked window, alone: frame by frame
+    #    (vda_state_scan_tiles) and chunk-wise (vda_state_scan_chunked, chunks
+    #    of five after one anchor), on this workload's heads and frames and on
+    #    the paper's own shard (7 heads per GPU, 100 interior frames).
+    result["scan_paths"] = [scan_paths(vda, torch, Hs, Fs, dk, dv, 5, 1, K)
+                            for Hs, Fs in ((H, F), (7, 100))]
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
         result["cpu_baseline"] = cpu_baseline(w, args.cpu_budget)

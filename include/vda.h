@@ -304,6 +304,38 @@ int vda_state_scan_tiles(const void* Inv_tiles, const float* B,
                          float* S_fwd, float* S_rev, hipStream_t stream);
 
 /*
+ * vda_state_scan_chunked -- steps a3 and a4 for a chunked local window, by
+ * chunk-wise scans (Sec. 4): the frames of each chunk of the window grid
+ * (chunks of `chunk` >= 1 frames counted from `offset` positions before frame
+ * 0, 0 <= offset < chunk, clipped to [0, F); the grid of vda_options) are
+ * composed into one affine map of Eq. A.1, S_out = S_in M_c + J_c, in each
+ * direction, and the chunk sequence is scanned:
+ *     forward  P = S_T/2 (or 0); for chunks c in order: S_fwd[h][first(c)] = P,
+ *              P = P M_c + J_c
+ *     reverse  R = S_T/2 (or 0); for chunks c in reverse order:
+ *              S_rev[h][last(c)] = R, R = R M_c + J_c
+ * with the frame maps of vda_forward_ex (joint rule, decay alpha if not NULL;
+ * Inv_tiles and B as for vda_state_scan_tiles).  These are the states the
+ * windowed readout reads (Eq. A.4); all other frames of S_fwd and S_rev are
+ * left untouched.  alpha [H][F][d_k] (16-byte aligned) and text_state
+ * [H][d_v][d_k] (4-byte aligned) are DEVICE pointers or NULL.  `work` is a
+ * caller-owned device buffer (16-byte aligned) of
+ * vda_state_scan_chunked_workspace(...) bytes for M_c (split-bf16 operand
+ * tiles) and J_c (fp32).  Products are split-bf16 with fp32 accumulation.
+ * Errors: VDA_ERR_SIZE for invalid chunk / offset, else as
+ * vda_state_scan_tiles.  This is the scan vda_forward_ex runs with bf16
+ * storage, the joint rule and window_chunk >= 2 (when the clip has at least
+ * two chunks).
+ */
+int vda_state_scan_chunked(const void* Inv_tiles, const float* B, const float* alpha,
+                           const float* text_state, int F, int H, int d_k, int d_v,
+                           int chunk, int offset, void* work,
+                           float* S_fwd, float* S_rev, hipStream_t stream);
+
+/* Bytes of the work buffer of vda_state_scan_chunked (0 for invalid sizes). */
+size_t vda_state_scan_chunked_workspace(int F, int H, int d_k, int d_v, int chunk, int offset);
+
+/*
  * vda_readout -- steps a5-a7, Eq. A.4 (own-frame window), Eq. 1a and Eq. 1c:
  *     out[h][t][u] = gate[h] * RMSNorm((S_fwd[h][t] + S_rev[h][t]) q[h][t][u]).
  * q and out are bf16 (is_f32 == 0; the summed state is rounded to bf16 for

@@ -59,6 +59,24 @@ hipError_t launch_state_scan_tiled(const void* Inv_tiles, const float* Bm, int F
                                    int d_v, const ScanOptions& o, float* S_fwd, float* S_rev,
                                    hipStream_t stream);
 
+// Chunk-wise scans (joint rule, bf16 storage path): the chunks of the
+// window grid (`chunk` frames counted from `offset` before frame 0) are
+// composed into affine maps (M_c as operand tiles, J_c fp32, in `work`),
+// then scanned; writes the state entering each chunk, forward at its first
+// frame of S_fwd and reverse at its last frame of S_rev.
+int chunk_count(int F, int chunk, int offset);
+// The chunk-sequence scan alone: x <- x M_c + J_c over the C chunks (M_c as
+// operand tiles [H][2][C], J_c [H][2][C][d_v][d_k]), storing the boundary
+// states as above.
+hipError_t launch_chunk_sequence_scan(const void* Mt, const float* Jc, const float* text_state,
+                                      int F, int H, int d_k, int d_v, int chunk, int offset,
+                                      int C, float* S_fwd, float* S_rev, hipStream_t stream);
+size_t chunked_scan_workspace(int F, int H, int d_k, int d_v, int chunk, int offset);
+hipError_t launch_state_scan_chunked(const void* Inv_tiles, const float* Bm, const float* alpha,
+                                     const float* text_state, int F, int H, int d_k, int d_v,
+                                     int chunk, int offset, void* work, float* S_fwd,
+                                     float* S_rev, hipStream_t stream);
+
 // Options of the gather beyond the core (defaults: own frame, no decay).
 struct GatherOptions {
   const float* alpha = nullptr;  // [H][F][d_k] channel decay, or null (1)

@@ -88,12 +88,36 @@ __device__ __forceinline__ void tiled_mfma_phase(
   }
 }
 
-template <int DK, bool DECAY>
+// Arguments of the tiled scan.  Frame scans: tiles = Inv_t tiles [H][F],
+// add = B [H][F][d_v][d_k].  Chunk scans (CHUNKED): tiles = M_c tiles
+// [H][2][C], add = J_c [H][2][C][d_v][d_k], over the C chunks of the window
+// grid (chunk, offset).
+struct TiledScanArgs {
+  const uint16_t* tiles;
+  const float* add;
+  const float* alpha;
+  const float* text_state;
+  int F, DV;
+  unsigned nwg;
+  int chunk, offset, C;
+  float* S_fwd;
+  float* S_rev;
+};
+
+// CHUNKED: the same recurrence over the chunk sequence,
+//     x <- x M_c + J_c,
+// storing the state entering chunk c at its first frame (forward) or its
+// last frame (reverse).  The additive term comes after the product here, so
+// step j adds J of the previous chunk (loaded one step late) to the product
+// before it stores and splits the state; the last step's product is unused.
+template <int DK, bool DECAY, bool CHUNKED>
 __global__ __launch_bounds__(kThreads)
-void scan_tiled_kernel(const uint16_t* __restrict__ Invt, const float* __restrict__ Bm,
-                       const float* __restrict__ alpha, const float* __restrict__ text_state,
-                       int F, int DV, unsigned nwg, float* __restrict__ S_fwd,
-                       float* __restrict__ S_rev) {
+void scan_tiled_kernel(TiledScanArgs a) {
+  static_assert(!(CHUNKED && DECAY), "chunk maps already hold the decay");
+  const int F = a.F, DV = a.DV, C = a.C;
+  const float* __restrict__ alpha = a.alpha;
+  const float* __restrict__ text_state = a.text_state;
+  const unsigned nwg = a.nwg;
   using D = TiledDims<DK>;
   constexpr int XLD = D::XLD, PLD = D::PLD, VW = D::VW, NG = D::NG;
   constexpr int NBW = D::NBW, KB = D::KB;
@@ -128,20 +152,21 @@ void scan_tiled_kernel(const uint16_t* __restrict__ Invt, const float* __restric
                    : 0.f;
   }
 
-  float* Sout = dir == 0 ? S_fwd : S_rev;
+  float* Sout = dir == 0 ? a.S_fwd : a.S_rev;
   const size_t row_off = (size_t)(rb * 16 + pr) * DK + pc;
-  // Entering states of this head, [F][d_v][d_k]: a range-checked buffer, so
-  // the padded step past the last frame stores nothing.
+  // Entering states of this head, [F][d_v][d_k]: a range-checked buffer.
   const __amdgpu_buffer_rsrc_t srsrc =
       make_rsrc(Sout + (size_t)hb * F * mat_b, (uint32_t)(F * mat_b * sizeof(float)));
-  // B of this head, range-checked (frames outside [0, F) read as zero).
+  // Steps: frames, or chunks; matrices (tiles) and additive terms of this
+  // chain, range-checked (indices outside read as zero).
+  const int nsteps = CHUNKED ? C : F;
+  const size_t chain_mats = CHUNKED ? ((size_t)hb * 2 + dir) * C : (size_t)hb * F;
   const __amdgpu_buffer_rsrc_t brsrc =
-      make_rsrc(Bm + (size_t)hb * F * mat_b, (uint32_t)(F * mat_b * sizeof(float)));
+      make_rsrc(a.add + chain_mats * mat_b, (uint32_t)(nsteps * mat_b * sizeof(float)));
   const __amdgpu_buffer_rsrc_t arsrc =
-      make_rsrc(DECAY ? alpha + (size_t)hb * F * DK : Bm, DECAY ? (uint32_t)(F * DK * 4) : 0u);
-  // Operand tiles of this head's frames, [F][d_k * d_k * 4 bytes].
-  const __amdgpu_buffer_rsrc_t trsrc =
-      make_rsrc(Invt + (size_t)hb * F * (DK * DK * 2), (uint32_t)F * (uint32_t)(DK * DK * 4));
+      make_rsrc(DECAY ? alpha + (size_t)hb * F * DK : a.add, DECAY ? (uint32_t)(F * DK * 4) : 0u);
+  const __amdgpu_buffer_rsrc_t trsrc = make_rsrc(a.tiles + chain_mats * (DK * DK * 2),
+                                                 (uint32_t)nsteps * (uint32_t)(DK * DK * 4));
 
   // This wave's tile offsets within a frame (out of range for the slices of
   // idle waves at d_k = 32).
@@ -156,7 +181,22 @@ void scan_tiled_kernel(const uint16_t* __restrict__ Invt, const float* __restric
         toff[m][ks][p] = nb < D::NB ? operand_tile_offset(DK, p, nb, ks, lane) : kOutOfRange;
   }
 
-  auto frame_of = [&](int step) { return dir == 0 ? step : F - 1 - step; };
+  // Matrix of step `step` (frame or chunk in scan order), the index of its
+  // additive term (chunks: the previous chunk's J, none before the first),
+  // and the frame whose entering state the step stores (-1: none).
+  auto frame_of = [&](int step) { return dir == 0 ? step : nsteps - 1 - step; };
+  auto add_of = [&](int step) {
+    if constexpr (CHUNKED) return step >= 1 ? frame_of(step - 1) : -1;
+    return frame_of(step);
+  };
+  auto store_frame = [&](int step) {
+    if (step >= nsteps) return -1;
+    if constexpr (CHUNKED) {
+      const int c = frame_of(step);
+      return dir == 0 ? max(0, c * a.chunk - a.offset) : min(F - 1, (c + 1) * a.chunk - a.offset - 1);
+    }
+    return frame_of(step);
+  };
 
   // Two-frame register ring, as separately named arrays (compile-time
   // indices only).
@@ -165,12 +205,14 @@ void scan_tiled_kernel(const uint16_t* __restrict__ Invt, const float* __restric
   u32x4 al0, al1;  // alpha_t, columns 4 tid .. 4 tid + 3 (threads tid < DK / 4)
   auto load_step = [&](int step, u32x4 (&t)[NBW][KB][2], float (&bb)[NG][VW], u32x4& al) {
     const int frame = frame_of(step);
+    const int ai = add_of(step);
     // B rows first (they are needed earlier in the step than the tiles),
     // and everything through buffer loads, which the compiler keeps in
     // program order.
 #pragma unroll
     for (int g = 0; g < NG; ++g) {
-      const uint32_t off = (uint32_t)(((size_t)frame * mat_b + row_off + g * 16 * VW) * 4u);
+      const uint32_t off =
+          ai >= 0 ? (uint32_t)(((size_t)ai * mat_b + row_off + g * 16 * VW) * 4u) : kOutOfRange;
       if constexpr (VW == 4) {
         const u32x4 x =
             __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(brsrc, (int)off, 0, 0));
@@ -204,35 +246,44 @@ void scan_tiled_kernel(const uint16_t* __restrict__ Invt, const float* __restric
   int cur = 0;
   auto step_body = [&](int step, u32x4 (&t)[NBW][KB][2], float (&bb)[NG][VW], u32x4& al,
                        const u32x4& al_next) {
-    // Frame index within the head; past the end it is out of the buffer
-    // range (>= F forward, negative and so huge as unsigned in reverse).
-    const int frame = dir == 0 ? step : F - 1 - step;
+    // Frame whose entering state this step stores (-1 for a padded step
+    // past the end: the stores go out of the buffer's range).
+    const int sf = store_frame(step);
     lds_barrier();  // xs[cur] holds the entering state; last step's plane reads are done
     {
-      const uint32_t off = (uint32_t)((size_t)(unsigned)frame * mat_b + row_off) * 4u;
 #pragma unroll
       for (int g = 0; g < NG; ++g) {
+        const uint32_t off =
+            sf >= 0 ? (uint32_t)(((size_t)sf * mat_b + row_off + g * 16 * VW) * 4u) : kOutOfRange;
         const int xo = pr * XLD + pc + g * 16 * VW;
         float v[VW];
         if constexpr (VW == 4) {
           const floatx4 xv = reinterpret_cast<const floatx4*>(xs[cur])[xo / 4];
 #pragma unroll
           for (int c = 0; c < 4; ++c) v[c] = xv[c];
-          store_b128(srsrc, off + g * 64u * VW,
-                     u32x4{__float_as_uint(v[0]), __float_as_uint(v[1]), __float_as_uint(v[2]),
-                           __float_as_uint(v[3])});
         } else {
           const float2 xv = *reinterpret_cast<const float2*>(&xs[cur][xo]);
           v[0] = xv.x;
           v[1] = xv.y;
-          store_b64(srsrc, off + g * 64u * VW, make_uint2(__float_as_uint(v[0]), __float_as_uint(v[1])));
         }
+        if constexpr (CHUNKED) {  // J of the previous chunk, after its product
+#pragma unroll
+          for (int c = 0; c < VW; ++c) v[c] += bb[g][c];
+        }
+        if constexpr (VW == 4)
+          store_b128(srsrc, off,
+                     u32x4{__float_as_uint(v[0]), __float_as_uint(v[1]), __float_as_uint(v[2]),
+                           __float_as_uint(v[3])});
+        else
+          store_b64(srsrc, off, make_uint2(__float_as_uint(v[0]), __float_as_uint(v[1])));
         if constexpr (DECAY) {
 #pragma unroll
           for (int c = 0; c < VW; ++c) v[c] *= alds[pc + g * 16 * VW + c];
         }
+        if constexpr (!CHUNKED) {  // B of this frame, before its product
 #pragma unroll
-        for (int c = 0; c < VW; ++c) v[c] += bb[g][c];
+          for (int c = 0; c < VW; ++c) v[c] += bb[g][c];
+        }
         // The product's A-operand, split once here into bf16 hi and lo.
         uint32_t hw[VW / 2], lw[VW / 2];
 #pragma unroll
@@ -266,7 +317,7 @@ void scan_tiled_kernel(const uint16_t* __restrict__ Invt, const float* __restric
     // Refill this slot with the frame two steps on, once its tiles are
     // consumed (past the end: a clamped, unused frame), always, so no branch
     // hides the loads from the wait-count bookkeeping.
-    load_step(min(step + 2, F - 1), t, bb, al);
+    load_step(min(step + 2, nsteps - 1), t, bb, al);
     cur ^= 1;
   };
 
@@ -274,46 +325,77 @@ void scan_tiled_kernel(const uint16_t* __restrict__ Invt, const float* __restric
   // the oldest load on loop entry.
   load_step(0, t0, bs0, al0);
   __builtin_amdgcn_sched_barrier(0);
-  load_step(min(1, F - 1), t1, bs1, al1);
+  load_step(min(1, nsteps - 1), t1, bs1, al1);
   __builtin_amdgcn_sched_barrier(0);
   if constexpr (DECAY) {  // alpha of step 0
     if (tid < DK / 4) reinterpret_cast<u32x4*>(alds)[tid] = al0;
   }
-  // The step count is padded to an even number; a padded step (step >= F)
-  // reads a clamped frame and its stores are dropped, so the loop body has
-  // no early exit.
-  for (int step0 = 0; step0 < F; step0 += 2) {
+  // The step count is padded to an even number; a padded step
+  // (step >= nsteps) reads a clamped matrix and stores nothing, so the loop
+  // body has no early exit.
+  for (int step0 = 0; step0 < nsteps; step0 += 2) {
     step_body(step0, t0, bs0, al0, al1);
     step_body(step0 + 1, t1, bs1, al1, al0);
   }
 }
 
-template <int DK>
-hipError_t launch_tiled_t(const void* Invt, const float* Bm, int F, int H, int d_v,
-                          const ScanOptions& o, float* S_fwd, float* S_rev, hipStream_t stream) {
-  const unsigned nwg = (unsigned)H * 2u * (unsigned)(d_v / 16);
-  const uint16_t* t = static_cast<const uint16_t*>(Invt);
-  if (o.alpha != nullptr)
-    hipLaunchKernelGGL((scan_tiled_kernel<DK, true>), dim3(nwg), dim3(kThreads), 0, stream, t, Bm,
-                       o.alpha, o.text_state, F, d_v, nwg, S_fwd, S_rev);
-  else
-    hipLaunchKernelGGL((scan_tiled_kernel<DK, false>), dim3(nwg), dim3(kThreads), 0, stream, t, Bm,
-                       o.alpha, o.text_state, F, d_v, nwg, S_fwd, S_rev);
+template <int DK, bool DECAY, bool CHUNKED>
+hipError_t launch_tiled_k(TiledScanArgs a, int H, hipStream_t stream) {
+  a.nwg = (unsigned)H * 2u * (unsigned)(a.DV / 16);
+  hipLaunchKernelGGL((scan_tiled_kernel<DK, DECAY, CHUNKED>), dim3(a.nwg), dim3(kThreads), 0,
+                     stream, a);
   return hipGetLastError();
 }
 
+template <int DK>
+hipError_t launch_tiled_t(const TiledScanArgs& a, int H, bool chunked, hipStream_t stream) {
+  if (chunked) return launch_tiled_k<DK, false, true>(a, H, stream);
+  if (a.alpha != nullptr) return launch_tiled_k<DK, true, false>(a, H, stream);
+  return launch_tiled_k<DK, false, false>(a, H, stream);
+}
+
+hipError_t launch_tiled(const TiledScanArgs& a, int H, int d_k, bool chunked, hipStream_t stream) {
+  switch (d_k) {
+    case 32: return launch_tiled_t<32>(a, H, chunked, stream);
+    case 64: return launch_tiled_t<64>(a, H, chunked, stream);
+    case 128: return launch_tiled_t<128>(a, H, chunked, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
 }  // namespace
+
+hipError_t launch_chunk_sequence_scan(const void* Mt, const float* Jc, const float* text_state,
+                                      int F, int H, int d_k, int d_v, int chunk, int offset,
+                                      int C, float* S_fwd, float* S_rev, hipStream_t stream) {
+  TiledScanArgs a{};
+  a.tiles = static_cast<const uint16_t*>(Mt);
+  a.add = Jc;
+  a.text_state = text_state;
+  a.F = F;
+  a.DV = d_v;
+  a.chunk = chunk;
+  a.offset = offset;
+  a.C = C;
+  a.S_fwd = S_fwd;
+  a.S_rev = S_rev;
+  return launch_tiled(a, H, d_k, true, stream);
+}
 
 hipError_t launch_state_scan_tiled(const void* Inv_tiles, const float* Bm, int F, int H, int d_k,
                                    int d_v, const ScanOptions& o, float* S_fwd, float* S_rev,
                                    hipStream_t stream) {
   if (o.frozen) return hipErrorInvalidValue;
-  switch (d_k) {
-    case 32: return launch_tiled_t<32>(Inv_tiles, Bm, F, H, d_v, o, S_fwd, S_rev, stream);
-    case 64: return launch_tiled_t<64>(Inv_tiles, Bm, F, H, d_v, o, S_fwd, S_rev, stream);
-    case 128: return launch_tiled_t<128>(Inv_tiles, Bm, F, H, d_v, o, S_fwd, S_rev, stream);
-    default: return hipErrorInvalidValue;
-  }
+  TiledScanArgs a{};
+  a.tiles = static_cast<const uint16_t*>(Inv_tiles);
+  a.add = Bm;
+  a.alpha = o.alpha;
+  a.text_state = o.text_state;
+  a.F = F;
+  a.DV = d_v;
+  a.S_fwd = S_fwd;
+  a.S_rev = S_rev;
+  return launch_tiled(a, H, d_k, false, stream);
 }
 
 }  // namespace vda

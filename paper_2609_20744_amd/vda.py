@@ -56,6 +56,8 @@ _SIGNATURES = {
     "vda_frame_inverse_tiles": (_I, [_P, _P, _I, _I, _I, _I, _I, _P, _P]),
     "vda_state_scan": (_I, [_P, _P, _I, _I, _I, _I, _I, _P, _P, _P]),
     "vda_state_scan_tiles": (_I, [_P, _P, _I, _I, _I, _I, _P, _P, _P]),
+    "vda_state_scan_chunked": (_I, [_P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _P, _P, _P, _P]),
+    "vda_state_scan_chunked_workspace": (ctypes.c_size_t, [_I, _I, _I, _I, _I, _I]),
     "vda_readout": (_I, [_P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _P, _P]),
 }
 
@@ -333,6 +335,45 @@ def state_scan_tiles(Inv_tiles, B, S_fwd=None, S_rev=None, stream=None):
                                       S_fwd.data_ptr(), S_rev.data_ptr(), _stream_ptr(dev, stream))
     _check(st, "vda_state_scan_tiles")
     return S_fwd, S_rev
+
+
+def state_scan_chunked(Inv_tiles, B, chunk, offset=0, alpha=None, text_state=None, S_fwd=None,
+                       S_rev=None, work=None, stream=None):
+    """Chunk-wise scans for a chunked window (vda_state_scan_chunked): the
+    states entering every chunk of the window grid, forward at the chunk's
+    first frame of S_fwd, reverse at its last frame of S_rev (other frames
+    untouched; new outputs are zero-filled).  Inv_tiles as for
+    state_scan_tiles, B [H, F, d_v, d_k] fp32, alpha [H, F, d_k] and
+    text_state [H, d_v, d_k] fp32 or None; work: a device buffer of
+    chunked_workspace(...) bytes (allocated if None)."""
+    torch = _torch()
+    H, F, d_v, d_k = B.shape
+    dev = B.device
+    if Inv_tiles.numel() * Inv_tiles.element_size() != H * F * d_k * d_k * 4:
+        raise ValueError("Inv_tiles must hold d_k * d_k * 4 bytes per frame")
+    for t, n in ((alpha, "alpha"), (text_state, "text_state")):
+        if t is not None:
+            _require(t, n, torch.float32, dev)
+    if S_fwd is None:
+        S_fwd = torch.zeros((H, F, d_v, d_k), dtype=torch.float32, device=dev)
+    if S_rev is None:
+        S_rev = torch.zeros((H, F, d_v, d_k), dtype=torch.float32, device=dev)
+    if work is None:
+        nbytes = chunked_workspace(F, H, d_k, d_v, chunk, offset)
+        work = torch.empty((max(nbytes, 16),), dtype=torch.uint8, device=dev)
+    with torch.cuda.device(dev):
+        st = lib.vda_state_scan_chunked(
+            Inv_tiles.data_ptr(), B.data_ptr(), alpha.data_ptr() if alpha is not None else None,
+            text_state.data_ptr() if text_state is not None else None, F, H, d_k, d_v, int(chunk),
+            int(offset), work.data_ptr(), S_fwd.data_ptr(), S_rev.data_ptr(),
+            _stream_ptr(dev, stream))
+    _check(st, "vda_state_scan_chunked")
+    return S_fwd, S_rev
+
+
+def chunked_workspace(F: int, H: int, d_k: int, d_v: int, chunk: int, offset: int = 0) -> int:
+    """Bytes of the work buffer of state_scan_chunked."""
+    return int(lib.vda_state_scan_chunked_workspace(F, H, d_k, d_v, int(chunk), int(offset)))
 
 
 def readout(q, S_fwd, S_rev, gate, d_v=None, out=None, stream=None):

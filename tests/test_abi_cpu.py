@@ -100,6 +100,35 @@ def test_stage_validation():
     assert L.vda_frame_inverse(big, None, 0, 1, 8, 16, 64, 2 * big, None) == 3
     assert L.vda_state_scan(big, 2 * big, 4, 2, 64, 16, 0, 3 * big, 4 * big, None) == 3
     assert L.vda_readout(big, 2 * big, 3 * big, 4 * big, 4, 64, 2, 64, 16, 0, 5 * big, None) == 3
+    # tiled inverse and scan: the same checks as their fp32-layout forms
+    it = L.vda_frame_inverse_tiles
+    assert it(None, None, 0, 1, 8, 64, 64, big, None) == 1
+    assert it(big, None, 0, 1, 8, 96, 64, 2 * big, None) == 3
+    assert it(big, 3 * big, 8, 2, 8, 64, 64, big + 8 * mat, None) == 5
+    sct = L.vda_state_scan_tiles
+    assert sct(None, 2 * big, 4, 2, 64, 64, 3 * big, 4 * big, None) == 1
+    assert sct(big, 2 * big, 4, 2, 64, 64, 3 * big, 3 * big, None) == 5
+    assert sct(big, 2 * big, 4, 2, 64, 48, 3 * big, 4 * big, None) == 3
+    assert sct(big + 4, 2 * big, 4, 2, 64, 64, 3 * big, 4 * big, None) == 4
+    # the frames of one head must stay within 32-bit byte offsets
+    assert sct(big, 2 * big, 40000, 1, 128, 128, 3 * big, 4 * big, None) == 2
+    # chunked scan: (Inv_tiles, B, alpha, text_state, F, H, d_k, d_v, chunk, offset, work,
+    #                S_fwd, S_rev, stream)
+    ch = L.vda_state_scan_chunked
+    assert ch(big, 2 * big, None, None, 12, 2, 64, 64, 5, 1, None, 3 * big, 4 * big, None) == 1
+    assert ch(big, 2 * big, None, None, 12, 2, 64, 64, 0, 0, 5 * big, 3 * big, 4 * big, None) == 2
+    assert ch(big, 2 * big, None, None, 12, 2, 64, 64, 5, 5, 5 * big, 3 * big, 4 * big, None) == 2
+    assert ch(big, 2 * big, None, None, 12, 2, 64, 64, 5, -1, 5 * big, 3 * big, 4 * big, None) == 2
+    assert ch(big, 2 * big, big + 8, None, 12, 2, 64, 64, 5, 1, 5 * big, 3 * big, 4 * big,
+              None) == 4
+    assert ch(big, 2 * big, None, None, 12, 2, 64, 64, 5, 1, 5 * big + 8, 3 * big, 4 * big,
+              None) == 4
+    assert ch(big, 2 * big, None, None, 12, 2, 64, 64, 5, 1, 3 * big, 3 * big, 4 * big, None) == 5
+    assert ch(big, 2 * big, None, None, 12, 2, 64, 48, 5, 1, 5 * big, 3 * big, 4 * big, None) == 3
+    ws = L.vda_state_scan_chunked_workspace
+    # 3 chunks (frames 0-3, 4-8, 9-11) x 2 directions x 2 heads x (M tiles + J)
+    assert ws(12, 2, 64, 32, 5, 1) == 3 * 2 * 2 * (64 * 64 * 4 + 32 * 64 * 4)
+    assert ws(12, 2, 64, 32, 5, 5) == 0 and ws(12, 2, 64, 48, 5, 1) == 0
 
 
 def test_single_hip_runtime_loaded():

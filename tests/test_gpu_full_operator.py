@@ -145,3 +145,101 @@ def test_full_size_sampled(V):
         exp = O.rmsnorm_gate(o, float(xo["gate"][h]))
         err = rel_max_err(got[h][frames, toks], exp)
         assert err <= tol_for(w), (h, err)
+
+
+@pytest.mark.parametrize("dk,dv", [(32, 64), (64, 128), (128, 32), (128, 128)])
+def test_chunked_scan_stage(V, dk, dv):
+    """Chunk-wise scans (Section 4) fed with the oracle's Inv_t (as split-bf16
+    operand tiles) and B_t: the state entering every chunk, forward at its
+    first frame and reverse at its last, equals the oracle's chunk-sequence
+    scan, with and without decay and text state; other frames stay
+    untouched."""
+    import torch
+    from vda_testutil import to_operand_tiles
+    H, F = 3, 13
+    _log(f"chunked scan dk={dk} dv={dv}")
+    w = I.custom("chunked", 1, H, F, 40, dk, dv, "f32", seed=dk + dv)
+    x = I.make_inputs(w)
+    xo = oracle_inputs(w, x)
+    alpha, S_T = I.make_decay(w), I.make_text_state(w)
+    As = np.empty((H, F, dk, dk))
+    Bs = np.empty((H, F, dv, dk))
+    for h in range(H):
+        As[h], Bs[h] = O.head_statistics(xo["k"][h], xo["v"][h], xo["beta"][h])
+    Inv = np.linalg.inv(np.eye(dk) + As)
+    T = to_operand_tiles(Inv).cuda()
+    Bd = to_device(Bs.astype(np.float32), "f32")
+    for chunk, offset in ((5, 1), (3, 0), (4, 3), (13, 0), (2, 1)):
+        for decay, text in ((False, False), (True, True)):
+            a_dev = to_device(alpha, "f32") if decay else None
+            t_dev = to_device(S_T, "f32") if text else None
+            Sf, Sr = V.state_scan_chunked(T, Bd, chunk, offset, alpha=a_dev, text_state=t_dev)
+            torch.cuda.synchronize()
+            Sf, Sr = Sf.double().cpu().numpy(), Sr.double().cpu().numpy()
+            ranges = O.chunk_ranges(F, chunk, offset)
+            firsts = {lo for lo, _ in ranges}
+            lasts = {hi for _, hi in ranges}
+            for h in range(H):
+                S0 = 0.5 * S_T[h].astype(np.float64) if text else np.zeros((dv, dk))
+                Pb, Rb = O.chunk_boundary_states(As[h], Bs[h], S0, chunk, offset,
+                                                 alpha[h].astype(np.float64) if decay else None)
+                for c, (lo, hi) in enumerate(ranges):
+                    ef = rel_max_err(Sf[h, lo], Pb[c]) if np.any(Pb[c]) else np.max(np.abs(Sf[h, lo]))
+                    er = rel_max_err(Sr[h, hi], Rb[c]) if np.any(Rb[c]) else np.max(np.abs(Sr[h, hi]))
+                    assert ef < 1e-4 and er < 1e-4, (chunk, offset, decay, text, h, c, ef, er)
+                for t in range(F):
+                    if t not in firsts:
+                        assert not np.any(Sf[h, t])
+                    if t not in lasts:
+                        assert not np.any(Sr[h, t])
+
+
+def test_chunked_scan_many_workgroups(V):
+    """Enough chunk chains that several workgroups run per compute unit and
+    in more than one round: bitwise repeatable, and equal to the oracle's
+    chunk-sequence scan at every boundary."""
+    import torch
+    from vda_testutil import to_operand_tiles
+    H, F, dk, dv = 24, 36, 64, 128
+    _log(f"chunked scan many workgroups H={H} F={F}")
+    rng = np.random.default_rng(5)
+    G = rng.standard_normal((H, F, dk, dk)) / np.sqrt(dk)
+    A = G @ np.swapaxes(G, -1, -2)
+    Inv = np.linalg.inv(np.eye(dk) + A)
+    Bm = rng.standard_normal((H, F, dv, dk))
+    alpha = rng.uniform(0.6, 1.0, (H, F, dk))
+    T = to_operand_tiles(Inv).cuda()
+    Bd, ad = to_device(Bm.astype(np.float32), "f32"), to_device(alpha.astype(np.float32), "f32")
+    S1 = V.state_scan_chunked(T, Bd, 5, 1, alpha=ad)
+    S2 = V.state_scan_chunked(T, Bd, 5, 1, alpha=ad)
+    torch.cuda.synchronize()
+    assert torch.equal(S1[0], S2[0]) and torch.equal(S1[1], S2[1])
+    Sf, Sr = S1[0].double().cpu().numpy(), S1[1].double().cpu().numpy()
+    a32 = alpha.astype(np.float32).astype(np.float64)
+    B32 = Bm.astype(np.float32).astype(np.float64)
+    for h in (0, H - 1):
+        # the oracle's chunk maps from Inv_t directly: A with (I + A)^-1 = Inv
+        A_h = np.linalg.inv(Inv[h]) - np.eye(dk)
+        Pb, Rb = O.chunk_boundary_states(A_h, B32[h], np.zeros((dv, dk)), 5, 1, a32[h])
+        for c, (lo, hi) in enumerate(O.chunk_ranges(F, 5, 1)):
+            if c > 0:
+                assert rel_max_err(Sf[h, lo], Pb[c]) < 1e-4, (h, c)
+            if c < len(Pb) - 1:
+                assert rel_max_err(Sr[h, hi], Rb[c]) < 1e-4, (h, c)
+
+
+@pytest.mark.parametrize("H,dk,dv", [(7, 128, 128), (3, 64, 32)])
+def test_full_operator_paper_shard(V, H, dk, dv):
+    """The paper's own shard shape (a few heads per GPU, 100 interior frames,
+    chunks of five after one anchor, decay and text state), where the
+    forward takes the chunk-wise scans: whole output against the oracle.
+    The token count is kept small (and ragged) so the oracle stays fast."""
+    _log(f"full operator paper shard H={H} dk={dk} dv={dv}")
+    w = I.custom("ex_shard", 1, H, 100, 37, dk, dv, "bf16", seed=46 + dk)
+    x = I.make_inputs(w)
+    alpha, S_T = I.make_decay(w), I.make_text_state(w)
+    got = _run(V, w, x, alpha, S_T, PAPER_WINDOW)
+    exp = _oracle(w, x, alpha, S_T, PAPER_WINDOW)
+    err = rel_max_err(got, exp)
+    _log(f"  rel err {err:.2e}")
+    assert err <= tol_for(w), err
