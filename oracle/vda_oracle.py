@@ -30,6 +30,10 @@ of the window grid into one affine map of Eq. A.1 and scan the chunk
 sequence (Section 4); they give the states at chunk boundaries, which equal
 the frame-by-frame scans' states there.
 
+The feature map before the operator (vda_prep: depthwise 5 x 5 spatial and
+five-tap temporal convolution of K and V, SiLU, L2 normalisation of Q and K,
+frame-major layout per head) is the VDA-Prep step of Section 4.
+
 The full gather (the *_ex functions at the end) adds what the core leaves
 at its special values: the channel-wise decay alpha_t (S_bar_t =
 S_{t-1} Diag(alpha_t), Eq. 3a/5 and A.1), the text state S_T starting both
@@ -427,3 +431,71 @@ def chunk_boundary_states(As, Bs, S0, chunk: int, offset: int = 0, alphas=None):
         M, J = chunk_map(As, Bs, range(hi, lo - 1, -1), alphas)
         R = R @ M + J
     return Pb, Rb
+
+
+# ----------------------------------------------------------------------------
+# VDA-Prep (Section 2.3 and Section 4): the linear branch's feature map
+# ----------------------------------------------------------------------------
+
+#: Epsilon of the L2 normalisation of Q and K (not stated in the paper).
+L2_EPS = 1e-6
+
+
+def depthwise_conv3(x: np.ndarray, w_spatial: np.ndarray, w_temporal: np.ndarray) -> np.ndarray:
+    """The separable short convolution of K and V: a depthwise 5 x 5 spatial
+    filter and a depthwise five-tap temporal filter (Section 2.3), centred,
+    as cross-correlations with zero padding at the clip and frame borders.
+
+    x [F, gh, gw, C] (C channels, one filter per channel); w_spatial
+    [C, 5, 5] indexed [c, dy, dx] for offsets dy - 2, dx - 2; w_temporal
+    [C, 5] for frame offsets dt - 2.  Both filters are linear in x, so the
+    order of the two passes does not matter; here spatial, then temporal."""
+    F, gh, gw, C = x.shape
+    r = w_spatial.shape[1] // 2
+    rt = w_temporal.shape[1] // 2
+    xp = np.zeros((F, gh + 2 * r, gw + 2 * r, C))
+    xp[:, r:r + gh, r:r + gw] = x
+    s = np.zeros((F, gh, gw, C))
+    for dy in range(2 * r + 1):
+        for dx in range(2 * r + 1):
+            s += w_spatial[:, dy, dx] * xp[:, dy:dy + gh, dx:dx + gw]
+    sp = np.zeros((F + 2 * rt, gh, gw, C))
+    sp[rt:rt + F] = s
+    out = np.zeros_like(s)
+    for dt in range(2 * rt + 1):
+        out += w_temporal[:, dt] * sp[dt:dt + F]
+    return out
+
+
+def silu(x: np.ndarray) -> np.ndarray:
+    """SiLU(x) = x * sigmoid(x)."""
+    return x / (1.0 + np.exp(-x))
+
+
+def l2_normalise(x: np.ndarray, eps: float = L2_EPS) -> np.ndarray:
+    """x / sqrt(sum x^2 + eps) over the last axis (one token of one head)."""
+    return x / np.sqrt(np.sum(x * x, axis=-1, keepdims=True) + eps)
+
+
+def vda_prep(q, k, v, grid, H: int, wk_spatial, wk_temporal, wv_spatial, wv_temporal,
+             eps: float = L2_EPS):
+    """The linear branch's feature map (Section 2.3; VDA-Prep of Section 4)
+    for one clip: K and V pass through their separable short convolution and
+    SiLU, Q and K are L2-normalised per token and head, and everything is
+    laid out frame-major per head.
+
+    q, k, v [F, N, H*d] (token-major projections, N = gh * gw tokens per
+    frame in row-major grid order, H heads of d channels each); grid =
+    (gh, gw); w*_spatial [H*d, 5, 5], w*_temporal [H*d, 5].
+    Returns (q, k, v) each [H, F, N, d]."""
+    F, N, Cq = q.shape
+    gh, gw = grid
+    assert gh * gw == N
+
+    def heads(x):
+        d = x.shape[-1] // H
+        return np.ascontiguousarray(x.reshape(F, N, H, d).transpose(2, 0, 1, 3))
+
+    kc = silu(depthwise_conv3(k.reshape(F, gh, gw, -1), wk_spatial, wk_temporal)).reshape(F, N, -1)
+    vc = silu(depthwise_conv3(v.reshape(F, gh, gw, -1), wv_spatial, wv_temporal)).reshape(F, N, -1)
+    return l2_normalise(heads(q), eps), l2_normalise(heads(kc), eps), heads(vc)

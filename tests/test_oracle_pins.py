@@ -597,6 +597,95 @@ def pin_chunk_scan_matches_frame_scan():
             np.testing.assert_allclose(Rb[c], R[hi + 2], rtol=1e-11, atol=1e-12)
 
 
+def _prep_case(rng, F=4, gh=5, gw=6, H=2, d=3):
+    C = H * d
+    x = {n: rng.standard_normal((F, gh * gw, C)) for n in ("q", "k", "v")}
+    w = {n: rng.standard_normal(shape) for n, shape in
+         (("ks", (C, 5, 5)), ("kt", (C, 5)), ("vs", (C, 5, 5)), ("vt", (C, 5)))}
+    return x, w, (gh, gw), H
+
+
+def pin_prep_conv_matches_library():
+    """Section 2.3: the depthwise 5 x 5 spatial and five-tap temporal filters
+    equal torch's grouped 3-D cross-correlation with the separable kernel
+    w_t[c, dt] w_s[c, dy, dx] and zero padding 2 (a textbook reduction)."""
+    import torch
+    rng = _rng(41)
+    F, gh, gw, C = 6, 5, 7, 3
+    x = rng.standard_normal((F, gh, gw, C))
+    ws, wt = rng.standard_normal((C, 5, 5)), rng.standard_normal((C, 5))
+    got = O.depthwise_conv3(x, ws, wt)
+    kern = torch.from_numpy(wt[:, :, None, None] * ws[:, None, :, :])[:, None]   # [C,1,5,5,5]
+    xt = torch.from_numpy(np.ascontiguousarray(x.transpose(3, 0, 1, 2)))[None]   # [1,C,F,gh,gw]
+    ref = torch.nn.functional.conv3d(xt, kern, padding=2, groups=C)[0].numpy().transpose(1, 2, 3, 0)
+    np.testing.assert_allclose(got, ref, rtol=1e-12, atol=1e-12)
+
+
+def pin_prep_conv_hand_cases():
+    """Hand-derived cases: centred unit taps pass the input through; a spatial
+    tap at offset (0, +1) reads the right-hand neighbour (zero past the last
+    column); a temporal tap at offset -1 reads the previous frame (zero before
+    the first)."""
+    rng = _rng(42)
+    F, gh, gw, C = 3, 2, 3, 2
+    x = rng.standard_normal((F, gh, gw, C))
+    ws = np.zeros((C, 5, 5))
+    wt = np.zeros((C, 5))
+    ws[:, 2, 2] = 1.0
+    wt[:, 2] = 1.0
+    np.testing.assert_array_equal(O.depthwise_conv3(x, ws, wt), x)
+    ws2 = np.zeros((C, 5, 5))
+    ws2[:, 2, 3] = 1.0
+    exp = np.zeros_like(x)
+    exp[:, :, :-1] = x[:, :, 1:]
+    np.testing.assert_array_equal(O.depthwise_conv3(x, ws2, wt), exp)
+    wt2 = np.zeros((C, 5))
+    wt2[:, 1] = 1.0
+    exp = np.zeros_like(x)
+    exp[1:] = x[:-1]
+    np.testing.assert_array_equal(O.depthwise_conv3(x, ws, wt2), exp)
+
+
+def pin_prep_feature_map():
+    """Section 2.3: K and V are convolved then passed through SiLU (torch's
+    silu), Q and K are L2-normalised per token and head (unit norm when the
+    norm dwarfs eps; torch's normalize), V is not normalised, and the layout
+    is [head][frame][token][channel] with head h taking channels h*d..h*d+d-1."""
+    import torch
+    rng = _rng(43)
+    x, w, grid, H = _prep_case(rng, d=8)
+    q, k, v = O.vda_prep(x["q"], x["k"], x["v"], grid, H, w["ks"], w["kt"], w["vs"], w["vt"])
+    F, N, C = x["q"].shape
+    d = C // H
+    conv = lambda t, ws, wt: O.depthwise_conv3(t.reshape(F, grid[0], grid[1], C), ws, wt).reshape(F, N, C)
+    silu = lambda t: torch.nn.functional.silu(torch.from_numpy(t)).numpy()
+    norm = lambda t: torch.nn.functional.normalize(torch.from_numpy(t), dim=-1).numpy()
+    kc, vc = silu(conv(x["k"], w["ks"], w["kt"])), silu(conv(x["v"], w["vs"], w["vt"]))
+    for h in range(H):
+        sl = slice(h * d, (h + 1) * d)
+        # eps inside the square root moves the result by ~eps / (2 |x|^2)
+        np.testing.assert_allclose(q[h], norm(x["q"][:, :, sl]), rtol=2e-5, atol=1e-9)
+        np.testing.assert_allclose(k[h], norm(kc[:, :, sl]), rtol=2e-5, atol=1e-9)
+        np.testing.assert_allclose(v[h], vc[:, :, sl], rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(np.linalg.norm(q, axis=-1), 1.0, atol=2e-5)
+
+
+def pin_prep_filters_commute():
+    """The spatial and temporal filters are linear and act on different axes,
+    so applying the temporal filter first (as a pass with a unit spatial
+    tap) and the spatial one second gives the same result."""
+    rng = _rng(44)
+    F, gh, gw, C = 5, 4, 6, 2
+    x = rng.standard_normal((F, gh, gw, C))
+    ws, wt = rng.standard_normal((C, 5, 5)), rng.standard_normal((C, 5))
+    unit_s = np.zeros((C, 5, 5))
+    unit_s[:, 2, 2] = 1.0
+    unit_t = np.zeros((C, 5))
+    unit_t[:, 2] = 1.0
+    two_pass = O.depthwise_conv3(O.depthwise_conv3(x, unit_s, wt), ws, unit_t)
+    np.testing.assert_allclose(O.depthwise_conv3(x, ws, wt), two_pass, rtol=1e-12, atol=1e-12)
+
+
 PINS = [f for name, f in sorted(globals().items()) if name.startswith("pin_")]
 
 
@@ -731,6 +820,31 @@ def _mut_chunk_ranges_unclipped(F, chunk, offset=0):
     return [(lo, min(F - 1, lo + chunk - 1)) for lo, _ in _ORIG_CHUNK_RANGES(F, chunk, offset)]
 
 
+def _mut_conv_wraps(x, w_spatial, w_temporal):
+    F, gh, gw, C = x.shape
+    s = np.zeros_like(x)
+    for dy in range(5):
+        for dx in range(5):
+            s += w_spatial[:, dy, dx] * np.roll(x, (2 - dy, 2 - dx), axis=(1, 2))
+    out = np.zeros_like(x)
+    for dt in range(5):
+        out += w_temporal[:, dt] * np.roll(s, 2 - dt, axis=0)
+    return out
+
+
+def _mut_conv_flipped(x, w_spatial, w_temporal):
+    return _ORIG_CONV(x, w_spatial[:, ::-1, ::-1], w_temporal[:, ::-1])
+
+
+def _mut_l2_over_tokens(x, eps=O.L2_EPS):
+    return x / np.sqrt(np.sum(x * x, axis=-2, keepdims=True) + eps)
+
+
+def _mut_silu_is_sigmoid(x):
+    return 1.0 / (1.0 + np.exp(-x))
+
+
+_ORIG_CONV = O.depthwise_conv3
 _ORIG_GATHER_EX = O.gathered_states_ex
 _ORIG_WINDOWS = O.local_windows
 _ORIG_CHUNK_RANGES = O.chunk_ranges
@@ -742,6 +856,10 @@ MUTANTS = [
     ("gathered_states_ex", _mut_text_state_not_halved),
     ("local_windows", _mut_windows_ignore_offset),
     ("chunk_map", _mut_chunk_map_wrong_order),
+    ("depthwise_conv3", _mut_conv_wraps),
+    ("depthwise_conv3", _mut_conv_flipped),
+    ("l2_normalise", _mut_l2_over_tokens),
+    ("silu", _mut_silu_is_sigmoid),
     ("chunk_ranges", _mut_chunk_ranges_unclipped),
     ("frame_statistics", _mut_stats_no_beta),
     ("frame_statistics", _mut_stats_beta_squared),
