@@ -145,6 +145,38 @@ def pmc_summary(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, copy_gib, 
             "write_factor": f_write, "kernels": kernels}
 
 
+def prep_bench(vda, torch, w, K):
+    """Time vda_prep on the workload's shape (B clips, F frames, H heads,
+    latent grid, d_k / d_v channels) from seeded synthetic projections.  Its
+    algorithmic bytes are the three bf16 inputs and outputs (filters are
+    negligible)."""
+    import numpy as np
+    from paper_2609_20744_amd import inputs as I
+    if w.dtype != "bf16" or w.grid is None or w.d_k not in (64, 128) or w.d_v not in (64, 128):
+        return None
+    x = I.make_prep_inputs(w.B, w.F, w.grid, w.H, w.d_k, w.d_v, seed=w.seed)
+    bf = lambda a: torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).cuda()
+    f32 = lambda a: torch.from_numpy(a).cuda()
+    args = (bf(x["q"]), bf(x["k"]), bf(x["v"]), w.grid, f32(x["wk_spatial"]),
+            f32(x["wk_temporal"]), f32(x["wv_spatial"]), f32(x["wv_temporal"]), w.H)
+    outs = vda.prep(*args)
+    for _ in range(3):
+        vda.prep(*args, outs=outs)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(K):
+        vda.prep(*args, outs=outs)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / K
+    tok = w.B * w.F * w.N
+    nbytes = 2 * tok * w.H * 2 * (2 * w.d_k + w.d_v)
+    print(f"[bench] vda_prep: {ms:.4f} ms", file=sys.stderr, flush=True)
+    return {"ms": ms, "tokens_per_s": tok / (ms / 1e3), "hbm_gbs_alg": nbytes / (ms / 1e3) / 1e9,
+            "frac_hbm_peak": nbytes / (ms / 1e3) / 1e9 / PEAK_HBM_GBS, "bytes_alg": nbytes}
+
+
 def scan_paths(vda, torch, H, F, dk, dv, chunk, offset, K):
     """Time the frame-by-frame and the chunk-wise scans of one shape on
     synthetic inverses (I + G G^T / d_k)^{-1}, written as operand tiles by the
@@ -423,7 +455,10 @@ def main() -> int:
         print(f"[bench] vda_forward_ex ({rule}, all options): {ms_ex:.4f} ms/step",
               file=sys.stderr, flush=True)
     result["full_operator"] = full
-    # 4. The two scan paths of a chunked window, alone: frame by frame
+    # 4. VDA-Prep (the feature map before the operator) on this workload's
+    #    shape: token-major bf16 projections -> frame-major features.
+    result["prep"] = prep_bench(vda, torch, w, K)
+    # 5. The two scan paths of a chunked window, alone: frame by frame
     #    (vda_state_scan_tiles) and chunk-wise (vda_state_scan_chunked, chunks
     #    of five after one anchor), on this workload's heads and frames and on
     #    the paper's own shard (7 heads per GPU, 100 interior frames).

@@ -182,6 +182,41 @@ int vda_forward_ex_f32(const float* q, const float* k, const float* v,
                        const vda_options* opts, float* out, hipStream_t stream);
 
 /* ------------------------------------------------------------------------- */
+/* VDA-Prep: the linear branch's feature map before the operator              */
+/* ------------------------------------------------------------------------- */
+
+/*
+ * vda_prep -- the feature map of the linear branch (Sec. 2.3; the VDA-Prep
+ * step of Sec. 4) from the QKV projections to the operator's inputs:
+ *     q_out = L2(q),  k_out = L2(SiLU(T_k * S_k * k)),  v_out = SiLU(T_v * S_v * v)
+ * S is a depthwise 5 x 5 spatial filter over each frame's latent grid and T
+ * a depthwise five-tap temporal filter over the frames, both centred
+ * cross-correlations with zero padding at the grid and clip borders:
+ *     (S x)[f][y][x][c] = sum_{i,j<5} w_spatial[c][i*5+j] x[f][y+i-2][x+j-2][c]
+ *     (T s)[f][y][x][c] = sum_{i<5}   w_temporal[c][i]    s[f+i-2][y][x][c]
+ * SiLU(x) = x / (1 + exp(-x)); L2 divides one token of one head by
+ * sqrt(sum of its d squared channels + 1e-6).  The F frames are the clip's
+ * interior frames (anchor rows already removed, Algorithm 1 step 2).
+ *  - q, k [B][F][grid_h*grid_w][H*d_k], v [B][F][grid_h*grid_w][H*d_v]:
+ *    bf16 DEVICE pointers, tokens of a frame in row-major grid order, head h
+ *    owning channels h*d .. h*d+d-1 (the projections' token-major layout).
+ *  - wk_spatial [H*d_k][25], wk_temporal [H*d_k][5], wv_spatial [H*d_v][25],
+ *    wv_temporal [H*d_v][5]: fp32 DEVICE pointers, one filter per channel.
+ *  - q_out, k_out [B*H][F][grid_h*grid_w][d_k], v_out [..][d_v]: bf16 DEVICE
+ *    pointers, the frame-major per-head layout of vda_forward (index b*H+h).
+ * The filters accumulate in fp32; results are rounded to bf16 once.
+ * d_k, d_v in {64, 128}; B, F, grid_h, grid_w, H >= 1.  Tensors 16-byte
+ * aligned, filters 4-byte aligned; no output may overlap an input or
+ * another output.  Errors: VDA_ERR_NULL, VDA_ERR_SIZE, VDA_ERR_UNSUPPORTED,
+ * VDA_ERR_ALIGN, VDA_ERR_OVERLAP, VDA_ERR_HIP.
+ */
+int vda_prep(const void* q, const void* k, const void* v,
+             const float* wk_spatial, const float* wk_temporal,
+             const float* wv_spatial, const float* wv_temporal,
+             int B, int F, int grid_h, int grid_w, int H, int d_k, int d_v,
+             void* q_out, void* k_out, void* v_out, hipStream_t stream);
+
+/* ------------------------------------------------------------------------- */
 /* Stage interface: the same kernels as vda_forward, one step per call, with  */
 /* caller-owned fp32 work buffers (all device pointers, 16-byte aligned).     */
 /* ------------------------------------------------------------------------- */

@@ -571,6 +571,43 @@ int vda_state_scan_chunked(const void* Inv_tiles, const float* B, const float* a
                                                    chunk, offset, work, S_fwd, S_rev, stream));
 }
 
+int vda_prep(const void* q, const void* k, const void* v, const float* wk_spatial,
+             const float* wk_temporal, const float* wv_spatial, const float* wv_temporal, int B,
+             int F, int grid_h, int grid_w, int H, int d_k, int d_v, void* q_out, void* k_out,
+             void* v_out, hipStream_t stream) {
+  if (!q || !k || !v || !wk_spatial || !wk_temporal || !wv_spatial || !wv_temporal || !q_out ||
+      !k_out || !v_out)
+    return VDA_ERR_NULL;
+  if (B < 1 || F < 1 || grid_h < 1 || grid_w < 1 || H < 1) return VDA_ERR_SIZE;
+  if ((d_k != 64 && d_k != 128) || (d_v != 64 && d_v != 128)) return VDA_ERR_UNSUPPORTED;
+  const long long N = (long long)grid_h * grid_w;
+  const long long dmax = d_k > d_v ? d_k : d_v;
+  // Byte offsets within one clip's projections are 32-bit; grids are
+  // one-dimensional.
+  if ((long long)F * N * H * dmax * 2 > 0x7fffffffLL) return VDA_ERR_SIZE;
+  if ((long long)B * H * ((grid_h + 3) / 4) * ((grid_w + 7) / 8) > 0x7fffffffLL ||
+      (long long)B * F * H * N > 0x7fffffffLL)
+    return VDA_ERR_SIZE;
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(q_out, 16) ||
+      !aligned(k_out, 16) || !aligned(v_out, 16) || !aligned(wk_spatial, 4) ||
+      !aligned(wk_temporal, 4) || !aligned(wv_spatial, 4) || !aligned(wv_temporal, 4))
+    return VDA_ERR_ALIGN;
+  const size_t tk = (size_t)B * F * N * H * d_k * 2, tv = (size_t)B * F * N * H * d_v * 2;
+  const Range in[] = {range_of(q, tk), range_of(k, tk), range_of(v, tv),
+                      range_of(wk_spatial, (size_t)H * d_k * 25 * 4),
+                      range_of(wk_temporal, (size_t)H * d_k * 5 * 4),
+                      range_of(wv_spatial, (size_t)H * d_v * 25 * 4),
+                      range_of(wv_temporal, (size_t)H * d_v * 5 * 4)};
+  const Range outs[] = {range_of(q_out, tk), range_of(k_out, tk), range_of(v_out, tv)};
+  for (const Range& o : outs)
+    for (const Range& i : in)
+      if (overlaps(o, i)) return VDA_ERR_OVERLAP;
+  if (overlaps(outs[0], outs[1]) || overlaps(outs[0], outs[2]) || overlaps(outs[1], outs[2]))
+    return VDA_ERR_OVERLAP;
+  return hip_status(vda::launch_prep(q, k, v, wk_spatial, wk_temporal, wv_spatial, wv_temporal, B,
+                                     F, grid_h, grid_w, H, d_k, d_v, q_out, k_out, v_out, stream));
+}
+
 int vda_state_scan_tiles(const void* Inv_tiles, const float* B, int F, int H, int d_k, int d_v,
                          float* S_fwd, float* S_rev, hipStream_t stream) {
   const int st = check_scan(Inv_tiles, B, F, H, d_k, d_v, S_fwd, S_rev);

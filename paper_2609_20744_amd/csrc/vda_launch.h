@@ -77,6 +77,14 @@ hipError_t launch_state_scan_chunked(const void* Inv_tiles, const float* Bm, con
                                      int chunk, int offset, void* work, float* S_fwd,
                                      float* S_rev, hipStream_t stream);
 
+// VDA-Prep: Q' = L2(Q), K' = L2(SiLU(conv_k(K))), V' = SiLU(conv_v(V)) from
+// token-major projections [B][F][gh*gw][H*d] to [B*H][F][gh*gw][d] (bf16;
+// d_k, d_v in {64, 128}).
+hipError_t launch_prep(const void* q, const void* k, const void* v, const float* wks,
+                       const float* wkt, const float* wvs, const float* wvt, int B, int F, int gh,
+                       int gw, int H, int d_k, int d_v, void* q_out, void* k_out, void* v_out,
+                       hipStream_t stream);
+
 // Options of the gather beyond the core (defaults: own frame, no decay).
 struct GatherOptions {
   const float* alpha = nullptr;  // [H][F][d_k] channel decay, or null (1)

@@ -54,6 +54,7 @@ class Workload:
     beta_sigma: float = 1.0
     beta_zero_frac: float = 0.0
     dup_frac: float = 0.0
+    grid: tuple | None = None  # latent grid (rows, cols) of the N tokens, when it has one
     description: str = field(default="", compare=False)
 
     @property
@@ -74,15 +75,15 @@ class Workload:
 # The five workloads the operator is measured and checked on.  The 768p
 # long clip is one GPU's head shard: 48x80 latent grid, 36 interior frames.
 WORKLOADS = {
-    "tiny_f32": Workload("tiny_f32", 1, 2, 4, 64, 64, 64, "f32", 0,
+    "tiny_f32": Workload("tiny_f32", 1, 2, 4, 64, 64, 64, "f32", 0, grid=(8, 8),
                          description="8x8 grid, 4 frames, fp32 storage"),
-    "small_bf16": Workload("small_bf16", 1, 8, 16, 1024, 128, 128, "bf16", 1,
+    "small_bf16": Workload("small_bf16", 1, 8, 16, 1024, 128, 128, "bf16", 1, grid=(32, 32),
                            description="32x32 grid, 16 frames"),
-    "480p_bf16": Workload("480p_bf16", 1, 24, 21, 1560, 128, 128, "bf16", 2,
+    "480p_bf16": Workload("480p_bf16", 1, 24, 21, 1560, 128, 128, "bf16", 2, grid=(30, 52),
                           description="30x52 latent grid, 21 frames"),
-    "768p_bf16": Workload("768p_bf16", 1, 16, 36, 3840, 128, 128, "bf16", 3,
+    "768p_bf16": Workload("768p_bf16", 1, 16, 36, 3840, 128, 128, "bf16", 3, grid=(48, 80),
                           description="48x80 latent grid, 36 frames, 16-head shard"),
-    "ragged_bf16": Workload("ragged_bf16", 2, 12, 64, 2025, 64, 128, "bf16", 7,
+    "ragged_bf16": Workload("ragged_bf16", 2, 12, 64, 2025, 64, 128, "bf16", 7, grid=(45, 45),
                             beta_sigma=2.0, beta_zero_frac=0.25, dup_frac=0.10,
                             description="45x45 grid, 64 frames, zero and near-duplicate writes"),
 }
@@ -229,3 +230,26 @@ def as_float64(x: np.ndarray, dtype: str) -> np.ndarray:
     if dtype == "bf16":
         return bf16_bits_to_f32(x).astype(np.float64)
     return np.asarray(x, dtype=np.float64)
+
+
+def make_prep_inputs(B: int, F: int, grid, H: int, d_k: int, d_v: int, seed: int = 0) -> dict:
+    """Synthetic inputs of the linear branch's feature map (VDA-Prep):
+    token-major projections q, k [B, F, gh*gw, H*d_k], v [B, F, gh*gw,
+    H*d_v] ~ N(0, 1), rounded to bf16 (returned as the bf16 bit patterns,
+    uint16); depthwise filters, fp32: spatial [H*d, 25] ~ N(0, 1/25) and
+    temporal [H*d, 5] ~ N(0, 1/5) for K and for V (so a filtered value has
+    about unit variance), from ``default_rng([seed, 1000 + b])`` per clip and
+    ``default_rng([seed, 999])`` for the filters."""
+    gh, gw = grid
+    N = gh * gw
+    out = {n: np.empty((B, F, N, H * d), np.uint16)
+           for n, d in (("q", d_k), ("k", d_k), ("v", d_v))}
+    for b in range(B):
+        rng = np.random.default_rng([seed, 1000 + b])
+        for n, d in (("q", d_k), ("k", d_k), ("v", d_v)):
+            out[n][b] = f32_to_bf16_bits(rng.standard_normal((F, N, H * d), dtype=np.float32))
+    rng = np.random.default_rng([seed, 999])
+    for n, d in (("k", d_k), ("v", d_v)):
+        out[f"w{n}_spatial"] = (rng.standard_normal((H * d, 25)) / 5.0).astype(np.float32)
+        out[f"w{n}_temporal"] = (rng.standard_normal((H * d, 5)) / np.sqrt(5.0)).astype(np.float32)
+    return out

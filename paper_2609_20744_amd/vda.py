@@ -58,6 +58,7 @@ _SIGNATURES = {
     "vda_state_scan_tiles": (_I, [_P, _P, _I, _I, _I, _I, _P, _P, _P]),
     "vda_state_scan_chunked": (_I, [_P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _P, _P, _P, _P]),
     "vda_state_scan_chunked_workspace": (ctypes.c_size_t, [_I, _I, _I, _I, _I, _I]),
+    "vda_prep": (_I, [_P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _P, _P, _P, _P]),
     "vda_readout": (_I, [_P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _P, _P]),
 }
 
@@ -374,6 +375,40 @@ def state_scan_chunked(Inv_tiles, B, chunk, offset=0, alpha=None, text_state=Non
 def chunked_workspace(F: int, H: int, d_k: int, d_v: int, chunk: int, offset: int = 0) -> int:
     """Bytes of the work buffer of state_scan_chunked."""
     return int(lib.vda_state_scan_chunked_workspace(F, H, d_k, d_v, int(chunk), int(offset)))
+
+
+def prep(q, k, v, grid, wk_spatial, wk_temporal, wv_spatial, wv_temporal, H, outs=None,
+         stream=None):
+    """VDA-Prep (vda_prep): q, k [B, F, N, H*d_k], v [B, F, N, H*d_v] bf16
+    projections with N = grid[0] * grid[1]; filters fp32 wk_spatial
+    [H*d_k, 25] (or [H*d_k, 5, 5]), wk_temporal [H*d_k, 5], likewise for v.
+    Returns (q', k', v') [B*H, F, N, d] bf16 (or fills `outs`)."""
+    torch = _torch()
+    dev = q.device
+    for t, n in ((q, "q"), (k, "k"), (v, "v")):
+        _require(t, n, torch.bfloat16, dev)
+    for t, n in ((wk_spatial, "wk_spatial"), (wk_temporal, "wk_temporal"),
+                 (wv_spatial, "wv_spatial"), (wv_temporal, "wv_temporal")):
+        _require(t, n, torch.float32, dev)
+    B, F, N, Ck = q.shape
+    Cv = v.shape[-1]
+    gh, gw = grid
+    if gh * gw != N or k.shape != q.shape or v.shape[:3] != q.shape[:3]:
+        raise ValueError("q, k, v must be [B, F, grid_h*grid_w, H*d]")
+    if Ck % H or Cv % H:
+        raise ValueError("channels must split into H heads")
+    d_k, d_v = Ck // H, Cv // H
+    if outs is None:
+        outs = (torch.empty((B * H, F, N, d_k), dtype=torch.bfloat16, device=dev),
+                torch.empty((B * H, F, N, d_k), dtype=torch.bfloat16, device=dev),
+                torch.empty((B * H, F, N, d_v), dtype=torch.bfloat16, device=dev))
+    with torch.cuda.device(dev):
+        st = lib.vda_prep(q.data_ptr(), k.data_ptr(), v.data_ptr(), wk_spatial.data_ptr(),
+                          wk_temporal.data_ptr(), wv_spatial.data_ptr(), wv_temporal.data_ptr(),
+                          B, F, gh, gw, H, d_k, d_v, outs[0].data_ptr(), outs[1].data_ptr(),
+                          outs[2].data_ptr(), _stream_ptr(dev, stream))
+    _check(st, "vda_prep")
+    return outs
 
 
 def readout(q, S_fwd, S_rev, gate, d_v=None, out=None, stream=None):

@@ -125,6 +125,21 @@ def test_stage_validation():
               None) == 4
     assert ch(big, 2 * big, None, None, 12, 2, 64, 64, 5, 1, 3 * big, 3 * big, 4 * big, None) == 5
     assert ch(big, 2 * big, None, None, 12, 2, 64, 48, 5, 1, 5 * big, 3 * big, 4 * big, None) == 3
+    pr = L.vda_prep
+    # (q, k, v, wks, wkt, wvs, wvt, B, F, gh, gw, H, d_k, d_v, q_out, k_out, v_out, stream)
+    w = [9 * big, 9 * big + 4096, 9 * big + 8192, 9 * big + 12288]
+    outs = [4 * big, 5 * big, 6 * big]
+    assert pr(None, 2 * big, 3 * big, *w, 1, 4, 6, 8, 2, 128, 128, *outs, None) == 1
+    assert pr(big, 2 * big, 3 * big, *w, 1, 0, 6, 8, 2, 128, 128, *outs, None) == 2
+    assert pr(big, 2 * big, 3 * big, *w, 1, 4, 6, 8, 2, 96, 128, *outs, None) == 3
+    assert pr(big, 2 * big, 3 * big, *w, 1, 4, 6, 8, 2, 128, 32, *outs, None) == 3
+    assert pr(big + 8, 2 * big, 3 * big, *w, 1, 4, 6, 8, 2, 128, 128, *outs, None) == 4
+    assert pr(big, 2 * big, 3 * big, *w, 1, 4, 6, 8, 2, 128, 128, big, 5 * big, 6 * big,
+              None) == 5
+    assert pr(big, 2 * big, 3 * big, *w, 1, 4, 6, 8, 2, 128, 128, 4 * big, 4 * big, 6 * big,
+              None) == 5
+    # one clip's projections beyond 32-bit byte offsets
+    assert pr(big, 2 * big, 3 * big, *w, 1, 4096, 64, 64, 2, 128, 128, *outs, None) == 2
     ws = L.vda_state_scan_chunked_workspace
     # 3 chunks (frames 0-3, 4-8, 9-11) x 2 directions x 2 heads x (M tiles + J)
     assert ws(12, 2, 64, 32, 5, 1) == 3 * 2 * 2 * (64 * 64 * 4 + 32 * 64 * 4)

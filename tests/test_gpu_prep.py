@@ -1,0 +1,125 @@
+"""GPU parity of VDA-Prep (vda_prep), the linear branch's feature map, against
+the fp64 oracle (oracle.vda_prep) through the C ABI.  Inputs are bf16
+projections; outputs are bf16, so the bar is the bf16 rounding of the result
+(2^-9 relative, one half-ulp) on top of fp32 accumulation: rel. max-norm
+error <= 5e-3 per output tensor."""
+import numpy as np
+import pytest
+
+import oracle.vda_oracle as O
+from paper_2609_20744_amd import inputs as I
+from vda_testutil import device_inputs, from_device, oracle_inputs, rel_max_err, tol_for
+
+pytestmark = pytest.mark.gpu
+
+TOL_PREP = 5e-3
+
+
+@pytest.fixture(scope="module")
+def V():
+    import torch
+    assert torch.cuda.is_available(), "the gpu tests need an MI355X"
+    from paper_2609_20744_amd import vda
+    return vda
+
+
+def _log(msg):
+    print(msg, flush=True)
+
+
+def _dev_bf16(bits):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).cuda()
+
+
+def _dev_f32(x):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).cuda()
+
+
+def _run(V, x, grid, H):
+    import torch
+    outs = V.prep(_dev_bf16(x["q"]), _dev_bf16(x["k"]), _dev_bf16(x["v"]), grid,
+                  _dev_f32(x["wk_spatial"]), _dev_f32(x["wk_temporal"]),
+                  _dev_f32(x["wv_spatial"]), _dev_f32(x["wv_temporal"]), H)
+    torch.cuda.synchronize()
+    return [from_device(t) for t in outs]
+
+
+def _oracle(x, grid, H, clips=None):
+    """Oracle prep of each clip, stacked to [B*H, F, N, d]."""
+    B = x["q"].shape[0]
+    res = [[], [], []]
+    C = lambda n: x[n].shape[-1]
+    ws = lambda n: x[f"w{n}_spatial"].astype(np.float64).reshape(C(n), 5, 5)
+    wt = lambda n: x[f"w{n}_temporal"].astype(np.float64)
+    for b in (range(B) if clips is None else clips):
+        f64 = {n: I.bf16_bits_to_f32(x[n][b]).astype(np.float64) for n in ("q", "k", "v")}
+        q, k, v = O.vda_prep(f64["q"], f64["k"], f64["v"], grid, H, ws("k"), wt("k"), ws("v"),
+                             wt("v"))
+        for i, t in enumerate((q, k, v)):
+            res[i].append(t)
+    return [np.concatenate(r) for r in res]
+
+
+@pytest.mark.parametrize("B,F,grid,H,dk,dv", [
+    (1, 7, (5, 9), 2, 128, 128),     # ragged grid against the 4 x 8 tile
+    (2, 3, (8, 16), 3, 64, 128),     # whole tiles, d_k = 64
+    (1, 1, (3, 3), 2, 128, 64),      # one frame: the temporal filter sees only zeros beside it
+    (1, 12, (6, 10), 1, 64, 64),
+])
+def test_prep_parity(V, B, F, grid, H, dk, dv):
+    _log(f"prep B={B} F={F} grid={grid} H={H} dk={dk} dv={dv}")
+    x = I.make_prep_inputs(B, F, grid, H, dk, dv, seed=F + H)
+    got = _run(V, x, grid, H)
+    exp = _oracle(x, grid, H)
+    for name, g, e in zip("qkv", got, exp):
+        err = rel_max_err(g, e)
+        _log(f"  {name}: rel err {err:.2e}")
+        assert err <= TOL_PREP, (name, err)
+
+
+def test_prep_768p_heads_sampled(V):
+    """The 768p latent shape (48 x 80 grid, 36 frames, 16 heads of 128
+    channels) in the launch configuration the benchmark times; the oracle
+    checks every output of two heads (first and last)."""
+    H, F, grid = 16, 36, (48, 80)
+    _log("prep 768p")
+    x = I.make_prep_inputs(1, F, grid, H, 128, 128, seed=3)
+    got = _run(V, x, grid, H)
+    d = 128
+    for h in (0, H - 1):
+        sl = slice(h * d, (h + 1) * d)
+        xs = {n: x[n][:, :, :, sl] for n in ("q", "k", "v")}
+        xs.update({k: v[sl] for k, v in x.items() if k.startswith("w")})
+        exp = _oracle(xs, grid, 1)
+        for name, g, e in zip("qkv", got, exp):
+            err = rel_max_err(g[h], e[0])
+            _log(f"  head {h} {name}: rel err {err:.2e}")
+            assert err <= TOL_PREP, (h, name, err)
+
+
+def test_prep_feeds_forward(V):
+    """vda_prep's outputs are vda_forward's inputs: the composed pass equals
+    the oracle's forward on the oracle's feature map (bf16 bar of the
+    forward)."""
+    import torch
+    B, F, grid, H, d = 2, 6, (6, 8), 2, 64
+    _log("prep -> forward")
+    x = I.make_prep_inputs(B, F, grid, H, d, d, seed=11)
+    q, k, v = V.prep(_dev_bf16(x["q"]), _dev_bf16(x["k"]), _dev_bf16(x["v"]), grid,
+                     _dev_f32(x["wk_spatial"]), _dev_f32(x["wk_temporal"]),
+                     _dev_f32(x["wv_spatial"]), _dev_f32(x["wv_temporal"]), H)
+    rng = np.random.default_rng(5)
+    N = grid[0] * grid[1]
+    beta = (1.0 / (1.0 + np.exp(-rng.standard_normal((B * H, F, N))))).astype(np.float32)
+    gate = (1.0 / (1.0 + np.exp(-rng.standard_normal(B * H)))).astype(np.float32)
+    y = V.forward(q, k, v, _dev_f32(beta), _dev_f32(gate))
+    torch.cuda.synchronize()
+    qo, ko, vo = _oracle(x, grid, H)
+    # the oracle forward consumes the same bf16-rounded features the GPU produced? no: its own
+    # fp64 feature map, so the bar is the forward's bf16 bar plus the prep rounding
+    ref = O.vda_forward(qo, ko, vo, beta.astype(np.float64), gate.astype(np.float64))
+    err = rel_max_err(from_device(y), ref)
+    _log(f"  rel err {err:.2e}")
+    assert err <= 2e-2, err
