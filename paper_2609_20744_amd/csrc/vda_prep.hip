@@ -8,23 +8,29 @@
 // token-major projections [B][F][gh*gw][H*d] (bf16); outputs are frame-major
 // per head, [B*H][F][gh*gw][d] (bf16), the layout the operator reads.
 //
-// Convolution kernel: one workgroup per (clip, head, 4 x 8 tile of the
-// grid) streams through all frames.  Per input frame it copies the tile and
-// its 2-token halo (8 x 12 tokens x d channels) into LDS, double-buffered:
-// the next frame's tile is in flight in registers during this frame's
-// filters.  Wave w owns grid row w of the
-// tile (8 tokens) and each lane two channels (one at d = 64), so a wave
-// moves whole 256-byte token rows and the filter taps of a lane's channels
-// stay in registers.  The spatial filter reads the 5 x 12 input window row
-// by row from LDS.  The temporal filter is a scatter: input frame f adds
+// Convolution kernel: one workgroup of eight waves per (clip, head, 8 x 8
+// tile of the grid) streams through all frames.  Per input frame it copies
+// the tile and its 2-token halo (12 x 12 tokens x d channels) into LDS,
+// expanded to fp32 once, double-buffered: the next frame's tile is in
+// flight in registers during this frame's filters.  Wave w owns grid row w
+// of the tile (8 tokens) and each lane two channels (one at d = 64), so a
+// wave moves whole token rows and the filter taps of a lane's channels stay
+// in registers.  The spatial filter reads the 5 x 12 input window row by
+// row from LDS.  The temporal filter is a scatter: input frame f adds
 // w_t[dt] * S(f) to output frame f - dt + 2, whose running sums sit in a
-// five-slot register ring; output frame f - 2 is then complete and is
-// finished (SiLU, the L2 reduction across the wave for K) and stored.  So
-// every input is read from memory once and every output written once.
+// five-slot register ring indexed by frame mod 5 (the frame loop is
+// unrolled five times so every slot index is a constant); output frame
+// f - 2 is then complete and is finished (SiLU, the L2 reduction across the
+// wave for K) and stored.  Every input is read from memory once per tile
+// that needs it (tiles sharing a halo run on one XCD, so the re-reads hit
+// its L2) and every output is written once.  The work is bound by the fp32
+// FMAs (25 + 5 per output channel).
 //
 // Q kernel: each wave normalises four tokens of one head per pass, a lane
 // holding eight channels (16-byte loads and stores), with the reduction
 // over the 16 lanes of each token.
+#include <type_traits>
+
 #include "vda_common.h"
 #include "vda_launch.h"
 
@@ -32,17 +38,60 @@ namespace vda {
 namespace {
 
 constexpr float kL2Eps = 1e-6f;  // the paper states none
-constexpr int kPTY = 4, kPTX = 8;                    // output tile (rows = waves)
+constexpr int kConvThreads = 512;                    // eight waves, one output row each
+constexpr int kPTY = 8, kPTX = 8;                    // output tile (rows = waves)
 constexpr int kPHY = kPTY + 4, kPHX = kPTX + 4;      // with the 2-token halo
+static_assert(kPTX == 8, "the L2 reduction sums eight tokens per wave row");
 
-__device__ __forceinline__ float silu(float x) { return x / (1.0f + __expf(-x)); }
-
-// Sum over the 64 lanes of a wave (every lane gets the total).
-__device__ __forceinline__ float wave_sum(float x) {
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) x += __shfl_xor(x, m);
-  return x;
+// SiLU with the hardware reciprocal (1 ulp): for x -> -inf, exp(-x)
+// overflows to inf and the result is -0, the limit.
+__device__ __forceinline__ float silu(float x) {
+  return x * __builtin_amdgcn_rcpf(1.0f + __expf(-x));
 }
+
+#define VDA_DPP(v, ctrl) __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), ctrl, 0xf, 0xf, false))
+
+// Sum over all 64 lanes of the two 32-lane halves' and four 16-lane rows'
+// copies: lanes 8 apart by DPP row_ror 8, then the 16- and 32-lane row
+// swaps of gfx950.  A swap of a register with itself leaves one lane's own
+// value in one result and its partner's in the other, so their sum is the
+// pair's sum in every lane.
+__device__ __forceinline__ float sum_lanes_8_apart(float x) {
+  x += VDA_DPP(x, 0x128);  // row_ror 8
+  const uint32_t u = __float_as_uint(x);
+  const auto r16 = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  x = __uint_as_float(r16[0]) + __uint_as_float(r16[1]);
+  const uint32_t w = __float_as_uint(x);
+  const auto r32 = __builtin_amdgcn_permlane32_swap(w, w, false, false);
+  return __uint_as_float(r32[0]) + __uint_as_float(r32[1]);
+}
+
+// Totals over the wave of eight per-token values: v[x] is this lane's part
+// of token x; the result in every lane is the total of token lane % 8.
+// Three halving exchanges (partners lane ^ 1, lane ^ 2, and lane + 4 within
+// each row of 16, which pairs lanes holding the same tokens) leave each lane
+// one token's partial sum; adding lanes 8 apart completes it.
+__device__ __forceinline__ float token_totals8(const float (&v)[8], int lane) {
+  const bool b0 = lane & 1, b1 = lane & 2, b2 = lane & 4;
+  float w[4], u[2];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const float a = v[2 * j] + VDA_DPP(v[2 * j], 0xb1);          // quad_perm [1,0,3,2]
+    const float b = v[2 * j + 1] + VDA_DPP(v[2 * j + 1], 0xb1);
+    w[j] = b0 ? b : a;  // token 2j + b0
+  }
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const float a = w[2 * i] + VDA_DPP(w[2 * i], 0x4e);          // quad_perm [2,3,0,1]
+    const float b = w[2 * i + 1] + VDA_DPP(w[2 * i + 1], 0x4e);
+    u[i] = b1 ? b : a;  // token 4i + 2 b1 + b0
+  }
+  const float a = u[0] + VDA_DPP(u[0], 0x124);                   // row_ror 4
+  const float b = u[1] + VDA_DPP(u[1], 0x124);
+  return sum_lanes_8_apart(b2 ? b : a);  // token lane % 8
+}
+
+#undef VDA_DPP
 
 struct PrepConvArgs {
   const uint16_t* in;  // [B][F][N][H*D] bf16
@@ -53,16 +102,18 @@ struct PrepConvArgs {
 };
 
 template <int D, bool NORM>
-__global__ __launch_bounds__(kThreads, 2)
+__global__ __launch_bounds__(kConvThreads, 1)
 void prep_conv_kernel(PrepConvArgs a) {
   constexpr int CPL = D / 64;            // channels per lane
   constexpr int TOK = kPHY * kPHX;       // tokens of the haloed tile
-  constexpr int CHUNKS = TOK * D * 2 / 16;  // 16-byte pieces of one frame's tile
-  __shared__ __align__(16) uint16_t tile[2][TOK * D];
+  constexpr int CHUNKS = TOK * D * 2 / 16;  // 16-byte bf16 pieces of one frame's tile
+  // Two frames of the haloed tile, expanded to fp32 once when written.
+  __shared__ __align__(16) float tile[2][TOK * D];
 
   const int F = a.F, gh = a.gh, gw = a.gw, H = a.H;
   const int N = gh * gw;
-  unsigned id = blockIdx.x;
+  // Consecutive tiles (x fastest) share halos: keep them on one XCD.
+  unsigned id = xcd_grouped_id(blockIdx.x, gridDim.x);
   const int tx = id % a.tiles_x;
   id /= a.tiles_x;
   const int ty = id % a.tiles_y;
@@ -88,17 +139,18 @@ void prep_conv_kernel(PrepConvArgs a) {
   }
 
   // One input frame's haloed tile: chunk q (16 bytes) of the tile is piece
-  // q % (D / 8) of token q / (D / 8), token (r, s) of the 8 x 12 window at
+  // q % (D / 8) of token q / (D / 8), token (r, s) of the 12 x 12 window at
   // grid (y0 - 2 + r, x0 - 2 + s); tokens off the grid read as zero.  Each
-  // thread moves chunks tid + 256 i, loaded into registers one frame ahead
-  // and written to LDS after the current frame's filters.
-  constexpr int CPT = (CHUNKS + kThreads - 1) / kThreads;  // chunks per thread
+  // thread moves chunks tid + 512 i, loaded into registers one frame ahead
+  // and written to LDS as eight fp32 values after the current frame's
+  // filters.
+  constexpr int CPT = (CHUNKS + kConvThreads - 1) / kConvThreads;  // chunks per thread
   const __amdgpu_buffer_rsrc_t irsrc =
       make_rsrc(a.in + (size_t)b * F * N * C, (uint32_t)((size_t)F * N * C * 2));
   uint32_t coff[CPT];  // byte offset within a frame, or out of range
 #pragma unroll
   for (int i = 0; i < CPT; ++i) {
-    const int q = tid + kThreads * i;
+    const int q = tid + kConvThreads * i;
     const int tok = q / (D / 8), piece = q % (D / 8);
     const int r = tok / kPHX, s = tok % kPHX;
     const int gy = y0 - 2 + r, gx = x0 - 2 + s;
@@ -114,19 +166,26 @@ void prep_conv_kernel(PrepConvArgs a) {
           u32x4, __builtin_amdgcn_raw_buffer_load_b128(
                      irsrc, (int)(coff[i] == kOutOfRange ? kOutOfRange : fb + coff[i]), 0, 0));
   };
-  auto store_frame = [&](uint16_t* dst) {
+  auto store_frame = [&](float* dst) {
 #pragma unroll
     for (int i = 0; i < CPT; ++i) {
-      const int q = tid + kThreads * i;
-      if (CHUNKS % kThreads == 0 || q < CHUNKS) reinterpret_cast<u32x4*>(dst)[q] = stage[i];
+      const int q = tid + kConvThreads * i;
+      if (CHUNKS % kConvThreads == 0 || q < CHUNKS) {
+        const u32x4 w = stage[i];
+        float4* d4 = reinterpret_cast<float4*>(dst + q * 8);
+        d4[0] = make_float4(bf16_lo(w[0]), bf16_hi(w[0]), bf16_lo(w[1]), bf16_hi(w[1]));
+        d4[1] = make_float4(bf16_lo(w[2]), bf16_hi(w[2]), bf16_lo(w[3]), bf16_hi(w[3]));
+      }
     }
   };
 
   // Output tokens of this wave: grid row y0 + wave, columns x0 .. x0 + 7.
   const int oy = y0 + wave;
   uint16_t* obase = a.out + ((size_t)(b * H + h) * F) * N * D;
-  // Running sums of the five pending output frames: after input frame f,
-  // slot s belongs to output frame f - 2 + s.
+  // Running sums of the pending output frames: output frame o lives in
+  // slot o % 5.  Slots start at zero (outputs 0 and 1 take their first
+  // terms by accumulation); the slot of output f + 2 is set, not added to,
+  // by input frame f, since output f - 3 left it one frame earlier.
   float ring[5][kPTX][CPL];
 #pragma unroll
   for (int s = 0; s < 5; ++s)
@@ -135,9 +194,12 @@ void prep_conv_kernel(PrepConvArgs a) {
 #pragma unroll
       for (int c = 0; c < CPL; ++c) ring[s][x][c] = 0.f;
 
-  // Input frame f (buffer f % 2): spatial filter, scattered into the ring;
-  // then output frame f - 2 (slot 0) is complete, and the ring moves on.
-  auto step = [&](int f, const uint16_t* tb) {
+  // Input frame f = f0 + P with f0 a multiple of 5, from buffer f % 2:
+  // spatial filter, then the temporal scatter (frame f adds w_t[dt] S(f)
+  // to output f + 2 - dt); output f - 2 is then complete.
+  auto step = [&](auto phase, int f) {
+    constexpr int P = decltype(phase)::value;
+    const float* tb = tile[f & 1];
     if (f < F) {
       float sp[kPTX][CPL];
 #pragma unroll
@@ -149,13 +211,13 @@ void prep_conv_kernel(PrepConvArgs a) {
         float in[kPHX][CPL];
 #pragma unroll
         for (int s = 0; s < kPHX; ++s) {
-          const uint16_t* p = tb + ((wave + dy) * kPHX + s) * D + lane * CPL;
+          const float* p = tb + ((wave + dy) * kPHX + s) * D + lane * CPL;
           if constexpr (CPL == 2) {
-            const uint32_t w2 = *reinterpret_cast<const uint32_t*>(p);
-            in[s][0] = bf16_lo(w2);
-            in[s][1] = bf16_hi(w2);
+            const float2 v2 = *reinterpret_cast<const float2*>(p);
+            in[s][0] = v2.x;
+            in[s][1] = v2.y;
           } else {
-            in[s][0] = __uint_as_float((uint32_t)*p << 16);
+            in[s][0] = *p;
           }
         }
 #pragma unroll
@@ -165,69 +227,73 @@ void prep_conv_kernel(PrepConvArgs a) {
 #pragma unroll
             for (int c = 0; c < CPL; ++c) sp[x][c] = fmaf(wsp[c][dy * 5 + dx], in[x + dx][c], sp[x][c]);
       }
-      // Frame f feeds output frame f + 2 - dt: slot 4 - dt.
 #pragma unroll
-      for (int dt = 0; dt < 5; ++dt)
-#pragma unroll
-        for (int x = 0; x < kPTX; ++x)
-#pragma unroll
-          for (int c = 0; c < CPL; ++c)
-            ring[4 - dt][x][c] = fmaf(wtp[c][dt], sp[x][c], ring[4 - dt][x][c]);
-    }
-    const int o = f - 2;
-    if (o >= 0 && o < F) {
-      float ssq[kPTX];
-#pragma unroll
-      for (int x = 0; x < kPTX; ++x) {
-        ssq[x] = 0.f;
+      for (int x = 0; x < kPTX; ++x)
 #pragma unroll
         for (int c = 0; c < CPL; ++c) {
-          const float y = silu(ring[0][x][c]);
-          ring[0][x][c] = y;
-          ssq[x] = fmaf(y, y, ssq[x]);
+          ring[(P + 2) % 5][x][c] = wtp[c][0] * sp[x][c];
+#pragma unroll
+          for (int dt = 1; dt < 5; ++dt)
+            ring[(P + 2 - dt + 5) % 5][x][c] = fmaf(wtp[c][dt], sp[x][c], ring[(P + 2 - dt + 5) % 5][x][c]);
+        }
+    }
+    const int o = f - 2;
+    constexpr int OS = (P + 3) % 5;  // slot of output f - 2
+    if (o >= 0 && o < F) {
+      float y[kPTX][CPL], scale[kPTX];
+#pragma unroll
+      for (int x = 0; x < kPTX; ++x) {
+        scale[x] = 0.f;
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) {
+          y[x][c] = silu(ring[OS][x][c]);
+          scale[x] = fmaf(y[x][c], y[x][c], scale[x]);
         }
       }
       if constexpr (NORM) {
+        // Lane x holds token x's 1 / sqrt(|y|^2 + eps); broadcast all eight.
+        const float own = rsqrtf(token_totals8(scale, lane) + kL2Eps);
 #pragma unroll
-        for (int x = 0; x < kPTX; ++x) ssq[x] = rsqrtf(wave_sum(ssq[x]) + kL2Eps);
+        for (int x = 0; x < kPTX; ++x)
+          scale[x] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(own), x));
+      } else {
+#pragma unroll
+        for (int x = 0; x < kPTX; ++x) scale[x] = 1.0f;
       }
       if (oy < gh) {
 #pragma unroll
         for (int x = 0; x < kPTX; ++x) {
           if (x0 + x < gw) {
             uint16_t* dst = obase + ((size_t)o * N + oy * gw + x0 + x) * D + lane * CPL;
-            const float sc = NORM ? ssq[x] : 1.0f;
             if constexpr (CPL == 2)
-              *reinterpret_cast<uint32_t*>(dst) = pack_bf16x2(ring[0][x][0] * sc, ring[0][x][1] * sc);
+              *reinterpret_cast<uint32_t*>(dst) = pack_bf16x2(y[x][0] * scale[x], y[x][1] * scale[x]);
             else
-              *dst = (uint16_t)(pack_bf16x2(ring[0][x][0] * sc, 0.f) & 0xffffu);
+              *dst = (uint16_t)(pack_bf16x2(y[x][0] * scale[x], 0.f) & 0xffffu);
           }
         }
       }
     }
-#pragma unroll
-    for (int s = 0; s < 4; ++s)
-#pragma unroll
-      for (int x = 0; x < kPTX; ++x)
-#pragma unroll
-        for (int c = 0; c < CPL; ++c) ring[s][x][c] = ring[s + 1][x][c];
-#pragma unroll
-    for (int x = 0; x < kPTX; ++x)
-#pragma unroll
-      for (int c = 0; c < CPL; ++c) ring[4][x][c] = 0.f;
+  };
+  // One frame: the next frame's tile is in flight during this frame's
+  // filters and is written to the other buffer (read last one frame ago).
+  auto frame = [&](auto phase, int f) {
+    if (f >= F + 2) return;
+    if (f + 1 < F) load_frame(f + 1);
+    step(phase, f);
+    if (f + 1 < F) store_frame(tile[(f + 1) & 1]);
+    lds_barrier();  // next tile complete; this tile's reads done
   };
 
-  // Frame 0's tile; then each frame loads the next one during its filters
-  // and writes it to the other buffer (read last one frame ago).  Two more
-  // steps than frames flush the last two outputs.
   load_frame(0);
   store_frame(tile[0]);
   lds_barrier();
-  for (int f = 0; f < F + 2; ++f) {
-    if (f + 1 < F) load_frame(f + 1);  // in flight during this frame's filters
-    step(f, tile[f & 1]);
-    if (f + 1 < F) store_frame(tile[(f + 1) & 1]);
-    lds_barrier();  // next tile complete; this tile's reads done
+  // Two more frames than inputs flush the last two outputs.
+  for (int f0 = 0; f0 < F + 2; f0 += 5) {
+    frame(std::integral_constant<int, 0>{}, f0);
+    frame(std::integral_constant<int, 1>{}, f0 + 1);
+    frame(std::integral_constant<int, 2>{}, f0 + 2);
+    frame(std::integral_constant<int, 3>{}, f0 + 3);
+    frame(std::integral_constant<int, 4>{}, f0 + 4);
   }
 }
 
@@ -286,7 +352,7 @@ hipError_t launch_conv_t(const PrepConvArgs& a0, int B, hipStream_t stream) {
   a.tiles_y = (a.gh + kPTY - 1) / kPTY;
   a.tiles_x = (a.gw + kPTX - 1) / kPTX;
   const long long nwg = (long long)B * a.H * a.tiles_y * a.tiles_x;
-  hipLaunchKernelGGL((prep_conv_kernel<D, NORM>), dim3((unsigned)nwg), dim3(kThreads), 0, stream, a);
+  hipLaunchKernelGGL((prep_conv_kernel<D, NORM>), dim3((unsigned)nwg), dim3(kConvThreads), 0, stream, a);
   return hipGetLastError();
 }
 
