@@ -64,13 +64,24 @@ def kernel_bytes(w, heads=None):
     }
 
 
+def prep_kernel_bytes(w):
+    """Algorithmic HBM bytes per launch of the VDA-Prep kernels: each reads
+    its bf16 projection once and writes the bf16 features once.  The K and V
+    convolutions are two launches of one kernel, so theirs is the mean."""
+    tok_heads = w.B * w.F * w.N * w.H
+    return {"prep_conv": tok_heads * 2 * 2 * (w.d_k + w.d_v) // 2,
+            "prep_qnorm": tok_heads * 2 * 2 * w.d_k}
+
+
 # Kernel of each stage, and the sources whose change makes counters taken
 # on it stale.
 KERNEL_OF = {"frame_stats": "stats_bf16_kernel", "frame_inverse": "inverse_kernel",
-             "state_scan": "scan_tiled_kernel", "readout": "readout_bf16_kernel"}
+             "state_scan": "scan_tiled_kernel", "readout": "readout_bf16_kernel",
+             "prep_conv": "prep_conv_kernel", "prep_qnorm": "prep_qnorm_kernel"}
 SOURCE_OF = {"frame_stats": ("vda_stats.hip",),
              "frame_inverse": ("vda_inverse.hip", "vda_inverse_body.h"),
-             "state_scan": ("vda_scan_tiled.hip",), "readout": ("vda_readout.hip",)}
+             "state_scan": ("vda_scan_tiled.hip",), "readout": ("vda_readout.hip",),
+             "prep_conv": ("vda_prep.hip",), "prep_qnorm": ("vda_prep.hip",)}
 
 
 def source_hash(stage: str) -> str:
@@ -129,7 +140,7 @@ def pmc_summary(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, copy_gib, 
     f_write = copy_bytes / load(copy_write_dir)["copy"]
     fetch, write = load(fetch_dir), load(write_dir)
     w = __import__("paper_2609_20744_amd.inputs", fromlist=["WORKLOADS"]).WORKLOADS[workload]
-    kb = kernel_bytes(w)
+    kb = {**kernel_bytes(w), **prep_kernel_bytes(w)}
     kernels = {}
     for stage, kname in KERNEL_OF.items():
         if kname not in fetch or kname not in write:
