@@ -41,50 +41,79 @@ struct TiledDims {
   static constexpr int NG = DK / (16 * VW);    // accesses per thread in the row-wise phase
 };
 
-// Matrix-core phase of one step for wave W: xs_next = x Inv_t for this
-// wave's output slices nb = W, W + 4, ..., with x from the bf16 hi / lo
+// One of this wave's tile loads: piece i of its NBW * KB * 2 pieces
+// (slice m = i / (2 KB), k step (i / 2) % KB, plane i % 2) of the tiles at
+// byte offset fbase of the tile buffer, into register slot t.
+template <int DK>
+__device__ __forceinline__ void load_tile_piece(
+    int i, u32x4 (&t)[TiledDims<DK>::NBW][TiledDims<DK>::KB][2],
+    const uint32_t (&toff)[TiledDims<DK>::NBW][TiledDims<DK>::KB][2],
+    __amdgpu_buffer_rsrc_t trsrc, uint32_t fbase) {
+  constexpr int KB = TiledDims<DK>::KB;
+  const int m = i / (2 * KB), ks = (i / 2) % KB, p = i % 2;
+  const uint32_t o = toff[m][ks][p];
+  t[m][ks][p] = __builtin_bit_cast(
+      u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                 trsrc, (int)(o == kOutOfRange ? kOutOfRange : fbase + o), 0, 0));
+}
+
+// Matrix-core phase of one step for wave w: xs_next = x Inv_t for this
+// wave's output slices nb = w, w + 4, ..., with x from the bf16 hi / lo
 // planes and Inv_t from the register tiles t[m][ks][plane].  Even and odd k
-// steps accumulate separately (two shorter dependency chains).
-template <int DK, int W>
+// steps accumulate separately (two shorter dependency chains).  After each
+// k step's three products the wave issues two of the loads that fill
+// another ring slot (tn) with the tiles of a later step (byte offset
+// `next`), so the loads stream out between the products rather than in one
+// burst that would stall the wave at issue.  (Issuing the products of all
+// pairs term by term, with a separate accumulator per pair, measured slower:
+// the phase is bound by the loads' issue, not by the products' latency.)
+// The wave index is a run-time (scalar) value: one code path for all waves,
+// so the compiler's wait-count bookkeeping sees no merging branches and
+// keeps its waits partial.
+template <int DK>
 __device__ __forceinline__ void tiled_mfma_phase(
     const uint16_t* __restrict__ xhi, const uint16_t* __restrict__ xlo,
-    float* __restrict__ xs_next,
-    const u32x4 (&t)[TiledDims<DK>::NBW][TiledDims<DK>::KB][2], int li, int lg) {
+    float* __restrict__ xs_next, const u32x4 (&t)[TiledDims<DK>::NBW][TiledDims<DK>::KB][2],
+    u32x4 (&tn)[TiledDims<DK>::NBW][TiledDims<DK>::KB][2],
+    const uint32_t (&toff)[TiledDims<DK>::NBW][TiledDims<DK>::KB][2],
+    __amdgpu_buffer_rsrc_t trsrc, uint32_t next, int wave, int li, int lg) {
   using D = TiledDims<DK>;
-  if constexpr (W >= D::NB) {
-    return;  // d_k = 32: two slices, waves 2 and 3 idle
-  } else {
-    // A-operand: row li of the block at k = 32 ks + 4 lg + e, 32 ks + 16 + 4 lg + e.
-    bf16x8 ahi[D::KB], alo[D::KB];
+  constexpr int NBW = D::NBW, KB = D::KB;
+  static_assert(D::NB % 4 == 0 || D::NB < 4, "slices are dealt out to four waves");
+  if (D::NB < 4 && wave >= D::NB) return;  // d_k = 32: two slices, waves 2 and 3 idle
+  // A-operand: row li of the block at k = 32 ks + 4 lg + e, 32 ks + 16 + 4 lg + e.
+  bf16x8 ahi[KB], alo[KB];
 #pragma unroll
-    for (int ks = 0; ks < D::KB; ++ks) {
-      const int o = li * D::PLD + 32 * ks + 4 * lg;
-      const u32x2 h0 = *reinterpret_cast<const u32x2*>(&xhi[o]);
-      const u32x2 h1 = *reinterpret_cast<const u32x2*>(&xhi[o + 16]);
-      const u32x2 l0 = *reinterpret_cast<const u32x2*>(&xlo[o]);
-      const u32x2 l1 = *reinterpret_cast<const u32x2*>(&xlo[o + 16]);
-      ahi[ks] = __builtin_bit_cast(bf16x8, u32x4{h0[0], h0[1], h1[0], h1[1]});
-      alo[ks] = __builtin_bit_cast(bf16x8, u32x4{l0[0], l0[1], l1[0], l1[1]});
+  for (int ks = 0; ks < KB; ++ks) {
+    const int o = li * D::PLD + 32 * ks + 4 * lg;
+    const u32x2 h0 = *reinterpret_cast<const u32x2*>(&xhi[o]);
+    const u32x2 h1 = *reinterpret_cast<const u32x2*>(&xhi[o + 16]);
+    const u32x2 l0 = *reinterpret_cast<const u32x2*>(&xlo[o]);
+    const u32x2 l1 = *reinterpret_cast<const u32x2*>(&xlo[o + 16]);
+    ahi[ks] = __builtin_bit_cast(bf16x8, u32x4{h0[0], h0[1], h1[0], h1[1]});
+    alo[ks] = __builtin_bit_cast(bf16x8, u32x4{l0[0], l0[1], l1[0], l1[1]});
+  }
+#pragma unroll
+  for (int m = 0; m < NBW; ++m) {
+    const int nb = wave + 4 * m;
+    floatx4 acc[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
+#pragma unroll
+    for (int ks = 0; ks < KB; ++ks) {
+      const bf16x8 bhi = __builtin_bit_cast(bf16x8, t[m][ks][0]);
+      const bf16x8 blo = __builtin_bit_cast(bf16x8, t[m][ks][1]);
+      floatx4& a = acc[ks & 1];
+      a = __builtin_amdgcn_mfma_f32_16x16x32_bf16(alo[ks], bhi, a, 0, 0, 0);
+      a = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi[ks], blo, a, 0, 0, 0);
+      a = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi[ks], bhi, a, 0, 0, 0);
+      const int piece = 2 * (m * KB + ks);  // this wave's pieces in (slice, k step, plane) order
+      load_tile_piece<DK>(piece, tn, toff, trsrc, next);
+      load_tile_piece<DK>(piece + 1, tn, toff, trsrc, next);
+      __builtin_amdgcn_sched_group_barrier(0x008, 3, 0);  // the three products
+      __builtin_amdgcn_sched_group_barrier(0x020, 2, 0);  // then two loads of the refill
     }
 #pragma unroll
-    for (int m = 0; m < D::NBW; ++m) {
-      const int nb = W + 4 * m;
-      if (nb < D::NB) {
-        floatx4 acc[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
-#pragma unroll
-        for (int ks = 0; ks < D::KB; ++ks) {
-          const bf16x8 bhi = __builtin_bit_cast(bf16x8, t[m][ks][0]);
-          const bf16x8 blo = __builtin_bit_cast(bf16x8, t[m][ks][1]);
-          floatx4& a = acc[ks & 1];
-          a = __builtin_amdgcn_mfma_f32_16x16x32_bf16(alo[ks], bhi, a, 0, 0, 0);
-          a = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi[ks], blo, a, 0, 0, 0);
-          a = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi[ks], bhi, a, 0, 0, 0);
-        }
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          xs_next[(lg * 4 + i) * D::XLD + nb * 16 + li] = acc[0][i] + acc[1][i];
-      }
-    }
+    for (int i = 0; i < 4; ++i)
+      xs_next[(lg * 4 + i) * D::XLD + nb * 16 + li] = acc[0][i] + acc[1][i];
   }
 }
 
@@ -198,12 +227,13 @@ void scan_tiled_kernel(TiledScanArgs a) {
     return frame_of(step);
   };
 
-  // Two-frame register ring, as separately named arrays (compile-time
-  // indices only).
-  u32x4 t0[NBW][KB][2], t1[NBW][KB][2];
-  float bs0[NG][VW], bs1[NG][VW];
-  u32x4 al0, al1;  // alpha_t, columns 4 tid .. 4 tid + 3 (threads tid < DK / 4)
-  auto load_step = [&](int step, u32x4 (&t)[NBW][KB][2], float (&bb)[NG][VW], u32x4& al) {
+  // Three-slot register ring, as separately named arrays (compile-time
+  // indices only): step s reads slot s % 3 while the loads of step s + 2
+  // fill slot (s + 2) % 3, which step s - 1 has released.
+  u32x4 t0[NBW][KB][2], t1[NBW][KB][2], t2[NBW][KB][2];
+  float bs0[NG][VW], bs1[NG][VW], bs2[NG][VW];
+  u32x4 al0, al1, al2;  // alpha_t, columns 4 tid .. 4 tid + 3 (threads tid < DK / 4)
+  auto load_add = [&](int step, float (&bb)[NG][VW], u32x4& al) {
     const int frame = frame_of(step);
     const int ai = add_of(step);
     // B rows first (they are needed earlier in the step than the tiles),
@@ -229,7 +259,10 @@ void scan_tiled_kernel(TiledScanArgs a) {
       const uint32_t off = tid < DK / 4 ? (uint32_t)(frame * DK + 4 * tid) * 4u : kOutOfRange;
       al = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(arsrc, (int)off, 0, 0));
     }
-    const uint32_t fbase = (uint32_t)frame * (uint32_t)(DK * DK * 4);
+  };
+  auto tile_base = [&](int step) { return (uint32_t)frame_of(step) * (uint32_t)(DK * DK * 4); };
+  auto load_tiles = [&](int step, u32x4 (&t)[NBW][KB][2]) {
+    const uint32_t fbase = tile_base(step);
 #pragma unroll
     for (int m = 0; m < NBW; ++m)
 #pragma unroll
@@ -244,12 +277,21 @@ void scan_tiled_kernel(TiledScanArgs a) {
   };
 
   int cur = 0;
-  auto step_body = [&](int step, u32x4 (&t)[NBW][KB][2], float (&bb)[NG][VW], u32x4& al,
-                       const u32x4& al_next) {
+  // Step `step` on slot (t, bb); (tn, bn, aln) is the slot the step fills
+  // with step + 2 (B and alpha at its start, the tiles between its
+  // products; past the end: a clamped, unused step), always, so no
+  // branch hides the loads from the wait-count bookkeeping; al_next is the
+  // alpha of step + 1, loaded a step ago.
+  auto step_body = [&](int step, const u32x4 (&t)[NBW][KB][2], const float (&bb)[NG][VW],
+                       const u32x4& al_next, u32x4 (&tn)[NBW][KB][2], float (&bn)[NG][VW],
+                       u32x4& aln) {
     // Frame whose entering state this step stores (-1 for a padded step
     // past the end: the stores go out of the buffer's range).
     const int sf = store_frame(step);
     lds_barrier();  // xs[cur] holds the entering state; last step's plane reads are done
+    const int refill = min(step + 2, nsteps - 1);
+    const uint32_t next = tile_base(refill);
+    load_add(refill, bn, aln);
     {
 #pragma unroll
       for (int g = 0; g < NG; ++g) {
@@ -308,34 +350,29 @@ void scan_tiled_kernel(TiledScanArgs a) {
     if constexpr (DECAY) {
       if (tid < DK / 4) reinterpret_cast<u32x4*>(alds)[tid] = al_next;
     }
-    switch (wave) {  // wave-uniform
-      case 0: tiled_mfma_phase<DK, 0>(xsp[0], xsp[1], xs[cur ^ 1], t, li, lg); break;
-      case 1: tiled_mfma_phase<DK, 1>(xsp[0], xsp[1], xs[cur ^ 1], t, li, lg); break;
-      case 2: tiled_mfma_phase<DK, 2>(xsp[0], xsp[1], xs[cur ^ 1], t, li, lg); break;
-      default: tiled_mfma_phase<DK, 3>(xsp[0], xsp[1], xs[cur ^ 1], t, li, lg); break;
-    }
-    // Refill this slot with the frame two steps on, once its tiles are
-    // consumed (past the end: a clamped, unused frame), always, so no branch
-    // hides the loads from the wait-count bookkeeping.
-    load_step(min(step + 2, nsteps - 1), t, bb, al);
+    // The products, with the second half of the refill between them.
+    tiled_mfma_phase<DK>(xsp[0], xsp[1], xs[cur ^ 1], t, tn, toff, trsrc, next, wave, li, lg);
     cur ^= 1;
   };
 
   // Issue the ring in slot order (pinned against rescheduling) so slot 0 is
   // the oldest load on loop entry.
-  load_step(0, t0, bs0, al0);
+  load_add(0, bs0, al0);
+  load_tiles(0, t0);
   __builtin_amdgcn_sched_barrier(0);
-  load_step(min(1, nsteps - 1), t1, bs1, al1);
+  load_add(min(1, nsteps - 1), bs1, al1);
+  load_tiles(min(1, nsteps - 1), t1);
   __builtin_amdgcn_sched_barrier(0);
   if constexpr (DECAY) {  // alpha of step 0
     if (tid < DK / 4) reinterpret_cast<u32x4*>(alds)[tid] = al0;
   }
-  // The step count is padded to an even number; a padded step
+  // The step count is padded to a multiple of three; a padded step
   // (step >= nsteps) reads a clamped matrix and stores nothing, so the loop
   // body has no early exit.
-  for (int step0 = 0; step0 < nsteps; step0 += 2) {
-    step_body(step0, t0, bs0, al0, al1);
-    step_body(step0 + 1, t1, bs1, al1, al0);
+  for (int step0 = 0; step0 < nsteps; step0 += 3) {
+    step_body(step0, t0, bs0, al1, t2, bs2, al2);
+    step_body(step0 + 1, t1, bs1, al2, t0, bs0, al0);
+    step_body(step0 + 2, t2, bs2, al0, t1, bs1, al1);
   }
 }
 
