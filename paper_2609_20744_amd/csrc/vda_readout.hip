@@ -69,8 +69,6 @@ void readout_bf16_kernel(const uint16_t* __restrict__ Q, const float* __restrict
   const unsigned L = xcd_grouped_id(blockIdx.x, nwg);
   const unsigned fh = L / chunks;
   const int chunk = L % chunks;
-  const int n_begin = chunk * tokens_per_chunk;
-  const int n_end = min(N, n_begin + tokens_per_chunk);
   const float g = gate[fh / F];
 
   const int tid = threadIdx.x;
@@ -117,36 +115,41 @@ void readout_bf16_kernel(const uint16_t* __restrict__ Q, const float* __restrict
   const uint16_t* qbase = Q + (size_t)fh * N * DK;
   uint16_t* obase = out + (size_t)fh * N * DV;
 
-  // Each wave owns every fourth 16-token group; the queries of its next
-  // kQ groups are in flight in a register ring (slot d: group n0 + 64*d).
-  // Rows past the range are clamped onto its last row (always valid memory);
-  // their outputs are dropped by the range-checked stores, so loads and
-  // stores need no branches.
+  // The frame's tokens go in 64-token super-groups, dealt out to its
+  // `chunks` workgroups in turn (super-group c, c + chunks, ...), so the
+  // workgroups of one frame sweep it together and the device streams a
+  // compact address window; within a super-group wave w takes the 16-token
+  // group at 16 w.  The queries of a wave's next kQ groups are in flight in
+  // a register ring (slot d: group n0 + S*d, S = 64 * chunks tokens apart).
+  // Rows past the frame are clamped onto its last row (always valid
+  // memory); their outputs are dropped by the range-checked stores, so
+  // loads and stores need no branches.
   constexpr int kQ = 3;
+  const int S = 64 * chunks;
   uint4 qr[kQ][KB];
   auto load_q = [&](int nq, uint4 (&qv)[KB]) {
-    const int row = min(nq + li, n_end - 1);
+    const int row = min(nq + li, N - 1);
 #pragma unroll
     for (int kb = 0; kb < KB; ++kb)
       qv[kb] = *reinterpret_cast<const uint4*>(qbase + (size_t)row * DK + kb * 32 + lg * 8);
   };
-  const __amdgpu_buffer_rsrc_t orsrc = make_rsrc(obase, (uint32_t)n_end * DV * 2u);
+  const __amdgpu_buffer_rsrc_t orsrc = make_rsrc(obase, (uint32_t)N * DV * 2u);
 
-  const int n_first = n_begin + wave * 16;
-  if (n_first >= n_end) return;
+  const int n_first = chunk * 64 + wave * 16;
+  if (n_first >= N) return;
   // Issue the ring in slot order (the scheduler must not reorder it), so on
   // loop entry slot 0 is the oldest load and waits stay partial.
 #pragma unroll
   for (int d = 0; d < kQ; ++d) {
-    load_q(n_first + 64 * d, qr[d]);
+    load_q(n_first + S * d, qr[d]);
     __builtin_amdgcn_sched_barrier(0);
   }
-  for (int n0 = n_first; n0 < n_end; n0 += 64 * kQ) {
+  for (int n0 = n_first; n0 < N; n0 += S * kQ) {
 #pragma unroll
     for (int d = 0; d < kQ; ++d) {
-      // Groups past the range (at most kQ-1 per wave) run on clamped rows;
+      // Groups past the frame (at most kQ-1 per wave) run on clamped rows;
       // their stores fall outside the buffer range and are dropped.
-      const int ng = n0 + 64 * d;
+      const int ng = n0 + S * d;
       floatx4 acc[MB];
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb) acc[mb] = floatx4{0.f, 0.f, 0.f, 0.f};
@@ -157,7 +160,7 @@ void readout_bf16_kernel(const uint16_t* __restrict__ Q, const float* __restrict
         for (int mb = 0; mb < MB; ++mb)
           acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sop[mb][kb], qop, acc[mb], 0, 0, 0);
       }
-      load_q(ng + 64 * kQ, qr[d]);
+      load_q(ng + S * kQ, qr[d]);
       // lane holds o[token ng + li][mb*16 + 4*lg + i]
       float ss = 0.f;
 #pragma unroll
