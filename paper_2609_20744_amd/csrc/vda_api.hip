@@ -198,17 +198,17 @@ Workspace workspace_layout(int F, int H, int d_k, int d_v, vda::SplitPlan plan) 
 
 // Whether the chunk-wise scans beat the frame-by-frame scan for a chunked
 // window, by a cost model fitted to measurements on MI355X at d = 128 (the
-// frame scan ~1.4 us per frame; the compose launch ~(6 * chunk + 14) us per
-// round of 2 * H * C workgroups over the compute units; the chunk-sequence
-// scan ~2.4 us per chunk).  Measured: 16 heads x 36 frames, 54 us frame by
-// frame against 61 us chunk-wise; 7 heads x 100 frames, 125 us against
-// 99 us (chunks of five after one anchor).
+// frame scan ~0.95 us per frame plus ~7 us; the compose launch
+// ~(5 * chunk + 13) us per round of 2 * H * C workgroups over the compute
+// units; the chunk-sequence scan ~2.2 us per chunk).  Measured: 16 heads x
+// 36 frames, 43 us frame by frame against 56 us chunk-wise; 7 heads x 100
+// frames, 98 us against 91 us (chunks of five after one anchor).
 bool chunked_scan_pays(int F, int H, int chunk, int offset) {
   const int C = vda::chunk_count(F, chunk, offset);
   if (C < 2) return false;
   const double rounds = std::max(1.0, 2.0 * H * C / (double)current_device_cus());
-  const double chunked_us = rounds * (6.0 * chunk + 14.0) + 2.4 * C;
-  const double frame_us = 1.4 * F;
+  const double chunked_us = rounds * (5.0 * chunk + 13.0) + 2.2 * C;
+  const double frame_us = 0.95 * F + 7.0;
   return chunked_us < frame_us;
 }
 
