@@ -345,7 +345,14 @@ int forward_impl(bool is_f32, const void* q, const void* k, const void* v, const
   so.text_state = ts_x;
   so.tokens = N;
   if (e == hipSuccess) {
-    if (chunked)
+    if (frozen && !is_f32) {
+      // bf16 storage: the frozen maps as operand tiles (in place over A_t),
+      // then the tiled scan in its map form.
+      e = vda::launch_frozen_tiles(A_part, alpha_x, F, H, pk, N, stream);
+      if (e == hipSuccess)
+        e = vda::launch_frozen_scan_tiled(A_part, B_part, ts_x, F, H, pk, pv, N, S_fwd, S_rev,
+                                          stream);
+    } else if (chunked)
       e = vda::launch_state_scan_chunked(Inv, B_part, alpha_x, ts_x, F, H, pk, pv, o.window_chunk,
                                          o.window_offset, chunk_work, S_fwd, S_rev, stream);
     else if (tiled)

@@ -52,6 +52,17 @@ hipError_t launch_state_scan(bool exact_f32, const float* Mat, const float* Bm, 
                              int d_k, int d_v, const ScanOptions& o, float* S_fwd, float* S_rev,
                              hipStream_t stream);
 
+// The frozen rule (Eq. 3c with the 1/sqrt(U) scaling) on the tiled scan:
+// launch_frozen_tiles overwrites each A_t [H][F][d_k][d_k] in place with the
+// operand tiles of M_t = Diag(alpha_t)(I - A_t / U) (alpha null: 1), and
+// launch_frozen_scan_tiled runs x <- x M_t + B_t / sqrt(U) in both
+// directions from S_T / 2 (or zero), storing every frame's entering state.
+hipError_t launch_frozen_tiles(float* A, const float* alpha, int F, int H, int d_k, int tokens,
+                               hipStream_t stream);
+hipError_t launch_frozen_scan_tiled(const void* M_tiles, const float* Bm, const float* text_state,
+                                    int F, int H, int d_k, int d_v, int tokens, float* S_fwd,
+                                    float* S_rev, hipStream_t stream);
+
 // Steps a3/a4 for the joint rule on the bf16 storage path, with Inv_t given
 // as split-bf16 operand tiles (operand_tile_offset); alpha and the text
 // state of `o` apply, `o.frozen` must be false.

@@ -118,9 +118,13 @@ __device__ __forceinline__ void tiled_mfma_phase(
 }
 
 // Arguments of the tiled scan.  Frame scans: tiles = Inv_t tiles [H][F],
-// add = B [H][F][d_v][d_k].  Chunk scans (CHUNKED): tiles = M_c tiles
-// [H][2][C], add = J_c [H][2][C][d_v][d_k], over the C chunks of the window
-// grid (chunk, offset).
+// add = B [H][F][d_v][d_k].  Map scans (CHUNKED), x <- x M + add_scale J:
+// chunk scans take tiles = M_c tiles [H][2][C] and add = J_c
+// [H][2][C][d_v][d_k] over the C chunks of the window grid (chunk, offset),
+// one set per direction (mats_per_head = 2C, dir_stride = C); the frozen
+// rule takes per-frame maps M_t = Diag(alpha_t)(I - A_t / U) and J_t = B_t
+// scaled by 1 / sqrt(U), shared by both directions (chunks of one frame,
+// mats_per_head = F, dir_stride = 0).
 struct TiledScanArgs {
   const uint16_t* tiles;
   const float* add;
@@ -129,6 +133,8 @@ struct TiledScanArgs {
   int F, DV;
   unsigned nwg;
   int chunk, offset, C;
+  int mats_per_head, dir_stride;
+  float add_scale;
   float* S_fwd;
   float* S_rev;
 };
@@ -189,7 +195,8 @@ void scan_tiled_kernel(TiledScanArgs a) {
   // Steps: frames, or chunks; matrices (tiles) and additive terms of this
   // chain, range-checked (indices outside read as zero).
   const int nsteps = CHUNKED ? C : F;
-  const size_t chain_mats = CHUNKED ? ((size_t)hb * 2 + dir) * C : (size_t)hb * F;
+  const size_t chain_mats =
+      CHUNKED ? (size_t)hb * a.mats_per_head + (size_t)dir * a.dir_stride : (size_t)hb * F;
   const __amdgpu_buffer_rsrc_t brsrc =
       make_rsrc(a.add + chain_mats * mat_b, (uint32_t)(nsteps * mat_b * sizeof(float)));
   const __amdgpu_buffer_rsrc_t arsrc =
@@ -310,7 +317,7 @@ void scan_tiled_kernel(TiledScanArgs a) {
         }
         if constexpr (CHUNKED) {  // J of the previous chunk, after its product
 #pragma unroll
-          for (int c = 0; c < VW; ++c) v[c] += bb[g][c];
+          for (int c = 0; c < VW; ++c) v[c] = fmaf(bb[g][c], a.add_scale, v[c]);
         }
         if constexpr (VW == 4)
           store_b128(srsrc, off,
@@ -376,6 +383,63 @@ void scan_tiled_kernel(TiledScanArgs a) {
   }
 }
 
+// The frozen rule's per-frame maps as operand tiles, in place over A_t:
+// M_t = Diag(alpha_t)(I - A_t / U), element [k][n] = alpha_k (delta_kn -
+// A_t[k][n] / U), split into bf16 hi and lo planes (operand_tile_offset).
+// One workgroup per frame reads its whole A_t (A is symmetric, so the eight
+// k values of a lane slot are two contiguous runs of row n) before any
+// thread writes.
+template <int DK>
+__global__ __launch_bounds__(kThreads)
+void frozen_tiles_kernel(float* __restrict__ A, const float* __restrict__ alpha, float inv_u) {
+  constexpr int SLOTS = DK * DK / 8;                          // 8 elements per lane slot
+  constexpr int SPT = (SLOTS + kThreads - 1) / kThreads;      // slots per thread
+  const int tid = threadIdx.x;
+  float* a = A + (size_t)blockIdx.x * DK * DK;
+  const float* al = alpha != nullptr ? alpha + (size_t)blockIdx.x * DK : nullptr;
+  float v[SPT][8];
+#pragma unroll
+  for (int i = 0; i < SPT; ++i) {
+    const int sl = tid + kThreads * i;
+    if (sl >= SLOTS) continue;
+    const int lane = sl % 64, tile = sl / 64;
+    const int nb = tile / (DK / 32), ks = tile % (DK / 32);
+    const int n = 16 * nb + lane % 16, g = lane / 16;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int k0 = 32 * ks + 16 * h + 4 * g;
+      const float4 r = *reinterpret_cast<const float4*>(a + (size_t)n * DK + k0);
+      const float rv[4] = {r.x, r.y, r.z, r.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int k = k0 + e;
+        const float m = (k == n ? 1.0f : 0.0f) - rv[e] * inv_u;
+        v[i][4 * h + e] = al != nullptr ? al[k] * m : m;
+      }
+    }
+  }
+  __syncthreads();  // every read of this frame's A_t is done before it is overwritten
+  char* t0 = reinterpret_cast<char*>(a);
+#pragma unroll
+  for (int i = 0; i < SPT; ++i) {
+    const int sl = tid + kThreads * i;
+    if (sl >= SLOTS) continue;
+    const int lane = sl % 64, tile = sl / 64;
+    const int nb = tile / (DK / 32), ks = tile % (DK / 32);
+    uint32_t hw[4], lw[4];
+#pragma unroll
+    for (int e = 0; e < 8; e += 2) {
+      const uint32_t hh = pack_bf16x2(v[i][e], v[i][e + 1]);
+      hw[e / 2] = hh;
+      lw[e / 2] = pack_bf16x2(v[i][e] - bf16_lo(hh), v[i][e + 1] - bf16_hi(hh));
+    }
+    *reinterpret_cast<u32x4*>(t0 + operand_tile_offset(DK, 0, nb, ks, lane)) =
+        u32x4{hw[0], hw[1], hw[2], hw[3]};
+    *reinterpret_cast<u32x4*>(t0 + operand_tile_offset(DK, 1, nb, ks, lane)) =
+        u32x4{lw[0], lw[1], lw[2], lw[3]};
+  }
+}
+
 template <int DK, bool DECAY, bool CHUNKED>
 hipError_t launch_tiled_k(TiledScanArgs a, int H, hipStream_t stream) {
   a.nwg = (unsigned)H * 2u * (unsigned)(a.DV / 16);
@@ -413,7 +477,43 @@ hipError_t launch_chunk_sequence_scan(const void* Mt, const float* Jc, const flo
   a.DV = d_v;
   a.chunk = chunk;
   a.offset = offset;
+  a.mats_per_head = 2 * C;
+  a.dir_stride = C;
+  a.add_scale = 1.0f;
   a.C = C;
+  a.S_fwd = S_fwd;
+  a.S_rev = S_rev;
+  return launch_tiled(a, H, d_k, true, stream);
+}
+
+hipError_t launch_frozen_tiles(float* A, const float* alpha, int F, int H, int d_k, int tokens,
+                               hipStream_t stream) {
+  const dim3 grid((unsigned)((long long)H * F));
+  const float inv_u = 1.0f / (float)tokens;
+  switch (d_k) {
+    case 32: hipLaunchKernelGGL(frozen_tiles_kernel<32>, grid, dim3(kThreads), 0, stream, A, alpha, inv_u); break;
+    case 64: hipLaunchKernelGGL(frozen_tiles_kernel<64>, grid, dim3(kThreads), 0, stream, A, alpha, inv_u); break;
+    case 128: hipLaunchKernelGGL(frozen_tiles_kernel<128>, grid, dim3(kThreads), 0, stream, A, alpha, inv_u); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_frozen_scan_tiled(const void* M_tiles, const float* Bm, const float* text_state,
+                                    int F, int H, int d_k, int d_v, int tokens, float* S_fwd,
+                                    float* S_rev, hipStream_t stream) {
+  TiledScanArgs a{};
+  a.tiles = static_cast<const uint16_t*>(M_tiles);
+  a.add = Bm;
+  a.text_state = text_state;
+  a.F = F;
+  a.DV = d_v;
+  a.chunk = 1;
+  a.offset = 0;
+  a.C = F;
+  a.mats_per_head = F;
+  a.dir_stride = 0;
+  a.add_scale = 1.0f / sqrtf((float)tokens);
   a.S_fwd = S_fwd;
   a.S_rev = S_rev;
   return launch_tiled(a, H, d_k, true, stream);

@@ -125,20 +125,23 @@ def test_ragged_and_single_frame(V, dtype):
             assert rel_max_err(got, exp) <= tol_for(w), (F, N, rule)
 
 
-def test_full_size_sampled(V):
+@pytest.mark.parametrize("rule", ["joint", "frozen"])
+def test_full_size_sampled(V, rule):
     """A 768p-shaped head pair (36 frames x 3840 tokens, d = 128) with every
     option, at sampled positions: the states come from all frames."""
+    _log(f"full operator 768p-shaped sampled rule={rule}")
     w = I.custom("ex_768p", 1, 2, 36, 3840, 128, 128, "bf16", seed=45)
     x = I.make_inputs(w)
     alpha, S_T = I.make_decay(w), I.make_text_state(w)
-    got = _run(V, w, x, alpha, S_T, PAPER_WINDOW)
+    got = _run(V, w, x, alpha, S_T, PAPER_WINDOW, rule)
     xo = oracle_inputs(w, x)
     windows = O.local_windows(w.F, *PAPER_WINDOW)
     rng = np.random.default_rng(7)
     for h in range(w.heads):
         As, Bs = O.head_statistics(xo["k"][h], xo["v"][h], xo["beta"][h])
         St = O.gathered_states_ex(As, Bs, S_T[h].astype(np.float64),
-                                  alpha[h].astype(np.float64), windows)
+                                  alpha[h].astype(np.float64), windows, rule=rule,
+                                  U=w.N if rule == "frozen" else None)
         frames = rng.integers(0, w.F, 64)
         toks = rng.integers(0, w.N, 64)
         o = np.einsum("sjc,sc->sj", St[frames], xo["q"][h][frames, toks])
