@@ -3,8 +3,9 @@
 //   o_{t,u} = S~_t q_{t,u}               (Eq. 1a)
 //   y_{t,u} = gate * o / sqrt(mean(o^2) + eps)   (Eq. 1c)
 //
-// bf16 path: a workgroup owns one frame of one head and a range of its
-// tokens.  It sums the two fp32 states, rounds S~ to bf16 once into LDS, and
+// bf16 path: a workgroup owns one frame of one head and every `chunks`-th
+// 64-token super-group of it (the frame's workgroups sweep it together).
+// It sums the two fp32 states, rounds S~ to bf16 once into LDS, and
 // each wavefront keeps all of S~ as MFMA A-operands in registers.  It then
 // streams 16-token groups: the group's queries are the B-operand (16-byte
 // loads straight from HBM, three groups in flight per wave), O^T = S~ Q^T is

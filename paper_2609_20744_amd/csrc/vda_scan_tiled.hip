@@ -13,11 +13,12 @@
 // operand tiles (operand_tile_offset), in exactly the lane order of the
 // B-operands of v_mfma_f32_16x16x32_bf16.  Each wave loads the tiles of its
 // own 16-column output slices straight into registers, one contiguous 1 KB
-// piece per load instruction, two frames ahead of use.  No LDS image of
-// Inv_t, no per-step split of it and no barrier for it remain on the serial
-// path, which is now the row-wise update (entering state out, decay, B_t in,
-// split into bf16 hi / lo), one barrier, the matrix products and another
-// barrier.
+// piece per load instruction, two steps ahead of use, through a three-slot
+// register ring whose refills are issued between the products.  No LDS
+// image of Inv_t, no per-step split of it and no barrier for it remain on
+// the serial path, which is the row-wise update (entering state out, decay,
+// B_t in, split into bf16 hi / lo), one barrier, the matrix products and
+// another barrier.
 //
 // Products: the state operand x is split into hi = bf16(x) and
 // lo = bf16(x - hi) once per step, and hi*hi + hi*lo + lo*hi runs on the
