@@ -84,13 +84,23 @@ SOURCE_OF = {"frame_stats": ("vda_stats.hip",),
              "prep_conv": ("vda_prep.hip",), "prep_qnorm": ("vda_prep.hip",)}
 
 
+def _code_only(text: str) -> str:
+    """C++ source without comments and with whitespace collapsed, so that an
+    edit of the comments alone does not mark measured counters stale."""
+    import re
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", " ", text)
+    return " ".join(text.split())
+
+
 def source_hash(stage: str) -> str:
-    """SHA-256 over the kernel's source files and the shared device header."""
+    """SHA-256 over the code (comments and layout aside) of the kernel's
+    source files and the shared device header."""
     import hashlib
     h = hashlib.sha256()
     for f in SOURCE_OF[stage] + ("vda_common.h",):
-        with open(os.path.join(ROOT, "paper_2609_20744_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
+        with open(os.path.join(ROOT, "paper_2609_20744_amd", "csrc", f)) as fh:
+            h.update(_code_only(fh.read()).encode())
     return h.hexdigest()
 
 

@@ -77,3 +77,12 @@ def test_committed_traffic_summary_is_well_formed():
     for stage, k in s["kernels"].items():
         assert stage in bench.KERNEL_OF
         assert k["hbm_bytes_per_launch"] == pytest.approx(k["hbm_read_bytes"] + k["hbm_write_bytes"])
+
+
+def test_source_hash_ignores_comments_and_layout():
+    """Counters stay attached to a kernel whose comments alone change."""
+    a = "int f(int x) {  // doubles\n  return 2 * x;  /* twice */\n}\n"
+    b = "// a new header comment\nint f(int x) {\n\n  return 2 * x;\n}\n"
+    c = "int f(int x) { return 3 * x; }"
+    assert bench._code_only(a) == bench._code_only(b)
+    assert bench._code_only(a) != bench._code_only(c)
