@@ -78,6 +78,20 @@ def prep_kernel_bytes(w):
 KERNEL_OF = {"frame_stats": "stats_bf16_kernel", "frame_inverse": "inverse_kernel",
              "state_scan": "scan_tiled_kernel", "readout": "readout_bf16_kernel",
              "prep_conv": "prep_conv_kernel", "prep_qnorm": "prep_qnorm_kernel"}
+def instance_of(w):
+    """The template instance of each stage's kernel that one pass of the
+    workload runs (bf16 storage); the summary reads its counters, not those
+    of other instances of the same kernel (the chunk-wise and frozen-rule
+    scans share the scan kernel's name).  The prep convolution keeps its bare
+    name: its K and V launches are two instances, averaged."""
+    dk, dv = w.d_k, w.d_v
+    return {"frame_stats": f"stats_bf16_kernel<{dk},{dv}>",
+            "frame_inverse": f"inverse_kernel<{dk},true>",
+            "state_scan": f"scan_tiled_kernel<{dk},false,false>",
+            "readout": f"readout_bf16_kernel<{dk},{dv}>",
+            "prep_qnorm": f"prep_qnorm_kernel<{dk}>"}
+
+
 SOURCE_OF = {"frame_stats": ("vda_stats.hip",),
              "frame_inverse": ("vda_inverse.hip", "vda_inverse_body.h"),
              "state_scan": ("vda_scan_tiled.hip",), "readout": ("vda_readout.hip",),
@@ -131,18 +145,26 @@ def pmc_summary(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, copy_gib, 
     import re
 
     def load(d):
-        """Average bytes per dispatch, by kernel: the library's kernels by
-        their function name, the calibration copy (torch's neg) as "copy"."""
+        """Average bytes per dispatch, by kernel: the library's kernels both
+        by function name and by template instance ("name<args>", no
+        spaces), the calibration copy (torch's neg) as "copy"."""
         out = {}
         with open(os.path.join(d, "run_counter_collection.csv")) as f:
             for r in csv.DictReader(f):
                 full = r["Kernel_Name"]
+                names = []
                 if "neg_kernel" in full:
-                    name = "copy"
+                    names = ["copy"]
                 else:
                     m = re.search(r"::(\w+)(<[^()]*>)?\(", full)
-                    name = m.group(1) if m else full
-                out.setdefault(name, []).append(float(r["Counter_Value"]) * 1024.0)
+                    if m:
+                        names = [m.group(1)]
+                        if m.group(2):
+                            names.append(m.group(1) + m.group(2).replace(" ", ""))
+                    else:
+                        names = [full]
+                for name in names:
+                    out.setdefault(name, []).append(float(r["Counter_Value"]) * 1024.0)
         return {n: sum(v) / len(v) for n, v in out.items()}
 
     copy_bytes = copy_gib * (1 << 30)
@@ -152,7 +174,9 @@ def pmc_summary(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, copy_gib, 
     w = __import__("paper_2609_20744_amd.inputs", fromlist=["WORKLOADS"]).WORKLOADS[workload]
     kb = {**kernel_bytes(w), **prep_kernel_bytes(w)}
     kernels = {}
+    inst = instance_of(w)
     for stage, kname in KERNEL_OF.items():
+        kname = inst.get(stage, kname)
         if kname not in fetch or kname not in write:
             continue
         rd, wr = fetch[kname] * f_fetch, write[kname] * f_write
