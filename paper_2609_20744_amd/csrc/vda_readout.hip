@@ -8,7 +8,7 @@
 // It sums the two fp32 states, rounds S~ to bf16 once into LDS, and
 // each wavefront keeps all of S~ as MFMA A-operands in registers.  It then
 // streams 16-token groups: the group's queries are the B-operand (16-byte
-// loads straight from HBM, three groups in flight per wave), O^T = S~ Q^T is
+// loads straight from HBM, two groups in flight per wave), O^T = S~ Q^T is
 // accumulated in fp32 by v_mfma_f32_16x16x32_bf16, and the RMSNorm over the
 // d_v outputs of a token is a lane-local sum plus two cross-lane exchanges.
 // The normalised, gated values are rounded to bf16 and stored 16 bytes per
@@ -125,7 +125,7 @@ void readout_bf16_kernel(const uint16_t* __restrict__ Q, const float* __restrict
   // Rows past the frame are clamped onto its last row (always valid
   // memory); their outputs are dropped by the range-checked stores, so
   // loads and stores need no branches.
-  constexpr int kQ = 3;
+  constexpr int kQ = 2;
   const int S = 64 * chunks;
   uint4 qr[kQ][KB];
   auto load_q = [&](int nq, uint4 (&qv)[KB]) {
