@@ -262,9 +262,10 @@ int forward_impl(bool is_f32, const void* q, const void* k, const void* v, const
   // Heads narrower than 32 channels run as zero-padded 32-channel heads; the
   // padded q, k, v, output, alpha and text state live after the state buffers.
   const int pk = padded_dim(d_k), pv = padded_dim(d_v);
-  // The frozen rule reads the statistics directly, so its frames are not split.
+  // The fp32 frozen rule's scan reads the statistics directly, so its frames
+  // are not split; the bf16 frozen rule's map tiles sum the partials.
   const vda::SplitPlan plan =
-      frozen ? vda::SplitPlan{0, 1} : default_plan(dev, F, N, H, pk, pv, is_f32);
+      frozen && is_f32 ? vda::SplitPlan{0, 1} : default_plan(dev, F, N, H, pk, pv, is_f32);
   const Workspace w = workspace_layout(F, H, pk, pv, plan);
   // With a chunked local window (bf16 storage, joint rule) the readout reads
   // the states at chunk boundaries only: chunk-wise scans compute just those,
@@ -348,7 +349,7 @@ int forward_impl(bool is_f32, const void* q, const void* k, const void* v, const
     if (frozen && !is_f32) {
       // bf16 storage: the frozen maps as operand tiles (in place over A_t),
       // then the tiled scan in its map form.
-      e = vda::launch_frozen_tiles(A_part, alpha_x, F, H, pk, N, stream);
+      e = vda::launch_frozen_tiles(A_part, B_part, plan, alpha_x, F, H, pk, pv, N, stream);
       if (e == hipSuccess)
         e = vda::launch_frozen_scan_tiled(A_part, B_part, ts_x, F, H, pk, pv, N, S_fwd, S_rev,
                                           stream);

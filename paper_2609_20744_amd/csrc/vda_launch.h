@@ -54,11 +54,13 @@ hipError_t launch_state_scan(bool exact_f32, const float* Mat, const float* Bm, 
 
 // The frozen rule (Eq. 3c with the 1/sqrt(U) scaling) on the tiled scan:
 // launch_frozen_tiles overwrites each A_t [H][F][d_k][d_k] in place with the
-// operand tiles of M_t = Diag(alpha_t)(I - A_t / U) (alpha null: 1), and
+// operand tiles of M_t = Diag(alpha_t)(I - A_t / U) (alpha null: 1), summing
+// the token-range partials of split frames (and folding their B_t partials
+// into B_part[frame]) under the plan the statistics used, and
 // launch_frozen_scan_tiled runs x <- x M_t + B_t / sqrt(U) in both
 // directions from S_T / 2 (or zero), storing every frame's entering state.
-hipError_t launch_frozen_tiles(float* A, const float* alpha, int F, int H, int d_k, int tokens,
-                               hipStream_t stream);
+hipError_t launch_frozen_tiles(float* A, float* B_part, SplitPlan plan, const float* alpha, int F,
+                               int H, int d_k, int d_v, int tokens, hipStream_t stream);
 hipError_t launch_frozen_scan_tiled(const void* M_tiles, const float* Bm, const float* text_state,
                                     int F, int H, int d_k, int d_v, int tokens, float* S_fwd,
                                     float* S_rev, hipStream_t stream);

@@ -26,6 +26,7 @@
 // operand; relative error ~1e-5 per step, which the non-expansive frame maps
 // of Prop. 1 keep from growing along the scan).
 #include "vda_common.h"
+#include "vda_inverse_body.h"
 #include "vda_launch.h"
 
 namespace vda {
@@ -389,13 +390,24 @@ void scan_tiled_kernel(TiledScanArgs a) {
 // A_t[k][n] / U), split into bf16 hi and lo planes (operand_tile_offset).
 // One workgroup per frame reads its whole A_t (A is symmetric, so the eight
 // k values of a lane slot are two contiguous runs of row n) before any
-// thread writes.
+// thread writes.  Under a split plan the frames from first_split on are the
+// sums of plan_splits token-range partials (partial s at A + s *
+// part_stride), and `extra` workgroups after the frames fold the B_t
+// partials of those frames in place, as the inverse step does.
 template <int DK>
 __global__ __launch_bounds__(kThreads)
-void frozen_tiles_kernel(float* __restrict__ A, const float* __restrict__ alpha, float inv_u) {
+void frozen_tiles_kernel(float* __restrict__ A, const float* __restrict__ alpha, float inv_u,
+                         unsigned first_split, int plan_splits, unsigned extra, size_t part_stride,
+                         float* __restrict__ B_part, size_t b_mat, size_t b_stride) {
   constexpr int SLOTS = DK * DK / 8;                          // 8 elements per lane slot
   constexpr int SPT = (SLOTS + kThreads - 1) / kThreads;      // slots per thread
   const int tid = threadIdx.x;
+  if (blockIdx.x >= gridDim.x - extra) {
+    const size_t f = first_split + (blockIdx.x - (gridDim.x - extra));
+    inv::fold_b_partials(B_part + f * b_mat, plan_splits, b_mat, b_stride, tid, kThreads);
+    return;
+  }
+  const int splits = blockIdx.x >= first_split ? plan_splits : 1;
   float* a = A + (size_t)blockIdx.x * DK * DK;
   const float* al = alpha != nullptr ? alpha + (size_t)blockIdx.x * DK : nullptr;
   float v[SPT][8];
@@ -409,7 +421,14 @@ void frozen_tiles_kernel(float* __restrict__ A, const float* __restrict__ alpha,
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       const int k0 = 32 * ks + 16 * h + 4 * g;
-      const float4 r = *reinterpret_cast<const float4*>(a + (size_t)n * DK + k0);
+      float4 r = *reinterpret_cast<const float4*>(a + (size_t)n * DK + k0);
+      for (int sp = 1; sp < splits; ++sp) {  // token-range partials, in split order
+        const float4 x = *reinterpret_cast<const float4*>(a + sp * part_stride + (size_t)n * DK + k0);
+        r.x += x.x;
+        r.y += x.y;
+        r.z += x.z;
+        r.w += x.w;
+      }
       const float rv[4] = {r.x, r.y, r.z, r.w};
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
@@ -487,16 +506,27 @@ hipError_t launch_chunk_sequence_scan(const void* Mt, const float* Jc, const flo
   return launch_tiled(a, H, d_k, true, stream);
 }
 
-hipError_t launch_frozen_tiles(float* A, const float* alpha, int F, int H, int d_k, int tokens,
-                               hipStream_t stream) {
-  const dim3 grid((unsigned)((long long)H * F));
+hipError_t launch_frozen_tiles(float* A, float* B_part, SplitPlan plan, const float* alpha, int F,
+                               int H, int d_k, int d_v, int tokens, hipStream_t stream) {
+  const long long count = (long long)H * F;
+  const int splits = plan.splits > 1 && plan.tail > 0 ? plan.splits : 1;
+  const unsigned first_split = splits > 1 ? (unsigned)(count - plan.tail) : (unsigned)count;
+  const size_t part_stride = (size_t)plan.tail * d_k * d_k;  // partial p of frame f: f + p * tail
+  const size_t b_mat = (size_t)d_v * d_k;
+  const size_t b_stride = (size_t)plan.tail * b_mat;
+  const unsigned extra = splits > 1 ? (unsigned)plan.tail : 0u;
+  const dim3 grid((unsigned)count + extra);
   const float inv_u = 1.0f / (float)tokens;
+#define VDA_FROZEN_TILES(DK)                                                                   \
+  hipLaunchKernelGGL(frozen_tiles_kernel<DK>, grid, dim3(kThreads), 0, stream, A, alpha, inv_u, \
+                     first_split, splits, extra, part_stride, B_part, b_mat, b_stride)
   switch (d_k) {
-    case 32: hipLaunchKernelGGL(frozen_tiles_kernel<32>, grid, dim3(kThreads), 0, stream, A, alpha, inv_u); break;
-    case 64: hipLaunchKernelGGL(frozen_tiles_kernel<64>, grid, dim3(kThreads), 0, stream, A, alpha, inv_u); break;
-    case 128: hipLaunchKernelGGL(frozen_tiles_kernel<128>, grid, dim3(kThreads), 0, stream, A, alpha, inv_u); break;
+    case 32: VDA_FROZEN_TILES(32); break;
+    case 64: VDA_FROZEN_TILES(64); break;
+    case 128: VDA_FROZEN_TILES(128); break;
     default: return hipErrorInvalidValue;
   }
+#undef VDA_FROZEN_TILES
   return hipGetLastError();
 }
 

@@ -126,6 +126,26 @@ def test_ragged_and_single_frame(V, dtype):
 
 
 @pytest.mark.parametrize("rule", ["joint", "frozen"])
+def test_split_frames(V, rule):
+    """Frames whose statistics are split into token ranges (12 frames, a
+    partial round, 2048 tokens each), with decay, text state and the paper's
+    window: the joint rule's inverse and the frozen rule's map tiles both sum
+    the partials, and both fold B's."""
+    import torch
+    _log(f"full operator split frames rule={rule}")
+    w = I.custom("ex_split", 1, 2, 6, 2048, 128, 128, "bf16", seed=46)
+    tail, splits = V.default_split_plan(w.F, w.N, w.heads, w.d_k, w.d_v, False)
+    assert splits > 1 and tail > 0, (tail, splits)
+    x = I.make_inputs(w)
+    alpha, S_T = I.make_decay(w), I.make_text_state(w)
+    got = _run(V, w, x, alpha, S_T, PAPER_WINDOW, rule)
+    exp = _oracle(w, x, alpha, S_T, PAPER_WINDOW, rule)
+    err = rel_max_err(got, exp)
+    _log(f"  rel err {err:.2e} (plan {tail} x {splits})")
+    assert err <= tol_for(w), err
+
+
+@pytest.mark.parametrize("rule", ["joint", "frozen"])
 def test_full_size_sampled(V, rule):
     """A 768p-shaped head pair (36 frames x 3840 tokens, d = 128) with every
     option, at sampled positions: the states come from all frames."""
