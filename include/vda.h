@@ -165,8 +165,9 @@ typedef struct vda_options {
  *     out[t][u] = gate * RMSNorm(S~_t q[t][u]).  A window
  * that covers the whole clip is evaluated as written (both sides read the
  * decayed initial state); callers that bypass the linear branch in that case
- * do so themselves.  The frozen rule never splits frames (its statistics are
- * used directly), so its workspace has P = H*F.  Errors: VDA_ERR_UNSUPPORTED
+ * do so themselves.  With fp32 storage the frozen rule never splits frames
+ * (its scan reads the statistics directly); with bf16 storage it splits them
+ * as vda_forward does (its map step sums the partials).  Errors: VDA_ERR_UNSUPPORTED
  * for an unknown rule, VDA_ERR_SIZE for invalid window fields, VDA_ERR_ALIGN,
  * VDA_ERR_OVERLAP if out overlaps alpha or text_state.
  */
