@@ -150,7 +150,11 @@ __device__ __forceinline__ void invert_rows(const float* A_part, int splits, siz
     if (kb % W == WV) {
       const floatx4 dd = acc[kb / W][kb];
       float d[4] = {dd[0], dd[1], dd[2], dd[3]};
+      // The pivot block is this matrix's critical path: while it runs, the
+      // SIMD's arbiter prefers this wave over the other matrices' waves.
+      __builtin_amdgcn_s_setprio(2);
       invert_pivot_block(d, li, lg);
+      __builtin_amdgcn_s_setprio(0);
 #pragma unroll
       for (int j = 0; j < NB; ++j) {
         const floatx4 v = j == kb ? floatx4{d[0], d[1], d[2], d[3]} : acc[kb / W][j];
