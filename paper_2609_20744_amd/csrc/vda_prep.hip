@@ -307,13 +307,15 @@ void prep_qnorm_kernel(const uint16_t* __restrict__ in, uint16_t* __restrict__ o
   const int lane = threadIdx.x & 63;
   const long long grp = (long long)blockIdx.x * 4 + (threadIdx.x >> 6);  // one wave pass each
   if (grp >= total_groups) return;
-  // Group = (clip, frame, head, block of TPW tokens).
+  // Group = (clip, frame, block of TPW tokens, head).
   const int nblocks = (N + TPW - 1) / TPW;
   long long g = grp;
-  const int nb = (int)(g % nblocks);
-  g /= nblocks;
+  // Heads fastest: consecutive waves read one token's head slices in turn,
+  // so the reads of a frame run sequentially through memory.
   const int h = (int)(g % H);
   g /= H;
+  const int nb = (int)(g % nblocks);
+  g /= nblocks;
   const long long bf = g;  // clip * F + frame
   const int t = lane / LPT, j = lane % LPT;
   const int n = nb * TPW + t;

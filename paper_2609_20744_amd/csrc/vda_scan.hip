@@ -360,7 +360,8 @@ __device__ __forceinline__ void scan_mfma_phase(const uint16_t* __restrict__ xhi
 //            matrix is I - A_t / U, built from A_t on the way into LDS, and
 //            the write B_t / sqrt(U) is added after the product, that is at
 //            the start of the next step (B is loaded one frame late), so the
-//            state kept between steps is S_t - B_t / sqrt(U).
+//            state kept between steps is S_t - B_t / sqrt(U).  (Not launched:
+//            with bf16 storage the frozen rule runs on the tiled scan.)
 // Both scans may start from a text state: S_T / 2 (Eq. 1b).
 template <int DK, bool FROZEN, bool DECAY>
 __global__ __launch_bounds__(kThreads)
@@ -597,12 +598,16 @@ hipError_t launch_scan_v(bool exact_f32, const float* Mat, const float* Bm, int 
   const unsigned nwg = (unsigned)H * 2u * (unsigned)(d_v / 16);
   const float inv_u = FROZEN ? 1.0f / (float)o.tokens : 0.0f;
   const float inv_sqrt_u = FROZEN ? 1.0f / sqrtf((float)o.tokens) : 0.0f;
-  if (exact_f32)
+  if (exact_f32) {
     hipLaunchKernelGGL((scan_f32_kernel<DK, FROZEN, DECAY>), dim3(nwg), dim3(kThreads), 0, stream,
                        Mat, Bm, o.alpha, o.text_state, F, d_v, nwg, inv_u, inv_sqrt_u, S_fwd, S_rev);
-  else
-    hipLaunchKernelGGL((scan_bf16_kernel<DK, FROZEN, DECAY>), dim3(nwg), dim3(kThreads), 0, stream,
-                       Mat, Bm, o.alpha, o.text_state, F, d_v, nwg, inv_u, inv_sqrt_u, S_fwd, S_rev);
+  } else {
+    // With bf16 storage the frozen rule runs on the tiled scan (map form).
+    if constexpr (FROZEN) return hipErrorInvalidValue;
+    else
+      hipLaunchKernelGGL((scan_bf16_kernel<DK, false, DECAY>), dim3(nwg), dim3(kThreads), 0, stream,
+                         Mat, Bm, o.alpha, o.text_state, F, d_v, nwg, inv_u, inv_sqrt_u, S_fwd, S_rev);
+  }
   return hipGetLastError();
 }
 
