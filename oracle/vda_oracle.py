@@ -38,9 +38,11 @@ The full gather (the *_ex functions at the end) adds what the core leaves
 at its special values: the channel-wise decay alpha_t (S_bar_t =
 S_{t-1} Diag(alpha_t), Eq. 3a/5 and A.1), the text state S_T starting both
 scans at S_T / 2 (Eq. 1b), the local window [l_t, h_t] with the decay bridge
-of Eq. A.4, and, as a selectable rule, the frozen-state additive update of
-Eq. 3c with the 1/sqrt(U) key scaling the paper compares against (Section
-3.2, Appendix A.2).
+of Eq. A.4, the content-dependent output gate G^L of Eq. 1c (one value per
+token and channel, applied after RMSNorm, in place of the per-head gate),
+and, as a selectable rule, the frozen-state additive update of Eq. 3c with
+the 1/sqrt(U) key scaling the paper compares against (Section 3.2, Appendix
+A.2).
 
 Index convention: the paper numbers frames 1..F; arrays here use 0..F-1, so
 array frame i is the paper's frame t = i + 1.
@@ -162,8 +164,10 @@ def readout(S_tilde: np.ndarray, q: np.ndarray) -> np.ndarray:
     return q @ S_tilde.T
 
 
-def rmsnorm_gate(o: np.ndarray, gate: float, eps: float = RMS_EPS) -> np.ndarray:
-    """Eq. 1c, linear branch: g * RMSNorm(o) over the last (d_v) axis."""
+def rmsnorm_gate(o: np.ndarray, gate, eps: float = RMS_EPS) -> np.ndarray:
+    """Eq. 1c, linear branch: G * RMSNorm(o), the RMS over the last (d_v)
+    axis; G is one value per head, or an array of o's shape (the
+    content-dependent output gate, elementwise)."""
     ms = np.mean(o * o, axis=-1, keepdims=True)
     return gate * o / np.sqrt(ms + eps)
 
@@ -349,30 +353,36 @@ def gathered_states_ex(As, Bs, S_T=None, alphas=None, windows=None, rule="joint"
 
 
 def head_forward_ex(q, k, v, beta, gate: float, alpha=None, S_T=None, windows=None,
-                    rule="joint", eps: float = RMS_EPS) -> np.ndarray:
+                    rule="joint", eps: float = RMS_EPS, gate_tokens=None) -> np.ndarray:
     """The full linear branch for one head problem (Algorithm 1, steps 3-7):
     q, k [F,N,d_k], v [F,N,d_v], beta [F,N], alpha [F,d_k] or None, S_T
-    [d_v,d_k] or None, windows as in gathered_states_ex -> y [F,N,d_v]."""
+    [d_v,d_k] or None, windows as in gathered_states_ex -> y [F,N,d_v].
+    gate_tokens [F,N,d_v], when given, is the output gate G^L of Eq. 1c per
+    token and channel, and replaces the per-head gate."""
     if np.any(beta < 0):
         raise ValueError("write strengths must be non-negative")
     As, Bs = head_statistics(k, v, beta)
     St = gathered_states_ex(As, Bs, S_T, alpha, windows, rule, U=k.shape[1])
     y = np.empty(q.shape[:2] + (v.shape[2],))
     for t in range(q.shape[0]):
-        y[t] = rmsnorm_gate(readout(St[t], q[t]), gate, eps)
+        g = gate if gate_tokens is None else gate_tokens[t]
+        y[t] = rmsnorm_gate(readout(St[t], q[t]), g, eps)
     return y
 
 
 def vda_forward_ex(q, k, v, beta, gate, alpha=None, S_T=None, chunk=1, radius=0, offset=0,
-                   rule="joint", eps: float = RMS_EPS) -> np.ndarray:
+                   rule="joint", eps: float = RMS_EPS, gate_tokens=None) -> np.ndarray:
     """All head problems: alpha [H,F,d_k] or None, S_T [H,d_v,d_k] or None,
-    one window layout for every head."""
+    gate_tokens [H,F,N,d_v] or None (then gate [H] applies), one window
+    layout for every head."""
     H, F = q.shape[0], q.shape[1]
     windows = local_windows(F, chunk, radius, offset)
     return np.stack([
-        head_forward_ex(q[h], k[h], v[h], beta[h], float(gate[h]),
+        head_forward_ex(q[h], k[h], v[h], beta[h],
+                        1.0 if gate is None else float(gate[h]),
                         None if alpha is None else alpha[h],
-                        None if S_T is None else S_T[h], windows, rule, eps)
+                        None if S_T is None else S_T[h], windows, rule, eps,
+                        None if gate_tokens is None else gate_tokens[h])
         for h in range(H)])
 
 

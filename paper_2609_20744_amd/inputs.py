@@ -26,8 +26,9 @@ v (float32 normals), beta logits, then the optional zero mask and duplicate
 picks.  q, k, v are rounded to the storage type with round-to-nearest-even
 (bf16) or kept as float32.
 
-For the full operator: channel decays alpha uniform in [0.6, 1] and a text
-state S_T with N(0, 1) / 2 entries, each from its own salted stream.
+For the full operator: channel decays alpha uniform in [0.6, 1], a text
+state S_T with N(0, 1) / 2 entries and output gates sigmoid(N(0, 1)) per
+token and channel, each from its own salted stream.
 """
 from __future__ import annotations
 
@@ -223,6 +224,15 @@ def make_text_state(w: Workload, scale: float = 0.5, salt: int = 102) -> np.ndar
     default_rng([seed, salt])."""
     rng = np.random.default_rng([w.seed, salt])
     return (scale * rng.standard_normal((w.heads, w.d_v, w.d_k))).astype(np.float32)
+
+
+def make_token_gates(w: Workload, salt: int = 103) -> np.ndarray:
+    """Content-dependent output gates G^L [H_total][F][N][d_v] = sigmoid(z),
+    z ~ N(0, 1), one per token and value channel, in the workload's storage
+    type (float32, or bf16 bit patterns), from default_rng([seed, salt])."""
+    rng = np.random.default_rng([w.seed, salt])
+    z = rng.standard_normal((w.heads, w.F, w.N, w.d_v), dtype=np.float32)
+    return _store(_sigmoid(z).astype(np.float32), w.dtype)
 
 
 def as_float64(x: np.ndarray, dtype: str) -> np.ndarray:

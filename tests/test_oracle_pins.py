@@ -534,6 +534,47 @@ def pin_frozen_rule_non_expansive_with_scaling():
         assert np.linalg.norm(d1 - d2) <= np.linalg.norm(S1 - S2) * (1 + 1e-12)
 
 
+def pin_token_gate_reduces_to_head_gate():
+    """Eq. 1c with a content-dependent gate G^L: a gate that is constant over
+    tokens and channels is the per-head gate, and a gate of ones leaves
+    RMSNorm(o) itself."""
+    rng = _rng(51)
+    H, F, N, dk, dv = 2, 4, 6, 3, 5
+    q, k, v, beta = (np.stack(z) for z in zip(*[_random_clip(rng, F, N, dk, dv) for _ in range(H)]))
+    gate = np.array([0.3, 0.8])
+    base = O.vda_forward_ex(q, k, v, beta, gate, chunk=2, radius=1)
+    full = np.broadcast_to(gate[:, None, None, None], (H, F, N, dv)).copy()
+    np.testing.assert_allclose(O.vda_forward_ex(q, k, v, beta, None, chunk=2, radius=1,
+                                                gate_tokens=full), base, rtol=1e-13, atol=0)
+    ones = O.vda_forward_ex(q, k, v, beta, None, chunk=2, radius=1, gate_tokens=np.ones((H, F, N, dv)))
+    np.testing.assert_allclose(ones * gate[:, None, None, None], base, rtol=1e-13, atol=0)
+
+
+def pin_token_gate_applies_after_norm():
+    """The gate multiplies the normalised readout channel by channel: scaling
+    one channel of one token's gate by c scales exactly that output by c, and
+    the result equals torch's rms_norm of the readout times the gate (not the
+    norm of the gated readout)."""
+    import torch
+    rng = _rng(52)
+    F, N, dk, dv = 3, 5, 4, 6
+    q, k, v, beta = _random_clip(rng, F, N, dk, dv)
+    G = rng.uniform(0.05, 1.0, (F, N, dv))
+    y = O.head_forward_ex(q, k, v, beta, 1.0, gate_tokens=G)
+    G2 = G.copy()
+    G2[1, 2, 3] *= 7.0
+    y2 = O.head_forward_ex(q, k, v, beta, 1.0, gate_tokens=G2)
+    np.testing.assert_allclose(y2[1, 2, 3], 7.0 * y[1, 2, 3], rtol=1e-13)
+    mask = np.ones_like(y, dtype=bool)
+    mask[1, 2, 3] = False
+    np.testing.assert_array_equal(y2[mask], y[mask])
+    As, Bs = O.head_statistics(k, v, beta)
+    St = O.gathered_states_ex(As, Bs)
+    o = np.einsum("tjc,tuc->tuj", St, q)
+    ref = torch.nn.functional.rms_norm(torch.from_numpy(o), (dv,), eps=O.RMS_EPS).numpy() * G
+    np.testing.assert_allclose(y, ref, rtol=1e-12, atol=1e-14)
+
+
 def pin_local_windows_paper_layout():
     """Section 2.1: chunks of five latent frames, each query chunk sees itself
     and one chunk on each side, a 15-frame window away from the sequence
@@ -849,12 +890,28 @@ _ORIG_GATHER_EX = O.gathered_states_ex
 _ORIG_WINDOWS = O.local_windows
 _ORIG_CHUNK_RANGES = O.chunk_ranges
 
+_ORIG_HEAD_FORWARD_EX = O.head_forward_ex
+
+
+def _mut_token_gate_before_norm(q, k, v, beta, gate, alpha=None, S_T=None, windows=None,
+                                rule="joint", eps=O.RMS_EPS, gate_tokens=None):
+    if gate_tokens is None:
+        return _ORIG_HEAD_FORWARD_EX(q, k, v, beta, gate, alpha, S_T, windows, rule, eps)
+    As, Bs = O.head_statistics(k, v, beta)
+    St = O.gathered_states_ex(As, Bs, S_T, alpha, windows, rule, U=k.shape[1])
+    y = np.empty(q.shape[:2] + (v.shape[2],))
+    for t in range(q.shape[0]):
+        y[t] = O.rmsnorm_gate(gate_tokens[t] * O.readout(St[t], q[t]), 1.0, eps)
+    return y
+
+
 MUTANTS = [
     ("decayed_frame_update", _mut_decay_after_update),
     ("decayed_frame_update", _mut_frozen_unscaled),
     ("gathered_states_ex", _mut_bridge_skips_own_decay),
     ("gathered_states_ex", _mut_text_state_not_halved),
     ("local_windows", _mut_windows_ignore_offset),
+    ("head_forward_ex", _mut_token_gate_before_norm),
     ("chunk_map", _mut_chunk_map_wrong_order),
     ("depthwise_conv3", _mut_conv_wraps),
     ("depthwise_conv3", _mut_conv_flipped),
