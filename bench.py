@@ -476,15 +476,21 @@ def main() -> int:
     }
     # 3. The full operator (vda_forward_ex) on the same workload, with every
     #    option: channel decay, text state, the paper's local window (chunks
-    #    of five frames, radius one, one leading anchor), for both rules.
-    #    Reported beside the headline, not as it.
+    #    of five frames, radius one, one leading anchor), for both rules, and
+    #    the joint rule with the output gate per token and channel (which
+    #    adds one read of an output-sized tensor).  Reported beside the
+    #    headline, not as it.
     alpha = dev(I.make_decay(w), "f32")
     text_state = dev(I.make_text_state(w), "f32")
+    gtok = dev(I.make_token_gates(w), w.dtype) if w.dtype == "bf16" else None
     full = {}
-    for rule in ("joint", "frozen"):
+    for rule, tg in (("joint", False), ("frozen", False), ("joint", True)):
+        if tg and gtok is None:
+            continue
         def fwd_ex():
-            vda.forward(q, k, v, beta, gate, out=out, alpha=alpha, text_state=text_state,
-                        window=(5, 1, 1), rule=rule)
+            vda.forward(q, k, v, beta, None if tg else gate, out=out, alpha=alpha,
+                        text_state=text_state, window=(5, 1, 1), rule=rule,
+                        gate_tokens=gtok if tg else None)
         for _ in range(max(2, args.warmup)):
             fwd_ex()
         torch.cuda.synchronize()
@@ -495,10 +501,10 @@ def main() -> int:
         e1.record()
         torch.cuda.synchronize()
         ms_ex = e0.elapsed_time(e1) / K
-        full[f"{rule}_decay_text_window"] = {"ms_per_step": ms_ex,
-                                             "tokens_per_s": w.tokens / (ms_ex / 1e3)}
-        print(f"[bench] vda_forward_ex ({rule}, all options): {ms_ex:.4f} ms/step",
-              file=sys.stderr, flush=True)
+        name = f"{rule}_decay_text_window" + ("_token_gate" if tg else "")
+        full[name] = {"ms_per_step": ms_ex, "tokens_per_s": w.tokens / (ms_ex / 1e3)}
+        print(f"[bench] vda_forward_ex ({name}): {ms_ex:.4f} ms/step", file=sys.stderr,
+              flush=True)
     result["full_operator"] = full
     # 4. VDA-Prep (the feature map before the operator) on this workload's
     #    shape: token-major bf16 projections -> frame-major features.

@@ -141,6 +141,13 @@ typedef enum {
  *    anchor frame).  Frame t's window [l_t, h_t] is its own chunk and
  *    window_radius >= 0 chunks on each side, clipped to [0, F).  The paper's
  *    setting is chunk 5, radius 1 (offset 1 with one leading anchor).
+ *  - gate_tokens: NULL (the per-head gate applies) or a DEVICE pointer to
+ *    [H][F][N][d_v] output gates G^L in the storage type of q and out (bf16
+ *    for vda_forward_ex, fp32 for vda_forward_ex_f32; 16-byte aligned): the
+ *    content-dependent sigmoid gate of Eq. 1c, one value per token and value
+ *    channel, computed upstream and applied after RMSNorm,
+ *    out[t][u][c] = G^L[t][u][c] * RMSNorm(S~_t q[t][u])[c].  It replaces
+ *    the per-head gate, whose pointer may then be NULL.
  */
 typedef struct vda_options {
   int rule;
@@ -149,6 +156,7 @@ typedef struct vda_options {
   int window_chunk;
   int window_radius;
   int window_offset;
+  const void* gate_tokens;
 } vda_options;
 
 /*
@@ -162,14 +170,16 @@ typedef struct vda_options {
  * after frames F-1..j), and the gather of Eq. A.4 reads
  *     S~_t = P_{l_t} Diag(prod_{r=l_t..t} alpha_r)
  *          + R_{h_t+1} Diag(prod_{r=t..h_t} alpha_r),
- *     out[t][u] = gate * RMSNorm(S~_t q[t][u]).  A window
+ *     out[t][u] = gate * RMSNorm(S~_t q[t][u])  (G^L elementwise in place of
+ * gate with gate_tokens).  A window
  * that covers the whole clip is evaluated as written (both sides read the
  * decayed initial state); callers that bypass the linear branch in that case
  * do so themselves.  With fp32 storage the frozen rule never splits frames
  * (its scan reads the statistics directly); with bf16 storage it splits them
  * as vda_forward does (its map step sums the partials).  Errors: VDA_ERR_UNSUPPORTED
  * for an unknown rule, VDA_ERR_SIZE for invalid window fields, VDA_ERR_ALIGN,
- * VDA_ERR_OVERLAP if out overlaps alpha or text_state.
+ * VDA_ERR_OVERLAP if out overlaps alpha, text_state or gate_tokens,
+ * VDA_ERR_NULL if both gate and gate_tokens are NULL.
  */
 int vda_forward_ex(const void* q, const void* k, const void* v,
                    const float* beta, const float* gate,

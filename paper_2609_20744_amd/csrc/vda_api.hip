@@ -222,12 +222,14 @@ int check_options(const vda_options* o, vda_options* out) {
   d.window_chunk = 1;
   d.window_radius = 0;
   d.window_offset = 0;
+  d.gate_tokens = nullptr;
   if (o) d = *o;
   if (d.rule != VDA_RULE_JOINT && d.rule != VDA_RULE_FROZEN_SCALED) return VDA_ERR_UNSUPPORTED;
   if (d.window_chunk < 1 || d.window_radius < 0 || d.window_offset < 0 ||
       d.window_offset >= d.window_chunk)
     return VDA_ERR_SIZE;
-  if (!aligned(d.alpha, 16) || !aligned(d.text_state, 4)) return VDA_ERR_ALIGN;
+  if (!aligned(d.alpha, 16) || !aligned(d.text_state, 4) || !aligned(d.gate_tokens, 16))
+    return VDA_ERR_ALIGN;
   *out = d;
   return VDA_OK;
 }
@@ -235,15 +237,18 @@ int check_options(const vda_options* o, vda_options* out) {
 int forward_impl(bool is_f32, const void* q, const void* k, const void* v, const float* beta,
                  const float* gate, int F, int N, int H, int d_k, int d_v,
                  const vda_options* opts, void* out, hipStream_t stream) {
-  if (!q || !k || !v || !beta || !gate || !out) return VDA_ERR_NULL;
+  if (!q || !k || !v || !beta || !out) return VDA_ERR_NULL;
   int st = check_shape(F, N, H, d_k, d_v, true);
   if (st != VDA_OK) return st;
-  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 16) ||
-      !aligned(beta, 4) || !aligned(gate, 4))
-    return VDA_ERR_ALIGN;
   vda_options o;
   st = check_options(opts, &o);
   if (st != VDA_OK) return st;
+  // The per-head gate may be absent only when the output gate per token
+  // replaces it.
+  if (!gate && !o.gate_tokens) return VDA_ERR_NULL;
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 16) ||
+      !aligned(beta, 4) || !aligned(gate, 4))
+    return VDA_ERR_ALIGN;
   // The window arithmetic stays within 32 bits.
   if ((long long)F + 2LL * (o.window_radius + 1) * o.window_chunk > 0x3fffffffLL) return VDA_ERR_SIZE;
   const size_t es = is_f32 ? 4 : 2;
@@ -251,7 +256,8 @@ int forward_impl(bool is_f32, const void* q, const void* k, const void* v, const
   const Range ro = range_of(out, tok * d_v * es);
   if (overlaps(ro, range_of(q, tok * d_k * es)) || overlaps(ro, range_of(k, tok * d_k * es)) ||
       overlaps(ro, range_of(v, tok * d_v * es)) || overlaps(ro, range_of(beta, tok * 4)) ||
-      overlaps(ro, range_of(gate, (size_t)H * 4)) ||
+      (gate && overlaps(ro, range_of(gate, (size_t)H * 4))) ||
+      (o.gate_tokens && overlaps(ro, range_of(o.gate_tokens, tok * d_v * es))) ||
       (o.alpha && overlaps(ro, range_of(o.alpha, (size_t)H * F * d_k * 4))) ||
       (o.text_state && overlaps(ro, range_of(o.text_state, (size_t)H * d_v * d_k * 4))))
     return VDA_ERR_OVERLAP;
@@ -282,8 +288,9 @@ int forward_impl(bool is_f32, const void* q, const void* k, const void* v, const
   const size_t a_pad = pk != d_k && o.alpha ? round_up((size_t)H * F * pk * 4, 256) : 0;
   const size_t t_pad = pad_any && o.text_state ? round_up((size_t)H * pv * pk * 4, 256) : 0;
   const size_t t_tmp = pad_any && o.text_state ? round_up((size_t)H * d_v * pk * 4, 256) : 0;
+  const size_t g_pad = o.gate_tokens && pv != d_v ? round_up(tok * pv * es, 256) : 0;
   const size_t ws_bytes =
-      round_up(w.total, 256) + 2 * qk_pad + 2 * v_pad + a_pad + t_pad + t_tmp + c_ws;
+      round_up(w.total, 256) + 2 * qk_pad + 2 * v_pad + a_pad + t_pad + t_tmp + g_pad + c_ws;
   const int wsi = acquire_workspace(dev, ws_bytes, stream);
   if (wsi < 0) return VDA_ERR_NOMEM;
   char* base = static_cast<char*>(workspace_ptr(dev, wsi));
@@ -317,7 +324,14 @@ int forward_impl(bool is_f32, const void* q, const void* k, const void* v, const
     ox = pad_base + 2 * qk_pad + v_pad;
   }
   char* opt_base = pad_base + 2 * qk_pad + 2 * v_pad;
-  void* chunk_work = opt_base + a_pad + t_pad + t_tmp;
+  void* chunk_work = opt_base + a_pad + t_pad + t_tmp + g_pad;
+  const void* gt_x = o.gate_tokens;
+  if (g_pad && e == hipSuccess) {  // output gates [tok][d_v] -> [tok][32], zero channels added
+    void* gp = opt_base + a_pad + t_pad + t_tmp;
+    e = vda::launch_pad_rows(o.gate_tokens, gp, (long long)tok, (int)(d_v * es), (int)(pv * es),
+                             stream);
+    gt_x = gp;
+  }
   if (a_pad && e == hipSuccess) {  // alpha [H][F][d_k] -> [H][F][32]
     float* ap = reinterpret_cast<float*>(opt_base);
     e = vda::launch_pad_rows(o.alpha, ap, (long long)H * F, d_k * 4, pk * 4, stream);
@@ -367,6 +381,7 @@ int forward_impl(bool is_f32, const void* q, const void* k, const void* v, const
   go.chunk = o.window_chunk;
   go.radius = o.window_radius;
   go.offset = o.window_offset;
+  go.gate_tokens = gt_x;
   if (e == hipSuccess)
     e = vda::launch_readout(is_f32, qx, S_fwd, S_rev, gate, F, N, H, pk, pv, d_v, go, ox, stream);
   if (e == hipSuccess && ox != out)

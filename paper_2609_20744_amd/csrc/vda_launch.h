@@ -104,6 +104,9 @@ struct GatherOptions {
   int chunk = 1;                 // local window: frames per chunk,
   int radius = 0;                // chunks on each side,
   int offset = 0;                // and chunk position of frame 0
+  // [H][F][N][d_v] output gate G^L per token and channel (the storage type
+  // of q and out), or null: the per-head gate applies.
+  const void* gate_tokens = nullptr;
 };
 
 // Steps a5-a7, Eq. A.4 / 1a / 1c: gather, readout, RMSNorm and gate.

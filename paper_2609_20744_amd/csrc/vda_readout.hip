@@ -1,7 +1,9 @@
 // Steps a5-a7: gather, readout, RMSNorm and gate.
 //   S~_t = P_{t-1} + R_{t+1}            (Eq. A.4 with the window [t, t], alpha = 1)
 //   o_{t,u} = S~_t q_{t,u}               (Eq. 1a)
-//   y_{t,u} = gate * o / sqrt(mean(o^2) + eps)   (Eq. 1c)
+//   y_{t,u} = G * o / sqrt(mean(o^2) + eps)      (Eq. 1c)
+// G is the per-head gate, or (TOKGATE) the output gate G^L per token and
+// channel, read beside the queries.
 //
 // bf16 path: a workgroup owns one frame of one head and every `chunks`-th
 // 64-token super-group of it (the frame's workgroups sweep it together).
@@ -52,13 +54,14 @@ __device__ __forceinline__ void bridge_decay(const float* alpha, int h, int F, i
   }
 }
 
-template <int DK, int DV>
+template <int DK, int DV, bool TOKGATE>
 __global__ __launch_bounds__(kThreads, 2)
 void readout_bf16_kernel(const uint16_t* __restrict__ Q, const float* __restrict__ S_fwd,
                          const float* __restrict__ S_rev, const float* __restrict__ gate,
                          int F, int N, int chunks, int tokens_per_chunk, unsigned nwg,
                          float inv_norm, const float* __restrict__ alpha, int wchunk,
-                         int wradius, int woffset, uint16_t* __restrict__ out) {
+                         int wradius, int woffset, const uint16_t* __restrict__ gtok,
+                         uint16_t* __restrict__ out) {
   constexpr int SLD = DK + 8;  // bf16 row stride of S~ in LDS
   constexpr int MB = DV / 16;  // 16-row blocks of S~ (output channels)
   constexpr int KB = DK / 32;  // 32-wide k steps
@@ -70,7 +73,7 @@ void readout_bf16_kernel(const uint16_t* __restrict__ Q, const float* __restrict
   const unsigned L = xcd_grouped_id(blockIdx.x, nwg);
   const unsigned fh = L / chunks;
   const int chunk = L % chunks;
-  const float g = gate[fh / F];
+  const float g = TOKGATE ? 1.0f : gate[fh / F];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -125,7 +128,7 @@ void readout_bf16_kernel(const uint16_t* __restrict__ Q, const float* __restrict
   // Rows past the frame are clamped onto its last row (always valid
   // memory); their outputs are dropped by the range-checked stores, so
   // loads and stores need no branches.
-  constexpr int kQ = 2;
+  constexpr int kQ = TOKGATE ? 1 : 2;  // the gated variant keeps its gate loads in the budget
   const int S = 64 * chunks;
   uint4 qr[kQ][KB];
   auto load_q = [&](int nq, uint4 (&qv)[KB]) {
@@ -134,6 +137,11 @@ void readout_bf16_kernel(const uint16_t* __restrict__ Q, const float* __restrict
     for (int kb = 0; kb < KB; ++kb)
       qv[kb] = *reinterpret_cast<const uint4*>(qbase + (size_t)row * DK + kb * 32 + lg * 8);
   };
+  // TOKGATE: a group's output gate, four channels per lane and row block in
+  // the accumulators' layout, loaded after the group's products (rows past
+  // the frame read as zero).
+  const __amdgpu_buffer_rsrc_t grsrc =
+      make_rsrc(TOKGATE ? gtok + (size_t)fh * N * DV : Q, TOKGATE ? (uint32_t)N * DV * 2u : 0u);
   const __amdgpu_buffer_rsrc_t orsrc = make_rsrc(obase, (uint32_t)N * DV * 2u);
 
   const int n_first = chunk * 64 + wave * 16;
@@ -162,6 +170,14 @@ void readout_bf16_kernel(const uint16_t* __restrict__ Q, const float* __restrict
           acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sop[mb][kb], qop, acc[mb], 0, 0, 0);
       }
       load_q(ng + S * kQ, qr[d]);
+      u32x2 gnow[MB];  // this group's gate, in flight during the norm's reduction
+      if constexpr (TOKGATE) {
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb)
+          gnow[mb] = __builtin_bit_cast(
+              u32x2, __builtin_amdgcn_raw_buffer_load_b64(
+                         grsrc, (int)(((uint32_t)(ng + li) * DV + mb * 16 + 4 * lg) * 2u), 0, 0));
+      }
       // lane holds o[token ng + li][mb*16 + 4*lg + i]
       float ss = 0.f;
 #pragma unroll
@@ -177,10 +193,18 @@ void readout_bf16_kernel(const uint16_t* __restrict__ Q, const float* __restrict
       // up to 1 KB.
       uint16_t* tile = otile + wave * (16 * OLD);
 #pragma unroll
-      for (int mb = 0; mb < MB; ++mb)
+      for (int mb = 0; mb < MB; ++mb) {
+        float sc[4] = {scale, scale, scale, scale};
+        if constexpr (TOKGATE) {
+          sc[0] *= bf16_lo(gnow[mb][0]);
+          sc[1] *= bf16_hi(gnow[mb][0]);
+          sc[2] *= bf16_lo(gnow[mb][1]);
+          sc[3] *= bf16_hi(gnow[mb][1]);
+        }
         *reinterpret_cast<uint2*>(&tile[li * OLD + mb * 16 + 4 * lg]) =
-            make_uint2(pack_bf16x2(acc[mb][0] * scale, acc[mb][1] * scale),
-                       pack_bf16x2(acc[mb][2] * scale, acc[mb][3] * scale));
+            make_uint2(pack_bf16x2(acc[mb][0] * sc[0], acc[mb][1] * sc[1]),
+                       pack_bf16x2(acc[mb][2] * sc[2], acc[mb][3] * sc[3]));
+      }
       constexpr int CPR = DV / 8;     // 16-byte chunks per token row
       constexpr int RPI = 64 / CPR;   // token rows per store instruction
 #pragma unroll
@@ -195,13 +219,13 @@ void readout_bf16_kernel(const uint16_t* __restrict__ Q, const float* __restrict
 
 // fp32 storage: fp32 products and sums.  16 threads per token, each owning
 // d_v/16 output channels; S~ in LDS (fp32), queries staged per 16 tokens.
-template <int DK, int DV>
+template <int DK, int DV, bool TOKGATE>
 __global__ __launch_bounds__(kThreads)
 void readout_f32_kernel(const float* __restrict__ Q, const float* __restrict__ S_fwd,
                         const float* __restrict__ S_rev, const float* __restrict__ gate,
                         int F, int N, int chunks, int tokens_per_chunk, float inv_norm,
                         const float* __restrict__ alpha, int wchunk, int wradius, int woffset,
-                        float* __restrict__ out) {
+                        const float* __restrict__ gtok, float* __restrict__ out) {
   constexpr int SLD = DK + 1;
   constexpr int VPT = DV / 16;  // output channels per thread
   __shared__ float st[DV * SLD];
@@ -211,7 +235,7 @@ void readout_f32_kernel(const float* __restrict__ Q, const float* __restrict__ S
   const int chunk = blockIdx.x % chunks;
   const int n_begin = chunk * tokens_per_chunk;
   const int n_end = min(N, n_begin + tokens_per_chunk);
-  const float g = gate[fh / F];
+  const float g = TOKGATE ? 1.0f : gate[fh / F];
   const int tid = threadIdx.x;
 
   // Gather (Eq. A.4), as in readout_bf16_kernel.
@@ -252,7 +276,10 @@ void readout_f32_kernel(const float* __restrict__ Q, const float* __restrict__ S
     const int n = n0 + tok;
     if (n < n_end) {
 #pragma unroll
-      for (int m = 0; m < VPT; ++m) out[((size_t)fh * N + n) * DV + part + 16 * m] = o[m] * scale;
+      for (int m = 0; m < VPT; ++m) {
+        const size_t idx = ((size_t)fh * N + n) * DV + part + 16 * m;
+        out[idx] = TOKGATE ? o[m] * scale * gtok[idx] : o[m] * scale;
+      }
     }
   }
 }
@@ -276,15 +303,24 @@ hipError_t launch_readout_t(bool is_f32, const void* q, const float* S_fwd, cons
   int tpc = (N + chunks - 1) / chunks;
   tpc = ((tpc + 63) / 64) * 64;
   const dim3 grid((unsigned)(fh_count * chunks));
-  if (is_f32)
-    hipLaunchKernelGGL((readout_f32_kernel<DK, DV>), grid, dim3(kThreads), 0, stream,
-                       static_cast<const float*>(q), S_fwd, S_rev, gate, F, N, chunks, tpc,
-                       inv_norm, go.alpha, go.chunk, go.radius, go.offset, static_cast<float*>(out));
-  else
-    hipLaunchKernelGGL((readout_bf16_kernel<DK, DV>), grid, dim3(kThreads), 0, stream,
-                       static_cast<const uint16_t*>(q), S_fwd, S_rev, gate, F, N, chunks, tpc,
-                       (unsigned)(fh_count * chunks), inv_norm, go.alpha, go.chunk, go.radius,
-                       go.offset, static_cast<uint16_t*>(out));
+#define VDA_READOUT_LAUNCH(TG)                                                                     \
+  if (is_f32)                                                                                      \
+    hipLaunchKernelGGL((readout_f32_kernel<DK, DV, TG>), grid, dim3(kThreads), 0, stream,          \
+                       static_cast<const float*>(q), S_fwd, S_rev, gate, F, N, chunks, tpc,       \
+                       inv_norm, go.alpha, go.chunk, go.radius, go.offset,                         \
+                       static_cast<const float*>(go.gate_tokens), static_cast<float*>(out));      \
+  else                                                                                             \
+    hipLaunchKernelGGL((readout_bf16_kernel<DK, DV, TG>), grid, dim3(kThreads), 0, stream,         \
+                       static_cast<const uint16_t*>(q), S_fwd, S_rev, gate, F, N, chunks, tpc,    \
+                       (unsigned)(fh_count * chunks), inv_norm, go.alpha, go.chunk, go.radius,     \
+                       go.offset, static_cast<const uint16_t*>(go.gate_tokens),                    \
+                       static_cast<uint16_t*>(out));
+  if (go.gate_tokens != nullptr) {
+    VDA_READOUT_LAUNCH(true)
+  } else {
+    VDA_READOUT_LAUNCH(false)
+  }
+#undef VDA_READOUT_LAUNCH
   return hipGetLastError();
 }
 

@@ -39,7 +39,8 @@ class VdaOptions(ctypes.Structure):
     """struct vda_options (include/vda.h)."""
     _fields_ = [("rule", ctypes.c_int), ("alpha", ctypes.c_void_p),
                 ("text_state", ctypes.c_void_p), ("window_chunk", ctypes.c_int),
-                ("window_radius", ctypes.c_int), ("window_offset", ctypes.c_int)]
+                ("window_radius", ctypes.c_int), ("window_offset", ctypes.c_int),
+                ("gate_tokens", ctypes.c_void_p)]
 
 
 RULES = {"joint": 0, "frozen": 1}
@@ -152,13 +153,16 @@ def _shape(q, k, v, beta, gate=None):
 
 
 def forward(q, k, v, beta, gate, out=None, stream=None, alpha=None, text_state=None,
-            window=None, rule="joint"):
+            window=None, rule="joint", gate_tokens=None):
     """VDA forward (vda_forward for bf16 tensors, vda_forward_f32 for fp32).
 
     With any of the full-operator options it calls vda_forward_ex(_f32):
     alpha [..., F, d_k] fp32 channel decays, text_state [..., d_v, d_k] fp32
-    S_T, window = (chunk, radius, offset) of the local window, and rule
-    'joint' (Eq. 5) or 'frozen' (Eq. 3c with 1/sqrt(U) key scaling)."""
+    S_T, window = (chunk, radius, offset) of the local window, rule 'joint'
+    (Eq. 5) or 'frozen' (Eq. 3c with 1/sqrt(U) key scaling), and
+    gate_tokens [..., F, N, d_v] (q's dtype), the output gate G^L of Eq. 1c
+    per token and channel, which replaces the per-head gate (gate may then
+    be None)."""
     torch = _torch()
     dt = q.dtype
     if dt not in (torch.bfloat16, torch.float32):
@@ -169,7 +173,8 @@ def forward(q, k, v, beta, gate, out=None, stream=None, alpha=None, text_state=N
     for t, n in ((q, "q"), (k, "k"), (v, "v")):
         _require(t, n, dt, dev)
     _require(beta, "beta", torch.float32, dev)
-    _require(gate, "gate", torch.float32, dev)
+    if gate is not None or gate_tokens is None:
+        _require(gate, "gate", torch.float32, dev)
     lead, F, N, H, d_k, d_v = _shape(q, k, v, beta, gate)
     if out is None:
         out = torch.empty(lead + (F, N, d_v), dtype=dt, device=dev)
@@ -177,7 +182,8 @@ def forward(q, k, v, beta, gate, out=None, stream=None, alpha=None, text_state=N
         _require(out, "out", dt, dev)
         if tuple(out.shape) != lead + (F, N, d_v):
             raise ValueError(f"out shape {tuple(out.shape)} must be {lead + (F, N, d_v)}")
-    if alpha is None and text_state is None and window is None and rule == "joint":
+    if alpha is None and text_state is None and window is None and rule == "joint" and \
+            gate_tokens is None:
         fn = lib.vda_forward if dt == torch.bfloat16 else lib.vda_forward_f32
         with torch.cuda.device(dev):
             st = fn(q.data_ptr(), k.data_ptr(), v.data_ptr(), beta.data_ptr(), gate.data_ptr(),
@@ -195,13 +201,20 @@ def forward(q, k, v, beta, gate, out=None, stream=None, alpha=None, text_state=N
         if tuple(text_state.shape) != lead + (d_v, d_k):
             raise ValueError(f"text_state shape {tuple(text_state.shape)} must be "
                              f"{lead + (d_v, d_k)}")
+    if gate_tokens is not None:
+        _require(gate_tokens, "gate_tokens", dt, dev)
+        if tuple(gate_tokens.shape) != lead + (F, N, d_v):
+            raise ValueError(f"gate_tokens shape {tuple(gate_tokens.shape)} must be "
+                             f"{lead + (F, N, d_v)}")
     chunk, radius, offset = (1, 0, 0) if window is None else (int(x) for x in window)
     opts = VdaOptions(RULES[rule], alpha.data_ptr() if alpha is not None else None,
                       text_state.data_ptr() if text_state is not None else None,
-                      chunk, radius, offset)
+                      chunk, radius, offset,
+                      gate_tokens.data_ptr() if gate_tokens is not None else None)
     fn = lib.vda_forward_ex if dt == torch.bfloat16 else lib.vda_forward_ex_f32
     with torch.cuda.device(dev):
-        st = fn(q.data_ptr(), k.data_ptr(), v.data_ptr(), beta.data_ptr(), gate.data_ptr(),
+        st = fn(q.data_ptr(), k.data_ptr(), v.data_ptr(), beta.data_ptr(),
+                gate.data_ptr() if gate is not None else None,
                 F, N, H, d_k, d_v, ctypes.byref(opts), out.data_ptr(), _stream_ptr(dev, stream))
     _check(st, fn.__name__)
     return out

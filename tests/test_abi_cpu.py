@@ -179,3 +179,11 @@ def test_forward_ex_validation():
     assert ex(opts(), d_k=48) == 3
     assert L.vda_forward_ex(None, 2 * big, 3 * big, 4 * big, 5 * big, 4, 64, 2, 64, 64, None,
                             6 * big, None) == 1
+    # output gates per token: 16-byte aligned, not overlapping out, and the
+    # per-head gate may then be NULL (but not both)
+    assert ex(vda.VdaOptions(0, None, None, 1, 0, 0, 9 * big + 8)) == 4
+    assert ex(vda.VdaOptions(0, None, None, 1, 0, 0, 9 * big), out=9 * big + 64) == 5
+    assert L.vda_forward_ex(big, 2 * big, 3 * big, 4 * big, None, 4, 64, 2, 64, 64,
+                            ctypes.byref(opts()), 6 * big, None) == 1
+    assert L.vda_forward_ex(big, 2 * big, 3 * big, 4 * big, None, 4, 64, 2, 64, 64, None,
+                            6 * big, None) == 1

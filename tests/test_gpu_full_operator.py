@@ -27,48 +27,54 @@ def _log(msg):
     print(msg, flush=True)
 
 
-def _run(V, w, x, alpha=None, S_T=None, window=None, rule="joint"):
+def _run(V, w, x, alpha=None, S_T=None, window=None, rule="joint", G=None):
     import torch
     d = device_inputs(w, x)
     a_dev = None if alpha is None else to_device(alpha, "f32")
     t_dev = None if S_T is None else to_device(S_T, "f32")
-    y = V.forward(d["q"], d["k"], d["v"], d["beta"], d["gate"], alpha=a_dev, text_state=t_dev,
-                  window=window, rule=rule)
+    g_dev = None if G is None else to_device(G, w.dtype)
+    y = V.forward(d["q"], d["k"], d["v"], d["beta"], None if G is not None else d["gate"],
+                  alpha=a_dev, text_state=t_dev, window=window, rule=rule, gate_tokens=g_dev)
     torch.cuda.synchronize()
     return from_device(y)
 
 
-def _oracle(w, x, alpha=None, S_T=None, window=None, rule="joint"):
+def _oracle(w, x, alpha=None, S_T=None, window=None, rule="joint", G=None):
     xo = oracle_inputs(w, x)
     chunk, radius, offset = window or (1, 0, 0)
     return O.vda_forward_ex(xo["q"], xo["k"], xo["v"], xo["beta"], xo["gate"],
                             None if alpha is None else alpha.astype(np.float64),
                             None if S_T is None else S_T.astype(np.float64),
-                            chunk, radius, offset, rule)
+                            chunk, radius, offset, rule,
+                            gate_tokens=None if G is None else I.as_float64(G, w.dtype))
 
 
 CASES = [
-    # name, (alpha, text state, window, rule)
-    ("decay", (True, False, None, "joint")),
-    ("text_state", (False, True, None, "joint")),
-    ("window", (False, False, PAPER_WINDOW, "joint")),
-    ("all", (True, True, PAPER_WINDOW, "joint")),
-    ("frozen", (False, False, None, "frozen")),
-    ("frozen_all", (True, True, PAPER_WINDOW, "frozen")),
+    # name, (alpha, text state, window, rule, output gate per token)
+    ("decay", (True, False, None, "joint", False)),
+    ("text_state", (False, True, None, "joint", False)),
+    ("window", (False, False, PAPER_WINDOW, "joint", False)),
+    ("all", (True, True, PAPER_WINDOW, "joint", False)),
+    ("frozen", (False, False, None, "frozen", False)),
+    ("frozen_all", (True, True, PAPER_WINDOW, "frozen", False)),
+    ("token_gate", (False, False, None, "joint", True)),
+    ("all_token_gate", (True, True, PAPER_WINDOW, "joint", True)),
+    ("frozen_all_token_gate", (True, True, PAPER_WINDOW, "frozen", True)),
 ]
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("name,case", CASES, ids=[c[0] for c in CASES])
 def test_full_operator(V, dtype, name, case):
-    has_a, has_t, window, rule = case
+    has_a, has_t, window, rule, has_g = case
     _log(f"full operator {name} dtype={dtype}")
     w = I.custom("ex", 1, 2, 12, 150, 64, 64, dtype, seed=41)
     x = I.make_inputs(w)
     alpha = I.make_decay(w) if has_a else None
     S_T = I.make_text_state(w) if has_t else None
-    got = _run(V, w, x, alpha, S_T, window, rule)
-    exp = _oracle(w, x, alpha, S_T, window, rule)
+    G = I.make_token_gates(w) if has_g else None
+    got = _run(V, w, x, alpha, S_T, window, rule, G)
+    exp = _oracle(w, x, alpha, S_T, window, rule, G)
     err = rel_max_err(got, exp)
     _log(f"  rel err {err:.2e}")
     assert err <= tol_for(w), err
@@ -80,12 +86,13 @@ def test_full_operator_dims(V, dtype, dk, dv):
     _log(f"full operator dims dtype={dtype} dk={dk} dv={dv}")
     w = I.custom("ex_dims", 1, 2, 9, 100, dk, dv, dtype, seed=dk + 7 * dv)
     x = I.make_inputs(w)
-    alpha, S_T = I.make_decay(w), I.make_text_state(w)
+    alpha, S_T, G = I.make_decay(w), I.make_text_state(w), I.make_token_gates(w)
     for rule in ("joint", "frozen"):
-        got = _run(V, w, x, alpha, S_T, (3, 1, 0), rule)
-        exp = _oracle(w, x, alpha, S_T, (3, 1, 0), rule)
-        err = rel_max_err(got, exp)
-        assert err <= tol_for(w), (rule, err)
+        for gt in (None, G):
+            got = _run(V, w, x, alpha, S_T, (3, 1, 0), rule, gt)
+            exp = _oracle(w, x, alpha, S_T, (3, 1, 0), rule, gt)
+            err = rel_max_err(got, exp)
+            assert err <= tol_for(w), (rule, gt is not None, err)
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
