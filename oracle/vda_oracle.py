@@ -37,8 +37,8 @@ frame-major layout per head) is the VDA-Prep step of Section 4.
 The full gather (the *_ex functions at the end) adds what the core leaves
 at its special values: the channel-wise decay alpha_t (S_bar_t =
 S_{t-1} Diag(alpha_t), Eq. 3a/5 and A.1), the text state S_T starting both
-scans at S_T / 2 (Eq. 1b), the local window [l_t, h_t] with the decay bridge
-of Eq. A.4, the content-dependent output gate G^L of Eq. 1c (one value per
+scans at S_T / 2 (Eq. 1b; text_state forms S_T from the prompt), the local
+window [l_t, h_t] with the decay bridge of Eq. A.4, the content-dependent output gate G^L of Eq. 1c (one value per
 token and channel, applied after RMSNorm, in place of the per-head gate),
 and, as a selectable rule, the frozen-state additive update of Eq. 3c with
 the 1/sqrt(U) key scaling the paper compares against (Section 3.2, Appendix
@@ -384,6 +384,21 @@ def vda_forward_ex(q, k, v, beta, gate, alpha=None, S_T=None, chunk=1, radius=0,
                         None if S_T is None else S_T[h], windows, rule, eps,
                         None if gate_tokens is None else gate_tokens[h])
         for h in range(H)])
+
+
+def text_state(k, v, beta, rule="joint") -> np.ndarray:
+    """S_T per head: the prompt summarised into one state, taken as a leading
+    virtual frame updated from the zero state (Sec. 2.2, Eq. 1b; Sec. 4).
+    k [H,L,d_k], v [H,L,d_v], beta [H,L] over the L prompt tokens; returns
+    [H,d_v,d_k].  The frame's statistics are Eq. 3b over its tokens; from
+    S_prev = 0 the joint rule gives S_T = B_T (I + A_T)^{-1} (Eq. 5) and the
+    frozen rule B_T / sqrt(L) (Eq. 3c, U = L, the prompt's own token count)."""
+    H, L, d_k = k.shape
+    out = np.empty((H, v.shape[-1], d_k))
+    for h in range(H):
+        A, B = frame_statistics(k[h], v[h], beta[h])
+        out[h] = decayed_frame_update(np.zeros_like(B), A, B, rule=rule, U=L)
+    return out
 
 
 # ----------------------------------------------------------------------------

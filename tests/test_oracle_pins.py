@@ -494,6 +494,55 @@ def pin_text_state_counted_once():
         np.testing.assert_allclose(St[t - 1], ref, rtol=1e-13, atol=1e-14)
 
 
+def pin_text_state_closed_forms():
+    """S_T from the prompt as one frame from zero.  One token: the joint
+    solve is Sherman-Morrison's beta/(1 + beta ||k||^2) v k^T and the frozen
+    rule (U = 1) is beta v k^T.  Orthonormal keys: each token's weight is
+    beta/(1 + beta) (the joint solve decouples), and the frozen rule divides
+    by sqrt(L)."""
+    rng = _rng(53)
+    dk, dv = 5, 4
+    k = rng.normal(size=(2, 1, dk))
+    v = rng.normal(size=(2, 1, dv))
+    beta = rng.uniform(0.1, 1.5, size=(2, 1))
+    for h in range(2):
+        b, kk, vv = beta[h, 0], k[h, 0], v[h, 0]
+        np.testing.assert_allclose(O.text_state(k, v, beta)[h],
+                                   b / (1 + b * kk @ kk) * np.outer(vv, kk), rtol=1e-12, atol=1e-14)
+        np.testing.assert_allclose(O.text_state(k, v, beta, "frozen")[h], b * np.outer(vv, kk),
+                                   rtol=1e-12, atol=1e-14)
+    L = 3
+    Q, _ = np.linalg.qr(rng.normal(size=(dk, dk)))
+    k = Q[:L][None]                                   # orthonormal rows
+    v = rng.normal(size=(1, L, dv))
+    beta = rng.uniform(0.1, 1.5, size=(1, L))
+    w = beta[0] / (1 + beta[0])
+    np.testing.assert_allclose(O.text_state(k, v, beta)[0],
+                               sum(w[u] * np.outer(v[0, u], k[0, u]) for u in range(L)),
+                               rtol=1e-12, atol=1e-14)
+    np.testing.assert_allclose(O.text_state(k, v, beta, "frozen")[0],
+                               sum(beta[0, u] * np.outer(v[0, u], k[0, u]) for u in range(L)) / np.sqrt(L),
+                               rtol=1e-12, atol=1e-14)
+
+
+def pin_text_state_minimises_eq4():
+    """The joint rule's S_T is the minimiser of Eq. 4 with S_bar = 0 over the
+    prompt tokens: no direction lowers the objective (central differences
+    vanish and second differences are positive)."""
+    rng = _rng(54)
+    L, dk, dv = 9, 4, 3
+    k = _unit_rows(rng.normal(size=(1, L, dk)))
+    v = rng.normal(size=(1, L, dv))
+    beta = rng.uniform(0, 1, size=(1, L))
+    S = O.text_state(k, v, beta)[0]
+    f = lambda X: _eq4(X, np.zeros_like(S), k[0], v[0], beta[0])
+    for _ in range(5):
+        E = rng.normal(size=S.shape)
+        eps = 1e-4
+        assert abs(f(S + eps * E) - f(S - eps * E)) / (2 * eps) < 1e-7
+        assert f(S + eps * E) > f(S) and f(S - eps * E) > f(S)
+
+
 def pin_frozen_rule_is_scaled_token_sum():
     """Eq. 3a with every key scaled by 1/sqrt(U) (SANA-WM's scaling, Section
     3.2): Sbar + sum_u beta_u (v_u - Sbar k'_u) k'_u^T with k' = k / sqrt(U),
@@ -905,6 +954,19 @@ def _mut_token_gate_before_norm(q, k, v, beta, gate, alpha=None, S_T=None, windo
     return y
 
 
+_ORIG_TEXT_STATE = O.text_state
+
+
+def _mut_text_state_halved(k, v, beta, rule="joint"):
+    return 0.5 * _ORIG_TEXT_STATE(k, v, beta, rule)
+
+
+def _mut_text_state_frame_u(k, v, beta, rule="joint"):
+    if rule != "frozen":
+        return _ORIG_TEXT_STATE(k, v, beta, rule)
+    return np.stack([O.frame_statistics(k[h], v[h], beta[h])[1] for h in range(k.shape[0])])
+
+
 MUTANTS = [
     ("decayed_frame_update", _mut_decay_after_update),
     ("decayed_frame_update", _mut_frozen_unscaled),
@@ -912,6 +974,8 @@ MUTANTS = [
     ("gathered_states_ex", _mut_text_state_not_halved),
     ("local_windows", _mut_windows_ignore_offset),
     ("head_forward_ex", _mut_token_gate_before_norm),
+    ("text_state", _mut_text_state_halved),
+    ("text_state", _mut_text_state_frame_u),
     ("chunk_map", _mut_chunk_map_wrong_order),
     ("depthwise_conv3", _mut_conv_wraps),
     ("depthwise_conv3", _mut_conv_flipped),
