@@ -227,6 +227,31 @@ int vda_prep(const void* q, const void* k, const void* v,
              int B, int F, int grid_h, int grid_w, int H, int d_k, int d_v,
              void* q_out, void* k_out, void* v_out, hipStream_t stream);
 
+/*
+ * vda_text_state -- the prompt state S_T of Eq. 1b (Sec. 2.2), formed as the
+ * paper does: the prompt is a leading virtual frame updated from the zero
+ * state (Sec. 4).  Per head h, over its L prompt tokens, with
+ * A_T = sum_u beta k k^T and B_T = sum_u beta v k^T (Eq. 3b):
+ *     rule VDA_RULE_JOINT           S_T[h] = B_T (I + A_T)^{-1}   (Eq. 5)
+ *     rule VDA_RULE_FROZEN_SCALED   S_T[h] = B_T / sqrt(L)        (Eq. 3c, U = L)
+ * The result is the text_state of vda_options (the scans then start from
+ * S_T / 2).
+ *  - k [H][L][d_k], v [H][L][d_v]: DEVICE, bf16 (is_f32 == 0) or fp32
+ *    (is_f32 != 0), 16-byte aligned; beta [H][L] fp32 >= 0, 4-byte aligned.
+ *  - S_T [H][d_v][d_k] fp32, DEVICE, 16-byte aligned, written entirely; it
+ *    must not overlap the inputs.
+ *  - d_k, d_v in {16, 32, 64, 128}; L, H >= 1, with the limits of the
+ *    frame shape (N = L, F = 1).
+ * The statistics, inverse and precision are those of vda_forward's frames
+ * (bf16 storage rounds beta * k to bf16; the inverse is fp32); the final
+ * product is an fp32 loop.  Work memory comes from the library's per-device
+ * cache, as for vda_forward.  Errors: VDA_ERR_NULL, VDA_ERR_SIZE,
+ * VDA_ERR_UNSUPPORTED (dimension or rule), VDA_ERR_ALIGN, VDA_ERR_OVERLAP,
+ * VDA_ERR_NOMEM, VDA_ERR_HIP.  Asynchronous on `stream`.
+ */
+int vda_text_state(const void* k, const void* v, const float* beta, int L, int H,
+                   int d_k, int d_v, int rule, int is_f32, float* S_T, hipStream_t stream);
+
 /* ------------------------------------------------------------------------- */
 /* Stage interface: the same kernels as vda_forward, one step per call, with  */
 /* caller-owned fp32 work buffers (all device pointers, 16-byte aligned).     */

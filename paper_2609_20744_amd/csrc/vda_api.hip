@@ -4,6 +4,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <cmath>
 #include <atomic>
 #include <mutex>
 #include <vector>
@@ -391,6 +392,64 @@ int forward_impl(bool is_f32, const void* q, const void* k, const void* v, const
   return hip_status(ef);
 }
 
+// The prompt state: one frame of L tokens per head from the zero state.
+int text_state_impl(const void* k, const void* v, const float* beta, int L, int H, int d_k,
+                    int d_v, int rule, int is_f32, float* S_T, hipStream_t stream) {
+  if (!k || !v || !beta || !S_T) return VDA_ERR_NULL;
+  int st = check_shape(1, L, H, d_k, d_v, true);
+  if (st != VDA_OK) return st;
+  if (rule != VDA_RULE_JOINT && rule != VDA_RULE_FROZEN_SCALED) return VDA_ERR_UNSUPPORTED;
+  if (!aligned(k, 16) || !aligned(v, 16) || !aligned(beta, 4) || !aligned(S_T, 16))
+    return VDA_ERR_ALIGN;
+  const size_t es = is_f32 ? 4 : 2;
+  const size_t tok = (size_t)H * L;
+  const Range rs = range_of(S_T, (size_t)H * d_v * d_k * 4);
+  if (overlaps(rs, range_of(k, tok * d_k * es)) || overlaps(rs, range_of(v, tok * d_v * es)) ||
+      overlaps(rs, range_of(beta, tok * 4)))
+    return VDA_ERR_OVERLAP;
+  const bool frozen = rule == VDA_RULE_FROZEN_SCALED;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return VDA_ERR_HIP;
+  const int pk = padded_dim(d_k), pv = padded_dim(d_v);
+  // The frozen rule reads B directly, so its frame is not split; the joint
+  // rule's inverse folds the partials of a split frame.
+  const vda::SplitPlan plan =
+      frozen ? vda::SplitPlan{0, 1} : default_plan(dev, 1, L, H, pk, pv, is_f32 != 0);
+  const Workspace w = workspace_layout(1, H, pk, pv, plan);
+  const size_t k_pad = pk != d_k ? round_up(tok * pk * es, 256) : 0;
+  const size_t v_pad = pv != d_v ? round_up(tok * pv * es, 256) : 0;
+  const size_t stats_bytes = round_up(w.s_fwd, 256);  // the A and B partials
+  const int wsi = acquire_workspace(dev, stats_bytes + k_pad + v_pad, stream);
+  if (wsi < 0) return VDA_ERR_NOMEM;
+  char* base = static_cast<char*>(workspace_ptr(dev, wsi));
+  float* A_part = reinterpret_cast<float*>(base + w.a_part);
+  float* B_part = reinterpret_cast<float*>(base + w.b_part);
+  char* pad_base = base + stats_bytes;
+  const void* kx = k;
+  const void* vx = v;
+  hipError_t e = hipSuccess;
+  if (k_pad) {
+    e = vda::launch_pad_rows(k, pad_base, (long long)tok, (int)(d_k * es), (int)(pk * es), stream);
+    kx = pad_base;
+  }
+  if (v_pad && e == hipSuccess) {
+    e = vda::launch_pad_rows(v, pad_base + k_pad, (long long)tok, (int)(d_v * es), (int)(pv * es),
+                             stream);
+    vx = pad_base + k_pad;
+  }
+  if (e == hipSuccess)
+    e = vda::launch_frame_stats(is_f32 != 0, kx, vx, beta, 1, L, H, pk, pv, plan, A_part, B_part,
+                                stream);
+  if (e == hipSuccess && !frozen)
+    e = vda::launch_frame_inverse(A_part, B_part, plan, H, pk, pv, false, A_part, stream);
+  if (e == hipSuccess)
+    e = vda::launch_text_state(B_part, frozen ? nullptr : A_part, H, pk, pv, d_k, d_v,
+                               (float)(1.0 / std::sqrt((double)L)), S_T, stream);
+  const hipError_t ef = release_workspace(dev, wsi, stream);
+  if (e != hipSuccess) return VDA_ERR_HIP;
+  return hip_status(ef);
+}
+
 }  // namespace
 
 extern "C" {
@@ -431,6 +490,11 @@ int vda_forward_ex_f32(const float* q, const float* k, const float* v, const flo
                        const float* gate, int F, int N, int H, int d_k, int d_v,
                        const vda_options* opts, float* out, hipStream_t stream) {
   return forward_impl(true, q, k, v, beta, gate, F, N, H, d_k, d_v, opts, out, stream);
+}
+
+int vda_text_state(const void* k, const void* v, const float* beta, int L, int H, int d_k,
+                   int d_v, int rule, int is_f32, float* S_T, hipStream_t stream) {
+  return text_state_impl(k, v, beta, L, H, d_k, d_v, rule, is_f32, S_T, stream);
 }
 
 int vda_default_split_plan(int F, int N, int H, int d_k, int d_v, int is_f32, int* tail_frames,

@@ -116,6 +116,12 @@ hipError_t launch_readout(bool is_f32, const void* q, const float* S_fwd, const 
                           const float* gate, int F, int N, int H, int d_k, int d_v,
                           int d_v_norm, const GatherOptions& g, void* out, hipStream_t stream);
 
+// The prompt state from its frame's reduced statistics: S = B Inv (joint
+// rule; Inv != null) or S = B * scale (frozen rule).  B [H][pv][pk], Inv
+// [H][pk][pk], S [H][d_v][d_k] (pk >= d_k, pv >= d_v).
+hipError_t launch_text_state(const float* B, const float* Inv, int H, int pk, int pv, int d_k,
+                             int d_v, float scale, float* S, hipStream_t stream);
+
 // Row-wise channel padding (zero fill) and its inverse, in 16-byte pieces.
 hipError_t launch_pad_rows(const void* src, void* dst, long long rows, int src_bytes,
                            int dst_bytes, hipStream_t stream);

@@ -51,6 +51,7 @@ _SIGNATURES = {
     "vda_forward_f32": (_I, [_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _P, _P]),
     "vda_forward_ex": (_I, [_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _P, _P, _P]),
     "vda_forward_ex_f32": (_I, [_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _P, _P, _P]),
+    "vda_text_state": (_I, [_P, _P, _P, _I, _I, _I, _I, _I, _I, _P, _P]),
     "vda_default_split_plan": (_I, [_I, _I, _I, _I, _I, _I, _P, _P]),
     "vda_frame_stats": (_I, [_P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _P, _P, _P]),
     "vda_frame_inverse": (_I, [_P, _P, _I, _I, _I, _I, _I, _P, _P]),
@@ -217,6 +218,46 @@ def forward(q, k, v, beta, gate, out=None, stream=None, alpha=None, text_state=N
                 gate.data_ptr() if gate is not None else None,
                 F, N, H, d_k, d_v, ctypes.byref(opts), out.data_ptr(), _stream_ptr(dev, stream))
     _check(st, fn.__name__)
+    return out
+
+
+def text_state(k, v, beta, rule="joint", out=None, stream=None):
+    """The prompt state S_T (vda_text_state): k [..., L, d_k], v [..., L, d_v]
+    (bfloat16 or float32), beta [..., L] float32; returns [..., d_v, d_k]
+    float32, the text_state argument of forward."""
+    torch = _torch()
+    dt = k.dtype
+    if dt not in (torch.bfloat16, torch.float32):
+        raise ValueError(f"k dtype {dt} must be bfloat16 or float32")
+    dev = k.device
+    if dev.type != "cuda":
+        raise ValueError("VDA runs on the GPU only; tensors must be on a cuda device")
+    _require(k, "k", dt, dev)
+    _require(v, "v", dt, dev)
+    _require(beta, "beta", torch.float32, dev)
+    if rule not in RULES:
+        raise ValueError(f"rule must be one of {sorted(RULES)}")
+    if k.dim() < 2:
+        raise ValueError("k must be [..., L, d_k]")
+    lead = tuple(k.shape[:-2])
+    L, d_k = k.shape[-2:]
+    d_v = v.shape[-1]
+    H = math.prod(lead) if lead else 1
+    if tuple(v.shape) != lead + (L, d_v):
+        raise ValueError(f"v shape {tuple(v.shape)} does not match k")
+    if tuple(beta.shape) != lead + (L,):
+        raise ValueError(f"beta shape {tuple(beta.shape)} must be {lead + (L,)}")
+    if out is None:
+        out = torch.empty(lead + (d_v, d_k), dtype=torch.float32, device=dev)
+    else:
+        _require(out, "out", torch.float32, dev)
+        if tuple(out.shape) != lead + (d_v, d_k):
+            raise ValueError(f"out shape {tuple(out.shape)} must be {lead + (d_v, d_k)}")
+    with torch.cuda.device(dev):
+        st = lib.vda_text_state(k.data_ptr(), v.data_ptr(), beta.data_ptr(), L, H, d_k, d_v,
+                                RULES[rule], int(dt == torch.float32), out.data_ptr(),
+                                _stream_ptr(dev, stream))
+    _check(st, "vda_text_state")
     return out
 
 

@@ -187,3 +187,23 @@ def test_forward_ex_validation():
                             ctypes.byref(opts()), 6 * big, None) == 1
     assert L.vda_forward_ex(big, 2 * big, 3 * big, 4 * big, None, 4, 64, 2, 64, 64, None,
                             6 * big, None) == 1
+
+
+def test_text_state_validation():
+    """vda_text_state rejects bad arguments before touching the device."""
+    big = 1 << 32
+    ts = vda.lib.vda_text_state
+    # (k, v, beta, L, H, d_k, d_v, rule, is_f32, S_T, stream)
+    assert ts(None, 2 * big, 3 * big, 77, 4, 128, 128, 0, 0, 4 * big, None) == 1
+    assert ts(big, 2 * big, 3 * big, 77, 4, 128, 128, 0, 0, None, None) == 1
+    assert ts(big, 2 * big, 3 * big, 0, 4, 128, 128, 0, 0, 4 * big, None) == 2
+    assert ts(big, 2 * big, 3 * big, 77, 0, 128, 128, 0, 0, 4 * big, None) == 2
+    assert ts(big, 2 * big, 3 * big, 77, 4, 48, 128, 0, 0, 4 * big, None) == 3
+    assert ts(big, 2 * big, 3 * big, 77, 4, 128, 128, 2, 0, 4 * big, None) == 3
+    assert ts(big + 8, 2 * big, 3 * big, 77, 4, 128, 128, 0, 0, 4 * big, None) == 4
+    assert ts(big, 2 * big, 3 * big, 77, 4, 128, 128, 0, 0, 4 * big + 4, None) == 4
+    # S_T [4][128][128] fp32 over the tail of v, or over beta
+    assert ts(big, 2 * big, 3 * big, 77, 4, 128, 128, 0, 1, 2 * big + 4096, None) == 5
+    assert ts(big, 2 * big, 3 * big, 77, 4, 128, 128, 1, 0, 3 * big - 4096, None) == 5
+    # one prompt frame of d = 128 stays within 32-bit byte offsets
+    assert ts(big, 2 * big, 3 * big, 1 << 22, 1, 128, 128, 0, 0, 4 * big, None) == 2
