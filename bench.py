@@ -505,6 +505,26 @@ def main() -> int:
         full[name] = {"ms_per_step": ms_ex, "tokens_per_s": w.tokens / (ms_ex / 1e3)}
         print(f"[bench] vda_forward_ex ({name}): {ms_ex:.4f} ms/step", file=sys.stderr,
               flush=True)
+    # The prompt state itself (vda_text_state): a 512-token prompt per head of
+    # the workload, one frame from zero, joint rule.
+    pw = I.custom("prompt", 1, w.heads, 1, 512, w.d_k, w.d_v, w.dtype, seed=w.seed + 77)
+    px = I.make_inputs(pw)
+    pk, pv = dev(px["k"][:, 0], w.dtype), dev(px["v"][:, 0], w.dtype)
+    pb = dev(px["beta"][:, 0], "f32")
+    s_out = vda.text_state(pk, pv, pb)
+    for _ in range(max(2, args.warmup)):
+        vda.text_state(pk, pv, pb, out=s_out)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(K):
+        vda.text_state(pk, pv, pb, out=s_out)
+    e1.record()
+    torch.cuda.synchronize()
+    full["text_state_prompt512"] = {"ms_per_call": e0.elapsed_time(e1) / K, "prompt_tokens": 512,
+                                    "heads": w.heads}
+    print(f"[bench] vda_text_state (512 prompt tokens): {e0.elapsed_time(e1) / K:.4f} ms/call",
+          file=sys.stderr, flush=True)
     result["full_operator"] = full
     # 4. VDA-Prep (the feature map before the operator) on this workload's
     #    shape: token-major bf16 projections -> frame-major features.
