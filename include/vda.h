@@ -132,8 +132,8 @@ typedef enum {
  *    decays in [0, 1] (16-byte aligned), one per frame and key channel:
  *    Sbar_t = S_{t-1} Diag(alpha_t) (Eq. 5, A.1; Eq. 3a for the frozen rule),
  *    and the decay bridge of Eq. A.4.  Values outside [0, 1] are not checked.
- *  - text_state: NULL (zero) or a DEVICE pointer to [H][d_v][d_k] fp32 S_T:
- *    both scans start from S_T / 2 (Eq. 1b).
+ *  - text_state: NULL (zero) or a DEVICE pointer to [H][d_v][d_k] fp32 S_T
+ *    (16-byte aligned): both scans start from S_T / 2 (Eq. 1b).
  *  - window_chunk, window_radius, window_offset: the local Softmax window of
  *    each frame (Sec. 2.1; App. A.3).  Frames are grouped into chunks of
  *    window_chunk >= 1 consecutive frames, counted from window_offset
@@ -388,8 +388,8 @@ int vda_state_scan_tiles(const void* Inv_tiles, const float* B,
  * with the frame maps of vda_forward_ex (joint rule, decay alpha if not NULL;
  * Inv_tiles and B as for vda_state_scan_tiles).  These are the states the
  * windowed readout reads (Eq. A.4); all other frames of S_fwd and S_rev are
- * left untouched.  alpha [H][F][d_k] (16-byte aligned) and text_state
- * [H][d_v][d_k] (4-byte aligned) are DEVICE pointers or NULL.  `work` is a
+ * left untouched.  alpha [H][F][d_k] and text_state [H][d_v][d_k] (both
+ * 16-byte aligned) are DEVICE pointers or NULL.  `work` is a
  * caller-owned device buffer (16-byte aligned) of
  * vda_state_scan_chunked_workspace(...) bytes for M_c (split-bf16 operand
  * tiles) and J_c (fp32).  Products are split-bf16 with fp32 accumulation.

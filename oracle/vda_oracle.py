@@ -211,12 +211,6 @@ def head_forward_sampled(q, k, v, beta, gate: float, frames, tokens,
 # Other forms of the same rule, and neighbouring rules, for the checks
 # ----------------------------------------------------------------------------
 
-def objective(S, S_bar, K, V, beta) -> float:
-    """Eq. 4: 1/2 ||S - S_bar||_F^2 + 1/2 sum_u beta_u ||S k_u - v_u||^2."""
-    r = K @ S.T - V                       # rows: S k_u - v_u
-    return 0.5 * np.sum((S - S_bar) ** 2) + 0.5 * np.sum(beta * np.sum(r * r, axis=1))
-
-
 def joint_frame_update_token_space(S_bar, K, V, beta) -> np.ndarray:
     """The same minimiser reached through a U x U solve in token space.
 

@@ -229,7 +229,7 @@ int check_options(const vda_options* o, vda_options* out) {
   if (d.window_chunk < 1 || d.window_radius < 0 || d.window_offset < 0 ||
       d.window_offset >= d.window_chunk)
     return VDA_ERR_SIZE;
-  if (!aligned(d.alpha, 16) || !aligned(d.text_state, 4) || !aligned(d.gate_tokens, 16))
+  if (!aligned(d.alpha, 16) || !aligned(d.text_state, 16) || !aligned(d.gate_tokens, 16))
     return VDA_ERR_ALIGN;
   *out = d;
   return VDA_OK;
@@ -641,7 +641,7 @@ int vda_state_scan_chunked(const void* Inv_tiles, const float* B, const float* a
   if (st != VDA_OK) return st;
   if (chunk < 1 || offset < 0 || offset >= chunk) return VDA_ERR_SIZE;
   if ((long long)F + 2LL * chunk > 0x3fffffffLL) return VDA_ERR_SIZE;
-  if (!aligned(work, 16) || !aligned(alpha, 16) || !aligned(text_state, 4)) return VDA_ERR_ALIGN;
+  if (!aligned(work, 16) || !aligned(alpha, 16) || !aligned(text_state, 16)) return VDA_ERR_ALIGN;
   const size_t fh = (size_t)H * F;
   const Range rw = range_of(work, vda::chunked_scan_workspace(F, H, d_k, d_v, chunk, offset));
   const Range rf = range_of(S_fwd, fh * d_v * d_k * 4), rr = range_of(S_rev, fh * d_v * d_k * 4);

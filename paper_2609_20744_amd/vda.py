@@ -277,17 +277,6 @@ def partial_count(count: int, tail_frames: int, splits: int) -> int:
     return count + tail_frames * (splits - 1) if splits > 1 else count
 
 
-def fold_partials(P, count: int, tail_frames: int, splits: int):
-    """Sum each frame's partials of a [partials, ...] tensor into [count, ...]
-    (in range order, the order the library adds them)."""
-    out = P[:count].clone()
-    if splits > 1:
-        first = count - tail_frames
-        for s in range(1, splits):
-            out[first:] += P[count + (s - 1) * tail_frames:count + s * tail_frames]
-    return out
-
-
 def frame_stats(k, v, beta, splits=None, tail_frames=None, A_part=None, B_part=None,
                 stream=None):
     """Step a1 (vda_frame_stats): partial A [P, d_k, d_k] and B [P, d_v, d_k],

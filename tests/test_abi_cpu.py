@@ -123,6 +123,8 @@ def test_stage_validation():
               None) == 4
     assert ch(big, 2 * big, None, None, 12, 2, 64, 64, 5, 1, 5 * big + 8, 3 * big, 4 * big,
               None) == 4
+    assert ch(big, 2 * big, None, 6 * big + 4, 12, 2, 64, 64, 5, 1, 5 * big, 3 * big, 4 * big,
+              None) == 4
     assert ch(big, 2 * big, None, None, 12, 2, 64, 64, 5, 1, 3 * big, 3 * big, 4 * big, None) == 5
     assert ch(big, 2 * big, None, None, 12, 2, 64, 48, 5, 1, 5 * big, 3 * big, 4 * big, None) == 3
     pr = L.vda_prep
@@ -173,6 +175,11 @@ def test_forward_ex_validation():
     assert ex(opts(chunk=5, offset=5)) == 2             # offset must be < chunk
     assert ex(opts(alpha=7 * big + 8)) == 4             # alpha 16-byte aligned
     assert ex(opts(ts=7 * big + 2)) == 4
+    # the text state is read with 16-byte loads (also when 16-channel heads
+    # pad it): 4- and 8-byte offsets are rejected, 16-byte ones accepted
+    assert ex(opts(ts=7 * big + 4)) == 4
+    assert ex(opts(ts=7 * big + 8), d_k=16, d_v=16) == 4
+    assert ex(opts(ts=7 * big + 16), d_k=16, d_v=16) != 4
     # out overlapping alpha or the text state
     assert ex(opts(alpha=7 * big), out=7 * big + 64) == 5
     assert ex(opts(ts=8 * big), out=8 * big - 64) == 5

@@ -50,8 +50,9 @@ def _frac(a):
 # Pins
 # ----------------------------------------------------------------------------
 
-def pin_golden_hand_example():
-    """Hand-derived exact example (tests/golden): Eq. 3b, 5, A.1, A.4, 1a, 1c."""
+def _golden_clip():
+    """The hand-derived clip of tests/golden as float64 arrays, with its gate
+    and the expected outputs y = gate * o / sqrt(ms) (eps = 0)."""
     with open(os.path.join(GOLDEN, "hand_example_dk2_dv2_F3.json")) as f:
         g = json.load(f)
     k = np.stack([_frac(fr["k"]) for fr in g["frames"]])
@@ -59,6 +60,13 @@ def pin_golden_hand_example():
     q = np.stack([_frac(fr["q"]) for fr in g["frames"]])
     beta = np.stack([_frac(fr["beta"]) for fr in g["frames"]])
     gate = float(Fraction(g["gate"]))
+    y = gate * _frac(g["o"]) / np.sqrt(_frac(g["ms"]))[..., None]
+    return g, q, k, v, beta, gate, y
+
+
+def pin_golden_hand_example():
+    """Hand-derived exact example (tests/golden): Eq. 3b, 5, A.1, A.4, 1a, 1c."""
+    g, q, k, v, beta, gate, y_expect = _golden_clip()
     As, Bs = O.head_statistics(k, v, beta)
     np.testing.assert_allclose(np.eye(2)[None] + As, _frac(g["A"]), rtol=0, atol=1e-14)
     np.testing.assert_allclose(Bs, _frac(g["B"]), rtol=0, atol=1e-14)
@@ -77,7 +85,40 @@ def pin_golden_hand_example():
         np.testing.assert_allclose(y, gate * o_expect[t] / np.sqrt(ms[t])[:, None],
                                    rtol=1e-14, atol=1e-14)
     y_all = O.head_forward(q, k, v, beta, gate, eps=0.0)
-    np.testing.assert_allclose(y_all, gate * o_expect / np.sqrt(ms)[..., None], rtol=1e-14)
+    np.testing.assert_allclose(y_all, y_expect, rtol=1e-14)
+
+
+def pin_golden_at_head_one_of_two():
+    """Eq. 1c and Algorithm 1 act per head: each head problem reads only its
+    own inputs and its own gate.  The hand-derived clip sits at head 1 of a
+    two-head call whose head 0 is a random clip with a different gate, decay,
+    text state and token gate; head 1 must give the hand-derived outputs and
+    head 0 its own single-head result, for both multi-head wrappers."""
+    _, q1, k1, v1, b1, g1, y1 = _golden_clip()
+    rng = _rng(61)
+    q0, k0, v0, b0 = _random_clip(rng, F=3, N=2, d_k=2, d_v=2)
+    g0 = 0.3
+    q, k, v, beta = (np.stack(z) for z in ((q0, q1), (k0, k1), (v0, v1), (b0, b1)))
+    gate = np.array([g0, g1])
+    y = O.vda_forward(q, k, v, beta, gate, eps=0.0)
+    np.testing.assert_allclose(y[1], y1, rtol=1e-14, atol=1e-14)
+    np.testing.assert_allclose(y[0], O.head_forward(q0, k0, v0, b0, g0, eps=0.0),
+                               rtol=1e-14, atol=1e-14)
+    # Extended wrapper: head 1 keeps alpha = 1 and no text state (the
+    # golden clip's own setting); head 0 has its own decay and text state.
+    alpha = np.stack([_random_alpha(rng, 3, 2), np.ones((3, 2))])
+    S_T = np.stack([rng.standard_normal((2, 2)), np.zeros((2, 2))])
+    ye = O.vda_forward_ex(q, k, v, beta, gate, alpha=alpha, S_T=S_T, eps=0.0)
+    np.testing.assert_allclose(ye[1], y1, rtol=1e-14, atol=1e-14)
+    ref0 = O.head_forward_ex(q0, k0, v0, b0, g0, alpha[0], S_T[0], O.local_windows(3), "joint", 0.0)
+    np.testing.assert_allclose(ye[0], ref0, rtol=1e-13, atol=1e-14)
+    # Token gates: head 1's is its head gate everywhere, head 0's is random.
+    G = np.stack([rng.uniform(0.05, 1.0, (3, 2, 2)), np.full((3, 2, 2), g1)])
+    yg = O.vda_forward_ex(q, k, v, beta, None, alpha=alpha, S_T=S_T, eps=0.0, gate_tokens=G)
+    np.testing.assert_allclose(yg[1], y1, rtol=1e-14, atol=1e-14)
+    ref0 = O.head_forward_ex(q0, k0, v0, b0, 1.0, alpha[0], S_T[0], O.local_windows(3), "joint",
+                             0.0, G[0])
+    np.testing.assert_allclose(yg[0], ref0, rtol=1e-13, atol=1e-14)
 
 
 def pin_stats_outer_product_sum():
@@ -967,7 +1008,50 @@ def _mut_text_state_frame_u(k, v, beta, rule="joint"):
     return np.stack([O.frame_statistics(k[h], v[h], beta[h])[1] for h in range(k.shape[0])])
 
 
+_ORIG_FORWARD = O.vda_forward
+_ORIG_FORWARD_EX = O.vda_forward_ex
+
+
+def _mut_forward_gate0(q, k, v, beta, gate, eps=O.RMS_EPS):
+    return np.stack([O.head_forward(q[h], k[h], v[h], beta[h], float(gate[0]), eps)
+                     for h in range(q.shape[0])])
+
+
+def _mut_forward_heads_reversed(q, k, v, beta, gate, eps=O.RMS_EPS):
+    return _ORIG_FORWARD(q, k, v, beta, gate, eps)[::-1]
+
+
+def _mut_forward_ex_alpha0(q, k, v, beta, gate, alpha=None, S_T=None, chunk=1, radius=0,
+                           offset=0, rule="joint", eps=O.RMS_EPS, gate_tokens=None):
+    a = None if alpha is None else np.broadcast_to(alpha[:1], alpha.shape)
+    return _ORIG_FORWARD_EX(q, k, v, beta, gate, a, S_T, chunk, radius, offset, rule, eps,
+                            gate_tokens)
+
+
+def _mut_forward_ex_text_state0(q, k, v, beta, gate, alpha=None, S_T=None, chunk=1, radius=0,
+                                offset=0, rule="joint", eps=O.RMS_EPS, gate_tokens=None):
+    s = None if S_T is None else np.broadcast_to(S_T[:1], S_T.shape)
+    return _ORIG_FORWARD_EX(q, k, v, beta, gate, alpha, s, chunk, radius, offset, rule, eps,
+                            gate_tokens)
+
+
+def _mut_forward_ex_token_gate0(q, k, v, beta, gate, alpha=None, S_T=None, chunk=1, radius=0,
+                                offset=0, rule="joint", eps=O.RMS_EPS, gate_tokens=None):
+    G = None if gate_tokens is None else np.broadcast_to(gate_tokens[:1], gate_tokens.shape)
+    return _ORIG_FORWARD_EX(q, k, v, beta, gate, alpha, S_T, chunk, radius, offset, rule, eps, G)
+
+
+def _mut_forward_ex_heads_reversed(*args, **kw):
+    return _ORIG_FORWARD_EX(*args, **kw)[::-1]
+
+
 MUTANTS = [
+    ("vda_forward", _mut_forward_gate0),
+    ("vda_forward", _mut_forward_heads_reversed),
+    ("vda_forward_ex", _mut_forward_ex_alpha0),
+    ("vda_forward_ex", _mut_forward_ex_text_state0),
+    ("vda_forward_ex", _mut_forward_ex_token_gate0),
+    ("vda_forward_ex", _mut_forward_ex_heads_reversed),
     ("decayed_frame_update", _mut_decay_after_update),
     ("decayed_frame_update", _mut_frozen_unscaled),
     ("gathered_states_ex", _mut_bridge_skips_own_decay),

@@ -52,6 +52,55 @@ def rel_max_err(y: np.ndarray, ref: np.ndarray) -> float:
     return num / den
 
 
+def fold_partials(P, count: int, tail_frames: int, splits: int):
+    """Sum each frame's token-range partials of a [partials, ...] tensor
+    (the statistics stage's output under the split plan (tail_frames,
+    splits)) into [count, ...]: partial s of split frame i is entry
+    count + (s - 1) * tail_frames + (i - (count - tail_frames))."""
+    out = P[:count].clone()
+    if splits > 1:
+        first = count - tail_frames
+        for s in range(1, splits):
+            out[first:] += P[count + (s - 1) * tail_frames:count + s * tail_frames]
+    return out
+
+
+class ErrorAccumulator:
+    """The rel. max-norm error ||y - ref||_inf / ||ref||_inf of a whole
+    output tensor [H][F][N][d_v] fed in head groups, with the max-abs error
+    and the (head, frame, token) where it occurs."""
+
+    def __init__(self):
+        self.num = 0.0
+        self.den = 0.0
+        self.worst = None
+
+    def add(self, y: np.ndarray, ref: np.ndarray, h0: int):
+        d = np.abs(y - ref)
+        if d.size:
+            i = np.unravel_index(int(np.argmax(d)), d.shape)
+            if self.worst is None or d[i] > self.num:
+                self.num = float(d[i])
+                self.worst = (h0 + int(i[0]), int(i[1]), int(i[2]))
+            self.den = max(self.den, float(np.max(np.abs(ref))))
+
+    def rel_max_err(self) -> float:
+        return self.num / self.den if self.den > 0 else self.num
+
+    def report(self) -> str:
+        return (f"rel max-norm error {self.rel_max_err():.3e}, max abs error {self.num:.3e} "
+                f"(|ref|_inf {self.den:.3e}), worst (head, frame, token) {self.worst}")
+
+
+#: (case, report) of the whole-output parity checks, printed at the end of
+#: the session so the margins appear in the test log.
+ERROR_RECORDS: list[tuple[str, str]] = []
+
+
+def record_error(case: str, acc: ErrorAccumulator):
+    ERROR_RECORDS.append((case, acc.report()))
+
+
 def sample_positions(w, rng, per_frame: int):
     """Token indices per frame: the first, the last, the last full 16-token
     group boundary and random ones."""
