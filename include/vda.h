@@ -86,7 +86,8 @@ const char* vda_status_string(int status);
  * library-owned device buffers: a buffer is reused by later calls on the
  * same stream, or on another stream once the work of its last call has
  * finished, and otherwise a new one is allocated (hipMalloc; VDA_ERR_NOMEM
- * on failure).  Cached buffers are kept until the process ends.
+ * on failure).  Cached buffers are kept until vda_release_workspace frees
+ * them or the process ends.
  * A 16-channel d_k or d_v is run as a 32-channel head whose extra channels
  * are zero: q, k (and v) are copied into padded workspace buffers, zero
  * channels leave A_t, B_t, the states and the readout unchanged, RMSNorm
@@ -251,6 +252,30 @@ int vda_prep(const void* q, const void* k, const void* v,
  */
 int vda_text_state(const void* k, const void* v, const float* beta, int L, int H,
                    int d_k, int d_v, int rule, int is_f32, float* S_T, hipStream_t stream);
+
+/*
+ * vda_release_workspace -- frees the workspace buffers that the library has
+ * cached on `device` (-1: the current device) for vda_forward,
+ * vda_forward_ex(_f32), vda_forward_f32 and vda_text_state, except buffers
+ * that a call on another host thread is using at that moment (they stay
+ * cached).  Before freeing a buffer it waits on the host until the work of
+ * the buffer's last call has finished, so it blocks the calling thread and
+ * must not be called while a stream is being captured.  Later calls
+ * allocate again as they need.  *bytes_freed (may be NULL) receives the
+ * bytes freed.  The current device is left as it was.
+ * Errors: VDA_ERR_SIZE if device < -1 or device is not a device index;
+ * VDA_ERR_HIP if the runtime fails (buffers freed before the failure stay
+ * freed).
+ */
+int vda_release_workspace(int device, size_t* bytes_freed);
+
+/*
+ * vda_workspace_bytes -- bytes of workspace the library currently holds
+ * cached on `device` (-1: the current device), in use or idle.
+ * Errors: VDA_ERR_NULL if bytes is NULL; VDA_ERR_SIZE, VDA_ERR_HIP as for
+ * vda_release_workspace.
+ */
+int vda_workspace_bytes(int device, size_t* bytes);
 
 /* ------------------------------------------------------------------------- */
 /* Stage interface: the same kernels as vda_forward, one step per call, with  */

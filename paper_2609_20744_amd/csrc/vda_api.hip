@@ -72,8 +72,8 @@ int current_device_cus() {
 }
 
 // Library-owned workspace cache per device.  Buffers come from hipMalloc
-// and stay cached until the process ends (a free would synchronise the
-// device).  A buffer is reused by a later call on the same stream (stream
+// and stay cached until vda_release_workspace or the end of the process (a
+// free synchronises the device, so calls never free).  A buffer is reused by a later call on the same stream (stream
 // order makes that safe) or, on another stream, once the event recorded after
 // its last use has completed; between acquire and release it is marked busy
 // so concurrent host threads never share it.  (Stream-ordered pool
@@ -120,8 +120,15 @@ int acquire_workspace(int dev, size_t bytes, hipStream_t stream) {
       return -1;
     }
     e.bytes = bytes;
-    c.entries.push_back(e);
-    pick = (int)c.entries.size() - 1;
+    // An empty slot left by vda_release_workspace is reused.
+    for (size_t i = 0; i < c.entries.size() && pick < 0; ++i)
+      if (!c.entries[i].ptr && !c.entries[i].busy) pick = (int)i;
+    if (pick < 0) {
+      c.entries.push_back(e);
+      pick = (int)c.entries.size() - 1;
+    } else {
+      c.entries[pick] = e;
+    }
   }
   c.entries[pick].busy = true;
   c.entries[pick].stream = stream;
@@ -141,6 +148,53 @@ hipError_t release_workspace(int dev, int idx, hipStream_t stream) {
   const hipError_t r = hipEventRecord(e.done, stream);
   e.busy = false;
   return r;
+}
+
+// Resolves `device` (-1: the current device) for the workspace entry points.
+int workspace_device(int device, int* dev) {
+  if (device < -1 || device >= kMaxDevices) return VDA_ERR_SIZE;
+  int count = 0;
+  if (hipGetDeviceCount(&count) != hipSuccess) return VDA_ERR_HIP;
+  if (device >= count) return VDA_ERR_SIZE;
+  if (device == -1 && (hipGetDevice(&device) != hipSuccess || device < 0 || device >= kMaxDevices))
+    return VDA_ERR_HIP;
+  *dev = device;
+  return VDA_OK;
+}
+
+// Frees the cached buffers of `dev` that no call holds, after the work of
+// each one's last call has finished, and returns the bytes freed in *freed.
+// A freed entry stays in the list as an empty slot (calls hold entries by
+// index) and is reused by the next allocation.
+int release_cached_workspace(int dev, size_t* freed) {
+  WsCache& c = ws_cache(dev);
+  std::lock_guard<std::mutex> lock(c.mu);
+  int cur = 0;
+  if (hipGetDevice(&cur) != hipSuccess) return VDA_ERR_HIP;
+  if (cur != dev && hipSetDevice(dev) != hipSuccess) return VDA_ERR_HIP;
+  int st = VDA_OK;
+  size_t bytes = 0;
+  for (WsEntry& e : c.entries) {
+    if (e.busy || !e.ptr) continue;
+    if (hipEventSynchronize(e.done) != hipSuccess || hipFree(e.ptr) != hipSuccess) {
+      st = VDA_ERR_HIP;
+      break;
+    }
+    (void)hipEventDestroy(e.done);
+    bytes += e.bytes;
+    e = WsEntry();
+  }
+  if (cur != dev && hipSetDevice(cur) != hipSuccess && st == VDA_OK) st = VDA_ERR_HIP;
+  if (freed) *freed = bytes;
+  return st;
+}
+
+size_t cached_workspace_bytes(int dev) {
+  WsCache& c = ws_cache(dev);
+  std::lock_guard<std::mutex> lock(c.mu);
+  size_t bytes = 0;
+  for (const WsEntry& e : c.entries) bytes += e.bytes;
+  return bytes;
 }
 
 // Workgroups of the statistics kernel one compute unit holds at once, per
@@ -235,9 +289,28 @@ int check_options(const vda_options* o, vda_options* out) {
   return VDA_OK;
 }
 
-int forward_impl(bool is_f32, const void* q, const void* k, const void* v, const float* beta,
-                 const float* gate, int F, int N, int H, int d_k, int d_v,
-                 const vda_options* opts, void* out, hipStream_t stream) {
+// Everything a forward call decides on the host before it launches: the
+// validated arguments, the padded widths, the split plan, the scan path and
+// the workspace layout (offsets from the workspace base).
+struct ForwardCall {
+  bool is_f32 = false, frozen = false, chunked = false, tiled = false;
+  const void *q = nullptr, *k = nullptr, *v = nullptr;
+  const float *beta = nullptr, *gate = nullptr;
+  int F = 0, N = 0, H = 0, d_k = 0, d_v = 0, pk = 0, pv = 0;
+  vda_options o;
+  void* out = nullptr;
+  size_t es = 0, tok = 0;
+  vda::SplitPlan plan{0, 1};
+  Workspace w;
+  size_t qk_pad = 0, v_pad = 0, a_pad = 0, t_pad = 0, t_tmp = 0, g_pad = 0, c_ws = 0;
+  size_t ws_bytes = 0;
+};
+
+// Every argument check of a forward call, on the host, before anything is
+// enqueued; the validated options go to *o.
+int check_forward(bool is_f32, const void* q, const void* k, const void* v, const float* beta,
+                  const float* gate, int F, int N, int H, int d_k, int d_v,
+                  const vda_options* opts, const void* out, vda_options* o_out) {
   if (!q || !k || !v || !beta || !out) return VDA_ERR_NULL;
   int st = check_shape(F, N, H, d_k, d_v, true);
   if (st != VDA_OK) return st;
@@ -262,120 +335,138 @@ int forward_impl(bool is_f32, const void* q, const void* k, const void* v, const
       (o.alpha && overlaps(ro, range_of(o.alpha, (size_t)H * F * d_k * 4))) ||
       (o.text_state && overlaps(ro, range_of(o.text_state, (size_t)H * d_v * d_k * 4))))
     return VDA_ERR_OVERLAP;
-  const bool frozen = o.rule == VDA_RULE_FROZEN_SCALED;
+  *o_out = o;
+  return VDA_OK;
+}
 
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return VDA_ERR_HIP;
+// Lays out a checked forward call on device `dev`.
+void plan_forward(bool is_f32, const void* q, const void* k, const void* v, const float* beta,
+                  const float* gate, int F, int N, int H, int d_k, int d_v,
+                  const vda_options& o, void* out, int dev, ForwardCall* c) {
+  const size_t es = is_f32 ? 4 : 2;
+  const size_t tok = (size_t)H * F * N;
+  ForwardCall& C = *c;
+  C = ForwardCall();
+  C.is_f32 = is_f32;
+  C.frozen = o.rule == VDA_RULE_FROZEN_SCALED;
+  C.q = q, C.k = k, C.v = v, C.beta = beta, C.gate = gate, C.out = out, C.o = o;
+  C.F = F, C.N = N, C.H = H, C.d_k = d_k, C.d_v = d_v;
+  C.es = es, C.tok = tok;
   // Heads narrower than 32 channels run as zero-padded 32-channel heads; the
   // padded q, k, v, output, alpha and text state live after the state buffers.
   const int pk = padded_dim(d_k), pv = padded_dim(d_v);
+  C.pk = pk, C.pv = pv;
   // The fp32 frozen rule's scan reads the statistics directly, so its frames
   // are not split; the bf16 frozen rule's map tiles sum the partials.
-  const vda::SplitPlan plan =
-      frozen && is_f32 ? vda::SplitPlan{0, 1} : default_plan(dev, F, N, H, pk, pv, is_f32);
-  const Workspace w = workspace_layout(F, H, pk, pv, plan);
+  C.plan = C.frozen && is_f32 ? vda::SplitPlan{0, 1} : default_plan(dev, F, N, H, pk, pv, is_f32);
+  C.w = workspace_layout(F, H, pk, pv, C.plan);
   // With a chunked local window (bf16 storage, joint rule) the readout reads
   // the states at chunk boundaries only: chunk-wise scans compute just those,
   // where they are the faster path.
-  const bool chunked = !is_f32 && !frozen && o.window_chunk >= 2 &&
-                       chunked_scan_pays(F, H, o.window_chunk, o.window_offset);
-  const size_t c_ws =
-      chunked ? round_up(vda::chunked_scan_workspace(F, H, pk, pv, o.window_chunk, o.window_offset),
-                         256)
-              : 0;
-  const size_t qk_pad = pk != d_k ? round_up(tok * pk * es, 256) : 0;
-  const size_t v_pad = pv != d_v ? round_up(tok * pv * es, 256) : 0;
+  C.chunked = !is_f32 && !C.frozen && o.window_chunk >= 2 &&
+              chunked_scan_pays(F, H, o.window_chunk, o.window_offset);
+  C.tiled = !is_f32 && !C.frozen;
+  C.c_ws = C.chunked ? round_up(vda::chunked_scan_workspace(F, H, pk, pv, o.window_chunk,
+                                                            o.window_offset),
+                                256)
+                     : 0;
+  C.qk_pad = pk != d_k ? round_up(tok * pk * es, 256) : 0;
+  C.v_pad = pv != d_v ? round_up(tok * pv * es, 256) : 0;
   const bool pad_any = pk != d_k || pv != d_v;
-  const size_t a_pad = pk != d_k && o.alpha ? round_up((size_t)H * F * pk * 4, 256) : 0;
-  const size_t t_pad = pad_any && o.text_state ? round_up((size_t)H * pv * pk * 4, 256) : 0;
-  const size_t t_tmp = pad_any && o.text_state ? round_up((size_t)H * d_v * pk * 4, 256) : 0;
-  const size_t g_pad = o.gate_tokens && pv != d_v ? round_up(tok * pv * es, 256) : 0;
-  const size_t ws_bytes =
-      round_up(w.total, 256) + 2 * qk_pad + 2 * v_pad + a_pad + t_pad + t_tmp + g_pad + c_ws;
-  const int wsi = acquire_workspace(dev, ws_bytes, stream);
-  if (wsi < 0) return VDA_ERR_NOMEM;
-  char* base = static_cast<char*>(workspace_ptr(dev, wsi));
-  float* A_part = reinterpret_cast<float*>(base + w.a_part);
-  float* B_part = reinterpret_cast<float*>(base + w.b_part);
-  float* S_fwd = reinterpret_cast<float*>(base + w.s_fwd);
-  float* S_rev = reinterpret_cast<float*>(base + w.s_rev);
+  C.a_pad = pk != d_k && o.alpha ? round_up((size_t)H * F * pk * 4, 256) : 0;
+  C.t_pad = pad_any && o.text_state ? round_up((size_t)H * pv * pk * 4, 256) : 0;
+  C.t_tmp = pad_any && o.text_state ? round_up((size_t)H * d_v * pk * 4, 256) : 0;
+  C.g_pad = o.gate_tokens && pv != d_v ? round_up(tok * pv * es, 256) : 0;
+  C.ws_bytes = round_up(C.w.total, 256) + 2 * C.qk_pad + 2 * C.v_pad + C.a_pad + C.t_pad +
+               C.t_tmp + C.g_pad + C.c_ws;
+}
+
+// Enqueues a planned forward call with its workspace at `base` (at least
+// C.ws_bytes bytes, 256-byte aligned).
+hipError_t launch_forward(const ForwardCall& C, char* base, hipStream_t stream) {
+  const vda_options& o = C.o;
+  const int F = C.F, N = C.N, H = C.H, d_k = C.d_k, d_v = C.d_v, pk = C.pk, pv = C.pv;
+  const size_t es = C.es, tok = C.tok;
+  float* A_part = reinterpret_cast<float*>(base + C.w.a_part);
+  float* B_part = reinterpret_cast<float*>(base + C.w.b_part);
+  float* S_fwd = reinterpret_cast<float*>(base + C.w.s_fwd);
+  float* S_rev = reinterpret_cast<float*>(base + C.w.s_rev);
   float* Inv = A_part;  // the inverse overwrites the first partial
-  char* pad_base = base + round_up(w.total, 256);
-  const void* qx = q;
-  const void* kx = k;
-  const void* vx = v;
-  void* ox = out;
+  char* pad_base = base + round_up(C.w.total, 256);
+  const void* qx = C.q;
+  const void* kx = C.k;
+  const void* vx = C.v;
+  void* ox = C.out;
   const float* alpha_x = o.alpha;
   const float* ts_x = o.text_state;
 
   hipError_t e = hipSuccess;
-  if (qk_pad) {
+  if (C.qk_pad) {
     void* qp = pad_base;
-    void* kp = pad_base + qk_pad;
-    e = vda::launch_pad_rows(q, qp, (long long)tok, (int)(d_k * es), (int)(pk * es), stream);
+    void* kp = pad_base + C.qk_pad;
+    e = vda::launch_pad_rows(C.q, qp, (long long)tok, (int)(d_k * es), (int)(pk * es), stream);
     if (e == hipSuccess)
-      e = vda::launch_pad_rows(k, kp, (long long)tok, (int)(d_k * es), (int)(pk * es), stream);
+      e = vda::launch_pad_rows(C.k, kp, (long long)tok, (int)(d_k * es), (int)(pk * es), stream);
     qx = qp;
     kx = kp;
   }
-  if (v_pad && e == hipSuccess) {
-    void* vp = pad_base + 2 * qk_pad;
-    e = vda::launch_pad_rows(v, vp, (long long)tok, (int)(d_v * es), (int)(pv * es), stream);
+  if (C.v_pad && e == hipSuccess) {
+    void* vp = pad_base + 2 * C.qk_pad;
+    e = vda::launch_pad_rows(C.v, vp, (long long)tok, (int)(d_v * es), (int)(pv * es), stream);
     vx = vp;
-    ox = pad_base + 2 * qk_pad + v_pad;
+    ox = pad_base + 2 * C.qk_pad + C.v_pad;
   }
-  char* opt_base = pad_base + 2 * qk_pad + 2 * v_pad;
-  void* chunk_work = opt_base + a_pad + t_pad + t_tmp + g_pad;
+  char* opt_base = pad_base + 2 * C.qk_pad + 2 * C.v_pad;
+  void* chunk_work = opt_base + C.a_pad + C.t_pad + C.t_tmp + C.g_pad;
   const void* gt_x = o.gate_tokens;
-  if (g_pad && e == hipSuccess) {  // output gates [tok][d_v] -> [tok][32], zero channels added
-    void* gp = opt_base + a_pad + t_pad + t_tmp;
+  if (C.g_pad && e == hipSuccess) {  // output gates [tok][d_v] -> [tok][32], zero channels added
+    void* gp = opt_base + C.a_pad + C.t_pad + C.t_tmp;
     e = vda::launch_pad_rows(o.gate_tokens, gp, (long long)tok, (int)(d_v * es), (int)(pv * es),
                              stream);
     gt_x = gp;
   }
-  if (a_pad && e == hipSuccess) {  // alpha [H][F][d_k] -> [H][F][32]
+  if (C.a_pad && e == hipSuccess) {  // alpha [H][F][d_k] -> [H][F][32]
     float* ap = reinterpret_cast<float*>(opt_base);
     e = vda::launch_pad_rows(o.alpha, ap, (long long)H * F, d_k * 4, pk * 4, stream);
     alpha_x = ap;
   }
-  if (t_pad && e == hipSuccess) {  // S_T [H][d_v][d_k] -> [H][d_v][pk] -> [H][pv][pk]
-    float* tt = reinterpret_cast<float*>(opt_base + a_pad);
-    float* tp = reinterpret_cast<float*>(opt_base + a_pad + t_tmp);
+  if (C.t_pad && e == hipSuccess) {  // S_T [H][d_v][d_k] -> [H][d_v][pk] -> [H][pv][pk]
+    float* tt = reinterpret_cast<float*>(opt_base + C.a_pad);
+    float* tp = reinterpret_cast<float*>(opt_base + C.a_pad + C.t_tmp);
     e = vda::launch_pad_rows(o.text_state, tt, (long long)H * d_v, d_k * 4, pk * 4, stream);
     if (e == hipSuccess)
       e = vda::launch_pad_rows(tt, tp, (long long)H, d_v * pk * 4, pv * pk * 4, stream);
     ts_x = tp;
   }
   if (e == hipSuccess)
-    e = vda::launch_frame_stats(is_f32, kx, vx, beta, F, N, H, pk, pv, plan, A_part, B_part,
+    e = vda::launch_frame_stats(C.is_f32, kx, vx, C.beta, F, N, H, pk, pv, C.plan, A_part, B_part,
                                 stream);
   // With bf16 storage the joint rule's inverse is written as split-bf16
   // operand tiles for the state scan.
-  const bool tiled = !is_f32 && !frozen;
-  if (e == hipSuccess && !frozen)
-    e = vda::launch_frame_inverse(A_part, B_part, plan, (long long)H * F, pk, pv, tiled, Inv,
+  if (e == hipSuccess && !C.frozen)
+    e = vda::launch_frame_inverse(A_part, B_part, C.plan, (long long)H * F, pk, pv, C.tiled, Inv,
                                   stream);
   vda::ScanOptions so;
-  so.frozen = frozen;
+  so.frozen = C.frozen;
   so.alpha = alpha_x;
   so.text_state = ts_x;
   so.tokens = N;
   if (e == hipSuccess) {
-    if (frozen && !is_f32) {
+    if (C.frozen && !C.is_f32) {
       // bf16 storage: the frozen maps as operand tiles (in place over A_t),
       // then the tiled scan in its map form.
-      e = vda::launch_frozen_tiles(A_part, B_part, plan, alpha_x, F, H, pk, pv, N, stream);
+      e = vda::launch_frozen_tiles(A_part, B_part, C.plan, alpha_x, F, H, pk, pv, N, stream);
       if (e == hipSuccess)
         e = vda::launch_frozen_scan_tiled(A_part, B_part, ts_x, F, H, pk, pv, N, S_fwd, S_rev,
                                           stream);
-    } else if (chunked)
+    } else if (C.chunked)
       e = vda::launch_state_scan_chunked(Inv, B_part, alpha_x, ts_x, F, H, pk, pv, o.window_chunk,
                                          o.window_offset, chunk_work, S_fwd, S_rev, stream);
-    else if (tiled)
+    else if (C.tiled)
       e = vda::launch_state_scan_tiled(Inv, B_part, F, H, pk, pv, so, S_fwd, S_rev, stream);
     else
-      e = vda::launch_state_scan(is_f32, frozen ? A_part : Inv, B_part, F, H, pk, pv, so, S_fwd,
-                                 S_rev, stream);
+      e = vda::launch_state_scan(C.is_f32, C.frozen ? A_part : Inv, B_part, F, H, pk, pv, so,
+                                 S_fwd, S_rev, stream);
   }
   vda::GatherOptions go;
   go.alpha = alpha_x;
@@ -384,9 +475,26 @@ int forward_impl(bool is_f32, const void* q, const void* k, const void* v, const
   go.offset = o.window_offset;
   go.gate_tokens = gt_x;
   if (e == hipSuccess)
-    e = vda::launch_readout(is_f32, qx, S_fwd, S_rev, gate, F, N, H, pk, pv, d_v, go, ox, stream);
-  if (e == hipSuccess && ox != out)
-    e = vda::launch_unpad_rows(ox, out, (long long)tok, (int)(pv * es), (int)(d_v * es), stream);
+    e = vda::launch_readout(C.is_f32, qx, S_fwd, S_rev, C.gate, F, N, H, pk, pv, d_v, go, ox,
+                            stream);
+  if (e == hipSuccess && ox != C.out)
+    e = vda::launch_unpad_rows(ox, C.out, (long long)tok, (int)(pv * es), (int)(d_v * es), stream);
+  return e;
+}
+
+int forward_impl(bool is_f32, const void* q, const void* k, const void* v, const float* beta,
+                 const float* gate, int F, int N, int H, int d_k, int d_v,
+                 const vda_options* opts, void* out, hipStream_t stream) {
+  vda_options o;
+  const int st = check_forward(is_f32, q, k, v, beta, gate, F, N, H, d_k, d_v, opts, out, &o);
+  if (st != VDA_OK) return st;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return VDA_ERR_HIP;
+  ForwardCall C;
+  plan_forward(is_f32, q, k, v, beta, gate, F, N, H, d_k, d_v, o, out, dev, &C);
+  const int wsi = acquire_workspace(dev, C.ws_bytes, stream);
+  if (wsi < 0) return VDA_ERR_NOMEM;
+  const hipError_t e = launch_forward(C, static_cast<char*>(workspace_ptr(dev, wsi)), stream);
   const hipError_t ef = release_workspace(dev, wsi, stream);
   if (e != hipSuccess) return VDA_ERR_HIP;
   return hip_status(ef);
@@ -495,6 +603,24 @@ int vda_forward_ex_f32(const float* q, const float* k, const float* v, const flo
 int vda_text_state(const void* k, const void* v, const float* beta, int L, int H, int d_k,
                    int d_v, int rule, int is_f32, float* S_T, hipStream_t stream) {
   return text_state_impl(k, v, beta, L, H, d_k, d_v, rule, is_f32, S_T, stream);
+}
+
+int vda_release_workspace(int device, size_t* bytes_freed) {
+  if (bytes_freed) *bytes_freed = 0;
+  int dev = 0;
+  const int st = workspace_device(device, &dev);
+  if (st != VDA_OK) return st;
+  return release_cached_workspace(dev, bytes_freed);
+}
+
+int vda_workspace_bytes(int device, size_t* bytes) {
+  if (!bytes) return VDA_ERR_NULL;
+  *bytes = 0;
+  int dev = 0;
+  const int st = workspace_device(device, &dev);
+  if (st != VDA_OK) return st;
+  *bytes = cached_workspace_bytes(dev);
+  return VDA_OK;
 }
 
 int vda_default_split_plan(int F, int N, int H, int d_k, int d_v, int is_f32, int* tail_frames,

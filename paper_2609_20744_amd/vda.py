@@ -62,6 +62,8 @@ _SIGNATURES = {
     "vda_state_scan_chunked_workspace": (ctypes.c_size_t, [_I, _I, _I, _I, _I, _I]),
     "vda_prep": (_I, [_P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _P, _P, _P, _P]),
     "vda_readout": (_I, [_P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _P, _P]),
+    "vda_release_workspace": (_I, [_I, _P]),
+    "vda_workspace_bytes": (_I, [_I, _P]),
 }
 
 
@@ -259,6 +261,23 @@ def text_state(k, v, beta, rule="joint", out=None, stream=None):
                                 _stream_ptr(dev, stream))
     _check(st, "vda_text_state")
     return out
+
+
+def release_workspace(device: int = -1) -> int:
+    """Free the library's cached workspace buffers on `device` (-1: the
+    current one) that no call is using (vda_release_workspace); waits for
+    their last work on the host.  Returns the bytes freed."""
+    n = ctypes.c_size_t(0)
+    _check(lib.vda_release_workspace(int(device), ctypes.byref(n)), "vda_release_workspace")
+    return n.value
+
+
+def workspace_bytes(device: int = -1) -> int:
+    """Bytes of workspace the library holds cached on `device` (-1: the
+    current one) (vda_workspace_bytes)."""
+    n = ctypes.c_size_t(0)
+    _check(lib.vda_workspace_bytes(int(device), ctypes.byref(n)), "vda_workspace_bytes")
+    return n.value
 
 
 def default_split_plan(F: int, N: int, H: int, d_k: int, d_v: int,

@@ -214,3 +214,17 @@ def test_text_state_validation():
     assert ts(big, 2 * big, 3 * big, 77, 4, 128, 128, 1, 0, 3 * big - 4096, None) == 5
     # one prompt frame of d = 128 stays within 32-bit byte offsets
     assert ts(big, 2 * big, 3 * big, 1 << 22, 1, 128, 128, 0, 0, 4 * big, None) == 2
+
+
+def test_workspace_entry_points_validation():
+    """vda_release_workspace / vda_workspace_bytes reject device indices below
+    -1 or beyond the library's device table before any runtime call, and a
+    NULL result pointer; *bytes_freed is cleared first."""
+    n = ctypes.c_size_t(123)
+    assert vda.lib.vda_release_workspace(-2, ctypes.byref(n)) == 2
+    assert n.value == 0
+    assert vda.lib.vda_release_workspace(64, None) == 2
+    assert vda.lib.vda_workspace_bytes(0, None) == 1
+    n = ctypes.c_size_t(123)
+    assert vda.lib.vda_workspace_bytes(-7, ctypes.byref(n)) == 2
+    assert n.value == 0
