@@ -63,7 +63,9 @@ typedef enum {
   VDA_ERR_ALIGN = 4,       /* a pointer is not aligned as required            */
   VDA_ERR_OVERLAP = 5,     /* the output overlaps an input                    */
   VDA_ERR_HIP = 6,         /* the HIP runtime reported an error               */
-  VDA_ERR_NOMEM = 7        /* workspace allocation failed                     */
+  VDA_ERR_NOMEM = 7,       /* workspace allocation failed                     */
+  VDA_ERR_SCRATCH = 8      /* vda_forward_noalloc: one head's workspace is
+                              larger than VDA_NOALLOC_SCRATCH_BYTES           */
 } vda_status;
 
 /* Human-readable name of a status code (static storage; never NULL). */
@@ -100,6 +102,36 @@ int vda_forward(const void* q, const void* k, const void* v,
                 const float* beta, const float* gate,
                 int F, int N, int H, int d_k, int d_v,
                 void* out, hipStream_t stream);
+
+/* Bytes of the fixed device scratch array of vda_forward_noalloc. */
+#define VDA_NOALLOC_SCRATCH_BYTES ((size_t)256 << 20)
+
+/*
+ * vda_forward_noalloc -- vda_forward for callers that cannot allocate device
+ * memory: code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc.  Same arguments, semantics, argument checks and kernels
+ * as vda_forward; the call allocates and frees nothing.  Its workspace is a
+ * fixed array of VDA_NOALLOC_SCRATCH_BYTES (256 MiB) of device memory that
+ * the library's code object holds on every device the library runs on,
+ * until the process ends.  The caller still passes all inputs and out.
+ * When vda_forward's workspace for all H heads is larger than the array,
+ * the heads run in consecutive groups, each as one forward pass over its
+ * heads (the largest groups that fit); head problems are independent, so
+ * the results are vda_forward's up to the summation order of the split
+ * statistics.  Every call on a device shares that device's one array, and
+ * the array keeps the last call's contents (nothing in it needs to start at
+ * zero): calls that overlap in time on one device, on different streams or
+ * from different threads, race and give undefined results; order them on
+ * one stream or with events.
+ * Errors: as vda_forward; VDA_ERR_SCRATCH (nothing enqueued) when a single
+ * head's workspace is larger than the array, e.g. more than about 1000
+ * frames at d_k = d_v = 128; VDA_ERR_HIP if the array's device address
+ * cannot be obtained or a launch fails.
+ */
+int vda_forward_noalloc(const void* q, const void* k, const void* v,
+                        const float* beta, const float* gate,
+                        int F, int N, int H, int d_k, int d_v,
+                        void* out, hipStream_t stream);
 
 /*
  * vda_forward_f32 -- identical semantics and arguments with fp32 storage for

@@ -500,6 +500,87 @@ int forward_impl(bool is_f32, const void* q, const void* k, const void* v, const
   return hip_status(ef);
 }
 
+// Fixed device scratch of vda_forward_noalloc: the code object holds it on
+// every device the library runs on, until the process ends.  Host code never
+// passes this name to a kernel (on the host it is only a stand-in for the
+// device array); it uses the address that hipGetSymbolAddress returns for
+// the current device.
+static __device__ __align__(256) unsigned char scratch[VDA_NOALLOC_SCRATCH_BYTES];
+
+// Device address of `scratch` on device `dev` (the current device), looked up
+// once per device; nullptr if the runtime cannot resolve it.
+char* scratch_ptr(int dev) {
+  static std::mutex mu;
+  static char* ptrs[kMaxDevices] = {};
+  std::lock_guard<std::mutex> lock(mu);
+  if (!ptrs[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return nullptr;
+    ptrs[dev] = static_cast<char*>(p);
+  }
+  return ptrs[dev];
+}
+
+// Workspace bytes of vda_forward over `heads` heads starting at head h0.
+size_t group_workspace(const void* q, const void* k, const void* v, const float* beta,
+                       const float* gate, int F, int N, int h0, int heads, int d_k, int d_v,
+                       const vda_options& o, void* out, int dev) {
+  const size_t tokh = (size_t)F * N;  // tokens per head
+  ForwardCall C;
+  plan_forward(false, static_cast<const char*>(q) + h0 * tokh * d_k * 2,
+               static_cast<const char*>(k) + h0 * tokh * d_k * 2,
+               static_cast<const char*>(v) + h0 * tokh * d_v * 2, beta + h0 * tokh, gate + h0, F,
+               N, heads, d_k, d_v, o, static_cast<char*>(out) + h0 * tokh * d_v * 2, dev, &C);
+  return C.ws_bytes;
+}
+
+// vda_forward with its workspace in `scratch`: the heads run in consecutive
+// groups, each as one forward over its heads, as many heads per group as fit.
+int forward_noalloc_impl(const void* q, const void* k, const void* v, const float* beta,
+                         const float* gate, int F, int N, int H, int d_k, int d_v, void* out,
+                         hipStream_t stream) {
+  vda_options o;
+  int st = check_forward(false, q, k, v, beta, gate, F, N, H, d_k, d_v, nullptr, out, &o);
+  if (st != VDA_OK) return st;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return VDA_ERR_HIP;
+  char* base = scratch_ptr(dev);
+  if (!base) return VDA_ERR_HIP;
+  constexpr size_t cap = VDA_NOALLOC_SCRATCH_BYTES;
+  auto fits = [&](int h0, int n) {
+    return group_workspace(q, k, v, beta, gate, F, N, h0, n, d_k, d_v, o, out, dev) <= cap;
+  };
+  // Nothing is enqueued unless every head fits on its own.
+  if (!fits(0, 1)) return VDA_ERR_SCRATCH;
+  // Largest group size that fits, by bisection on the workspace of a group
+  // at the first head (the workspace grows with the heads up to the
+  // statistics' split partials; each group is re-checked below).
+  int g = H;
+  if (!fits(0, H)) {
+    int lo = 1, hi = H;  // fits(lo), !fits(hi)
+    while (hi - lo > 1) {
+      const int mid = lo + (hi - lo) / 2;
+      if (fits(0, mid)) lo = mid;
+      else hi = mid;
+    }
+    g = lo;
+  }
+  const size_t tokh = (size_t)F * N;
+  for (int h0 = 0; h0 < H;) {
+    int n = std::min(g, H - h0);
+    while (n > 1 && !fits(h0, n)) --n;
+    ForwardCall C;
+    plan_forward(false, static_cast<const char*>(q) + h0 * tokh * d_k * 2,
+                 static_cast<const char*>(k) + h0 * tokh * d_k * 2,
+                 static_cast<const char*>(v) + h0 * tokh * d_v * 2, beta + h0 * tokh, gate + h0,
+                 F, N, n, d_k, d_v, o, static_cast<char*>(out) + h0 * tokh * d_v * 2, dev, &C);
+    if (C.ws_bytes > cap) return VDA_ERR_SCRATCH;  // cannot happen: one head fits
+    if (launch_forward(C, base, stream) != hipSuccess) return VDA_ERR_HIP;
+    h0 += n;
+  }
+  return VDA_OK;
+}
+
 // The prompt state: one frame of L tokens per head from the zero state.
 int text_state_impl(const void* k, const void* v, const float* beta, int L, int H, int d_k,
                     int d_v, int rule, int is_f32, float* S_T, hipStream_t stream) {
@@ -573,6 +654,8 @@ const char* vda_status_string(int status) {
     case VDA_ERR_OVERLAP: return "VDA_ERR_OVERLAP: the output overlaps an input";
     case VDA_ERR_HIP: return "VDA_ERR_HIP: the HIP runtime reported an error";
     case VDA_ERR_NOMEM: return "VDA_ERR_NOMEM: workspace allocation failed";
+    case VDA_ERR_SCRATCH:
+      return "VDA_ERR_SCRATCH: one head needs more workspace than the fixed scratch array holds";
     default: return "VDA: unknown status";
   }
 }
@@ -580,6 +663,12 @@ const char* vda_status_string(int status) {
 int vda_forward(const void* q, const void* k, const void* v, const float* beta, const float* gate,
                 int F, int N, int H, int d_k, int d_v, void* out, hipStream_t stream) {
   return forward_impl(false, q, k, v, beta, gate, F, N, H, d_k, d_v, nullptr, out, stream);
+}
+
+int vda_forward_noalloc(const void* q, const void* k, const void* v, const float* beta,
+                        const float* gate, int F, int N, int H, int d_k, int d_v, void* out,
+                        hipStream_t stream) {
+  return forward_noalloc_impl(q, k, v, beta, gate, F, N, H, d_k, d_v, out, stream);
 }
 
 int vda_forward_f32(const float* q, const float* k, const float* v, const float* beta,

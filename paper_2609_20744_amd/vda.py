@@ -30,7 +30,8 @@ HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))
 
 VDA_OK = 0
 STATUS_NAMES = {0: "VDA_OK", 1: "VDA_ERR_NULL", 2: "VDA_ERR_SIZE", 3: "VDA_ERR_UNSUPPORTED",
-                4: "VDA_ERR_ALIGN", 5: "VDA_ERR_OVERLAP", 6: "VDA_ERR_HIP", 7: "VDA_ERR_NOMEM"}
+                4: "VDA_ERR_ALIGN", 5: "VDA_ERR_OVERLAP", 6: "VDA_ERR_HIP", 7: "VDA_ERR_NOMEM",
+                8: "VDA_ERR_SCRATCH"}
 
 _P = ctypes.c_void_p
 _I = ctypes.c_int
@@ -49,6 +50,7 @@ _SIGNATURES = {
     "vda_status_string": (ctypes.c_char_p, [_I]),
     "vda_forward": (_I, [_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _P, _P]),
     "vda_forward_f32": (_I, [_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _P, _P]),
+    "vda_forward_noalloc": (_I, [_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _P, _P]),
     "vda_forward_ex": (_I, [_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _P, _P, _P]),
     "vda_forward_ex_f32": (_I, [_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _P, _P, _P]),
     "vda_text_state": (_I, [_P, _P, _P, _I, _I, _I, _I, _I, _I, _P, _P]),
@@ -105,7 +107,7 @@ def _check(status: int, where: str) -> None:
     if status != VDA_OK:
         if status == 1:
             raise ValueError(f"{where}: {status_string(status)}")
-        if status in (2, 3, 4, 5):
+        if status in (2, 3, 4, 5, 8):
             raise ValueError(f"{where}: {status_string(status)}")
         raise VDAError(status, where)
 
@@ -260,6 +262,35 @@ def text_state(k, v, beta, rule="joint", out=None, stream=None):
                                 RULES[rule], int(dt == torch.float32), out.data_ptr(),
                                 _stream_ptr(dev, stream))
     _check(st, "vda_text_state")
+    return out
+
+
+def forward_noalloc(q, k, v, beta, gate, out=None, stream=None):
+    """vda_forward_noalloc: vda_forward (bf16 tensors) with the library's
+    fixed device scratch array as workspace; the library allocates nothing
+    (out is allocated here by torch when not given)."""
+    torch = _torch()
+    dev = q.device
+    if q.dtype != torch.bfloat16:
+        raise ValueError("vda_forward_noalloc takes bfloat16 q, k, v")
+    if dev.type != "cuda":
+        raise ValueError("VDA runs on the GPU only; tensors must be on a cuda device")
+    for t, n in ((q, "q"), (k, "k"), (v, "v")):
+        _require(t, n, torch.bfloat16, dev)
+    _require(beta, "beta", torch.float32, dev)
+    _require(gate, "gate", torch.float32, dev)
+    lead, F, N, H, d_k, d_v = _shape(q, k, v, beta, gate)
+    if out is None:
+        out = torch.empty(lead + (F, N, d_v), dtype=q.dtype, device=dev)
+    else:
+        _require(out, "out", q.dtype, dev)
+        if tuple(out.shape) != lead + (F, N, d_v):
+            raise ValueError(f"out shape {tuple(out.shape)} must be {lead + (F, N, d_v)}")
+    with torch.cuda.device(dev):
+        st = lib.vda_forward_noalloc(q.data_ptr(), k.data_ptr(), v.data_ptr(), beta.data_ptr(),
+                                     gate.data_ptr(), F, N, H, d_k, d_v, out.data_ptr(),
+                                     _stream_ptr(dev, stream))
+    _check(st, "vda_forward_noalloc")
     return out
 
 
