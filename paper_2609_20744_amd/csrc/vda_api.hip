@@ -252,18 +252,24 @@ Workspace workspace_layout(int F, int H, int d_k, int d_v, vda::SplitPlan plan) 
 }
 
 // Whether the chunk-wise scans beat the frame-by-frame scan for a chunked
-// window, by a cost model fitted to measurements on MI355X at d = 128 (the
-// frame scan ~0.95 us per frame plus ~7 us; the compose launch
-// ~(5 * chunk + 13) us per round of 2 * H * C workgroups over the compute
-// units; the chunk-sequence scan ~2.2 us per chunk).  Measured: 16 heads x
-// 36 frames, 43 us frame by frame against 56 us chunk-wise; 7 heads x 100
-// frames, 98 us against 91 us (chunks of five after one anchor).
-bool chunked_scan_pays(int F, int H, int chunk, int offset) {
+// window, by a cost model fitted per key width to measurements on MI355X
+// (both scans alone, d_v = d_k, chunks of five after one anchor, at 16 heads
+// x 36 frames and 7 heads x 100 frames).  The frame scan costs about
+// a * F + b us; the chunk-wise scans s * (5 * chunk + 13) us per round of
+// 2 * H * C compose workgroups over the compute units plus g us per chunk.
+//   d_k = 128: frame 43.4 / 97.6 us, chunk-wise 56.6 / 90.1 us
+//   d_k =  64: frame 18.5 / 46.4 us, chunk-wise 15.1 / 24.3 us
+//   d_k =  32: frame 13.6 / 33.7 us, chunk-wise 10.8 / 14.5 us
+bool chunked_scan_pays(int F, int H, int d_k, int chunk, int offset) {
   const int C = vda::chunk_count(F, chunk, offset);
   if (C < 2) return false;
+  struct Fit { double a, b, s, g; };
+  const Fit fit = d_k >= 128 ? Fit{0.847, 12.9, 1.042, 2.12}
+                  : d_k >= 64 ? Fit{0.436, 2.8, 0.274, 0.587}
+                              : Fit{0.314, 2.3, 0.247, 0.176};
   const double rounds = std::max(1.0, 2.0 * H * C / (double)current_device_cus());
-  const double chunked_us = rounds * (5.0 * chunk + 13.0) + 2.2 * C;
-  const double frame_us = 0.95 * F + 7.0;
+  const double chunked_us = rounds * fit.s * (5.0 * chunk + 13.0) + fit.g * C;
+  const double frame_us = fit.a * F + fit.b;
   return chunked_us < frame_us;
 }
 
@@ -364,7 +370,7 @@ void plan_forward(bool is_f32, const void* q, const void* k, const void* v, cons
   // the states at chunk boundaries only: chunk-wise scans compute just those,
   // where they are the faster path.
   C.chunked = !is_f32 && !C.frozen && o.window_chunk >= 2 &&
-              chunked_scan_pays(F, H, o.window_chunk, o.window_offset);
+              chunked_scan_pays(F, H, pk, o.window_chunk, o.window_offset);
   C.tiled = !is_f32 && !C.frozen;
   C.c_ws = C.chunked ? round_up(vda::chunked_scan_workspace(F, H, pk, pv, o.window_chunk,
                                                             o.window_offset),

@@ -90,6 +90,13 @@ WORKLOADS = {
 }
 
 
+# The paper's own shard: 56 heads over 8 GPUs (7 per GPU), a 48x84 latent
+# grid and 102 latent frames, 100 of them interior; d = 128 (the head width
+# is not stated).  Timed and checked with the full operator's options.
+PAPER_SHARD = Workload("paper_shard_bf16", 1, 7, 100, 4032, 128, 128, "bf16", 11, grid=(48, 84),
+                       description="48x84 latent grid, 100 interior frames, 7-head shard")
+
+
 def custom(name: str, B: int, H: int, F: int, N: int, d_k: int, d_v: int,
            dtype: str = "bf16", seed: int = 0, **kw) -> Workload:
     """A workload with arbitrary shape (property sweeps, edge cases)."""

@@ -86,3 +86,26 @@ def test_source_hash_ignores_comments_and_layout():
     c = "int f(int x) { return 3 * x; }"
     assert bench._code_only(a) == bench._code_only(b)
     assert bench._code_only(a) != bench._code_only(c)
+
+
+def test_counter_summary_derives_mfma_rates(tmp_path):
+    """Matrix-core counters per kernel instance: mean over dispatches, 512
+    FLOPs per MOPS unit, rate over the dispatch's own duration."""
+    d = tmp_path / "pmc"
+    os.makedirs(d)
+    inv = "void vda::(anonymous namespace)::inverse_kernel<128, true>(float const*, int)"
+    rows = []
+    # two dispatches of 10 us each: 1e6 and 3e6 F32 MOPS units
+    for disp, mops in ((1, 1e6), (2, 3e6)):
+        for cname, val in (("SQ_INSTS_VALU_MFMA_MOPS_F32", mops), ("MfmaUtil", 10.0 * disp)):
+            rows.append(f'{disp},"{inv}","{cname}",{val},1000,11000')
+    (d / "run_counter_collection.csv").write_text(
+        '"Dispatch_Id","Kernel_Name","Counter_Name","Counter_Value","Start_Timestamp",'
+        '"End_Timestamp"\n' + "\n".join(rows) + "\n")
+    s = bench.counter_summary([str(d)])
+    k = s["inverse_kernel<128,true>"]
+    assert k["dispatches"] == 2
+    assert k["mean_duration_us"] == pytest.approx(10.0)
+    assert k["counters"]["MfmaUtil"] == pytest.approx(15.0)
+    assert k["mfma_f32_tflops"] == pytest.approx(2e6 * 512 / 1e-5 / 1e12)
+    assert k["frac_f32_mfma_peak"] == pytest.approx(k["mfma_f32_tflops"] / 157.3)

@@ -273,3 +273,42 @@ def test_full_operator_paper_shard(V, H, dk, dv):
     err = rel_max_err(got, exp)
     _log(f"  rel err {err:.2e}")
     assert err <= tol_for(w), err
+
+
+@pytest.mark.parametrize("rule", ["joint", "frozen"])
+def test_full_operator_paper_shard_full_size(V, rule):
+    """The paper's own shard at full size: 7 heads x 100 interior frames x
+    4032 tokens (48 x 84 grid), d = 128, with decay, a text state and the
+    paper's window, in the launch configuration bench.py times (the joint
+    rule takes the chunk-wise scans here).  The oracle's states come from
+    every frame of every head; outputs are compared at the first and last
+    token of every frame and at 256 random (frame, token) positions per
+    head."""
+    import torch
+    w = I.PAPER_SHARD
+    _log(f"full operator paper shard full size rule={rule}: H={w.heads} F={w.F} N={w.N}")
+    x = I.make_inputs(w)
+    alpha, S_T = I.make_decay(w), I.make_text_state(w)
+    d = device_inputs(w, x)
+    y = V.forward(d["q"], d["k"], d["v"], d["beta"], d["gate"], alpha=to_device(alpha, "f32"),
+                  text_state=to_device(S_T, "f32"), window=PAPER_WINDOW, rule=rule)
+    torch.cuda.synchronize()
+    del d
+    windows = O.local_windows(w.F, *PAPER_WINDOW)
+    rng = np.random.default_rng(11)
+    worst = 0.0
+    for h in range(w.heads):
+        xo = oracle_inputs(w, I.make_inputs(w, heads=[h]))
+        As, Bs = O.head_statistics(xo["k"][0], xo["v"][0], xo["beta"][0])
+        St = O.gathered_states_ex(As, Bs, S_T[h].astype(np.float64),
+                                  alpha[h].astype(np.float64), windows, rule=rule,
+                                  U=w.N if rule == "frozen" else None)
+        frames = np.concatenate([np.repeat(np.arange(w.F), 2), rng.integers(0, w.F, 256)])
+        toks = np.concatenate([np.tile([0, w.N - 1], w.F), rng.integers(0, w.N, 256)])
+        o = np.einsum("sjc,sc->sj", St[frames], xo["q"][0][frames, toks])
+        exp = O.rmsnorm_gate(o, float(xo["gate"][0]))
+        got = from_device(y[h][torch.from_numpy(frames).cuda(), torch.from_numpy(toks).cuda()])
+        err = rel_max_err(got, exp)
+        worst = max(worst, err)
+        assert err <= tol_for(w), (h, err)
+    _log(f"  rel max-norm error over the sampled outputs {worst:.3e}")
