@@ -22,15 +22,19 @@ void inverse_kernel(const float* A_part, unsigned first_split, int plan_splits, 
                     float* B_part, size_t b_mat, size_t b_stride) {
   constexpr int NB = DK / 16;
   constexpr int W = NB < 4 ? NB : 4;
-  __shared__ __align__(16) float piv[2][NB][64 * 4];  // [buffer][block j][lane][4]
+  __shared__ __align__(16) float piv[3][NB][64 * 4];  // [buffer][block j][lane][4]
 
   const int tid = threadIdx.x;
   if (blockIdx.x >= gridDim.x - extra) {
     // One of the workgroups past the matrices: fold the token-range partials
-    // of B_t of split frame first_split + (its index) into the first partial
-    // (in place), alongside the inversions.
-    const size_t f = first_split + (blockIdx.x - (gridDim.x - extra));
-    inv::fold_b_partials(B_part + f * b_mat, plan_splits, b_mat, b_stride, tid, 64 * W);
+    // of B_t of split frame first_split + (its index) / 4, quarter (its
+    // index) % 4 of the matrix, into the first partial (in place), alongside
+    // the inversions.
+    const unsigned e = blockIdx.x - (gridDim.x - extra);
+    const size_t f = first_split + e / 4;
+    const size_t quarter = b_mat / 4;
+    inv::fold_b_partials(B_part + f * b_mat, plan_splits, (e % 4) * quarter,
+                         (e % 4 + 1) * quarter, b_stride, tid, 64 * W);
     return;
   }
   const size_t base = (size_t)blockIdx.x * (DK * DK);
@@ -50,8 +54,9 @@ hipError_t launch_frame_inverse(const float* A_part, float* B_part, SplitPlan pl
   const size_t part_stride = (size_t)plan.tail * d_k * d_k;
   const size_t b_mat = (size_t)d_v * d_k;
   const size_t b_stride = (size_t)plan.tail * b_mat;
-  // One workgroup per matrix, then one per split frame to fold its B partials.
-  const unsigned extra = splits > 1 ? (unsigned)plan.tail : 0u;
+  // One workgroup per matrix, then four per split frame to fold its B
+  // partials (a quarter of the matrix each, one memory round trip).
+  const unsigned extra = splits > 1 ? 4u * (unsigned)plan.tail : 0u;
   const dim3 grid((unsigned)count + extra);
   switch (d_k) {
     case 32:

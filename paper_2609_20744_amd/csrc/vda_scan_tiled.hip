@@ -392,8 +392,9 @@ void scan_tiled_kernel(TiledScanArgs a) {
 // k values of a lane slot are two contiguous runs of row n) before any
 // thread writes.  Under a split plan the frames from first_split on are the
 // sums of plan_splits token-range partials (partial s at A + s *
-// part_stride), and `extra` workgroups after the frames fold the B_t
-// partials of those frames in place, as the inverse step does.
+// part_stride), and `extra` workgroups after the frames (four per split
+// frame, a quarter of B_t each) fold the B_t partials of those frames in
+// place, as the inverse step does.
 template <int DK>
 __global__ __launch_bounds__(kThreads)
 void frozen_tiles_kernel(float* __restrict__ A, const float* __restrict__ alpha, float inv_u,
@@ -402,14 +403,53 @@ void frozen_tiles_kernel(float* __restrict__ A, const float* __restrict__ alpha,
   constexpr int SLOTS = DK * DK / 8;                          // 8 elements per lane slot
   constexpr int SPT = (SLOTS + kThreads - 1) / kThreads;      // slots per thread
   const int tid = threadIdx.x;
-  if (blockIdx.x >= gridDim.x - extra) {
-    const size_t f = first_split + (blockIdx.x - (gridDim.x - extra));
-    inv::fold_b_partials(B_part + f * b_mat, plan_splits, b_mat, b_stride, tid, kThreads);
+  if (blockIdx.x >= gridDim.x - extra) {  // four workgroups per split frame
+    const unsigned e = blockIdx.x - (gridDim.x - extra);
+    const size_t f = first_split + e / 4;
+    const size_t quarter = b_mat / 4;
+    inv::fold_b_partials(B_part + f * b_mat, plan_splits, (e % 4) * quarter,
+                         (e % 4 + 1) * quarter, b_stride, tid, kThreads);
     return;
   }
   const int splits = blockIdx.x >= first_split ? plan_splits : 1;
   float* a = A + (size_t)blockIdx.x * DK * DK;
   const float* al = alpha != nullptr ? alpha + (size_t)blockIdx.x * DK : nullptr;
+  // Row segment (n, k0 .. k0 + 3) of slot i, half h: the eight k values of a
+  // lane slot are two contiguous runs of row n (A is symmetric).  All of a
+  // partial's segments are loaded in one memory round trip, and the
+  // token-range partials are added in split order.
+  auto seg = [&](int i, int h) -> size_t {
+    const int sl = tid + kThreads * i;
+    const int lane = sl % 64, tile = sl / 64;
+    const int nb = tile / (DK / 32), ks = tile % (DK / 32);
+    const int n = 16 * nb + lane % 16, g = lane / 16;
+    return (size_t)n * DK + 32 * ks + 16 * h + 4 * g;
+  };
+  float4 r[SPT][2];
+#pragma unroll
+  for (int i = 0; i < SPT; ++i)
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+      if (tid + kThreads * i < SLOTS) r[i][h] = *reinterpret_cast<const float4*>(a + seg(i, h));
+  for (int sp = 1; sp < splits; ++sp) {
+    float4 x[SPT][2];
+#pragma unroll
+    for (int i = 0; i < SPT; ++i)
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+        if (tid + kThreads * i < SLOTS)
+          x[i][h] = *reinterpret_cast<const float4*>(a + sp * part_stride + seg(i, h));
+#pragma unroll
+    for (int i = 0; i < SPT; ++i)
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+        if (tid + kThreads * i < SLOTS) {
+          r[i][h].x += x[i][h].x;
+          r[i][h].y += x[i][h].y;
+          r[i][h].z += x[i][h].z;
+          r[i][h].w += x[i][h].w;
+        }
+  }
   float v[SPT][8];
 #pragma unroll
   for (int i = 0; i < SPT; ++i) {
@@ -421,15 +461,7 @@ void frozen_tiles_kernel(float* __restrict__ A, const float* __restrict__ alpha,
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       const int k0 = 32 * ks + 16 * h + 4 * g;
-      float4 r = *reinterpret_cast<const float4*>(a + (size_t)n * DK + k0);
-      for (int sp = 1; sp < splits; ++sp) {  // token-range partials, in split order
-        const float4 x = *reinterpret_cast<const float4*>(a + sp * part_stride + (size_t)n * DK + k0);
-        r.x += x.x;
-        r.y += x.y;
-        r.z += x.z;
-        r.w += x.w;
-      }
-      const float rv[4] = {r.x, r.y, r.z, r.w};
+      const float rv[4] = {r[i][h].x, r[i][h].y, r[i][h].z, r[i][h].w};
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int k = k0 + e;
@@ -514,7 +546,7 @@ hipError_t launch_frozen_tiles(float* A, float* B_part, SplitPlan plan, const fl
   const size_t part_stride = (size_t)plan.tail * d_k * d_k;  // partial p of frame f: f + p * tail
   const size_t b_mat = (size_t)d_v * d_k;
   const size_t b_stride = (size_t)plan.tail * b_mat;
-  const unsigned extra = splits > 1 ? (unsigned)plan.tail : 0u;
+  const unsigned extra = splits > 1 ? 4u * (unsigned)plan.tail : 0u;
   const dim3 grid((unsigned)count + extra);
   const float inv_u = 1.0f / (float)tokens;
 #define VDA_FROZEN_TILES(DK)                                                                   \

@@ -283,6 +283,12 @@ void stats_bf16_kernel(const uint16_t* __restrict__ K, const uint16_t* __restric
 }
 
 // fp32 storage: plain fp32 products and sums (no rounding of beta * k).
+// The output X = [A_t; B_t] ((d_k + d_v) x d_k) is dealt out to the threads
+// in R x C register tiles (C = 8 columns, 4 for d_k = 32), so each token
+// costs a thread R + C LDS reads for R * C fused multiply-adds.  A tile of
+// 32 tokens of k, v and beta is loaded by range-checked buffer loads that
+// are all in flight together (tokens past the range read as zero), then
+// staged in LDS; every output sums its tokens in order.
 template <int DK, int DV>
 __global__ __launch_bounds__(kThreads)
 void stats_f32_kernel(const float* __restrict__ K, const float* __restrict__ V,
@@ -291,50 +297,74 @@ void stats_f32_kernel(const float* __restrict__ K, const float* __restrict__ V,
                       float* __restrict__ A_part, float* __restrict__ B_part) {
   constexpr int DX = DK + DV;
   constexpr int T = 32;
-  constexpr int OPT = DX * DK / kThreads;  // outputs per thread
-  __shared__ float xs[T][DX];
-  __shared__ float ys[T][DK];
+  constexpr int C = DK >= 64 ? 8 : 4;          // columns per thread
+  constexpr int CG = DK / C;                   // column groups
+  constexpr int R = DX * CG / kThreads;        // rows per thread
+  static_assert(R * C * kThreads == DX * DK, "register tiles cover the output");
+  constexpr int LPT = T * DX / kThreads;       // loaded elements per thread and tile
+  static_assert(LPT * kThreads == T * DX, "tile loads divide evenly");
+  __shared__ __align__(16) float xs[T][DX];
+  __shared__ __align__(16) float ys[T][DK];
 
   const StatsItem it = stats_item(blockIdx.x, fh_count, tail, splits, N, tokens_per_split);
-  const unsigned fh = it.fh;
-  const int n_begin = it.n_begin;
-  const int n_end = it.n_end;
+  const unsigned fh = (unsigned)uniform((int)it.fh);
+  const int n_begin = uniform(it.n_begin);
+  const int n_end = uniform(it.n_end);
   const int tid = threadIdx.x;
+  const __amdgpu_buffer_rsrc_t krsrc = make_rsrc(K + (size_t)fh * N * DK, (uint32_t)(n_end * DK * 4));
+  const __amdgpu_buffer_rsrc_t vrsrc = make_rsrc(V + (size_t)fh * N * DV, (uint32_t)(n_end * DV * 4));
+  const __amdgpu_buffer_rsrc_t brsrc = make_rsrc(beta + (size_t)fh * N, (uint32_t)(n_end * 4));
+  const int j0 = (tid % CG) * C;
+  const int x0 = (tid / CG) * R;
 
-  float acc[OPT];
+  float acc[R][C];
 #pragma unroll
-  for (int m = 0; m < OPT; ++m) acc[m] = 0.f;
+  for (int r = 0; r < R; ++r)
+#pragma unroll
+    for (int c = 0; c < C; ++c) acc[r][c] = 0.f;
 
   for (int n0 = n_begin; n0 < n_end; n0 += T) {
-    lds_barrier();
-    for (int idx = tid; idx < T * DX; idx += kThreads) {
+    float xv[LPT], bv[LPT];
+#pragma unroll
+    for (int l = 0; l < LPT; ++l) {
+      const int idx = tid + l * kThreads;
       const int e = idx / DX, c = idx % DX;
-      const int n = n0 + e;
-      float x = 0.f;
-      if (n < n_end)
-        x = c < DK ? K[((size_t)fh * N + n) * DK + c] : V[((size_t)fh * N + n) * DV + (c - DK)];
-      xs[e][c] = x;
-      if (c < DK) ys[e][c] = n < n_end ? x * beta[(size_t)fh * N + n] : 0.f;
+      const uint32_t n = (uint32_t)(n0 + e);
+      xv[l] = c < DK ? load_f32(krsrc, (n * DK + c) * 4u) : load_f32(vrsrc, (n * DV + c - DK) * 4u);
+      bv[l] = load_f32(brsrc, n * 4u);
+    }
+    lds_barrier();  // the previous tile's reads are done
+#pragma unroll
+    for (int l = 0; l < LPT; ++l) {
+      const int idx = tid + l * kThreads;
+      const int e = idx / DX, c = idx % DX;
+      xs[e][c] = xv[l];
+      if (c < DK) ys[e][c] = xv[l] * bv[l];
     }
     lds_barrier();
+#pragma unroll 4
     for (int e = 0; e < T; ++e) {
+      float xr[R], yc[C];
 #pragma unroll
-      for (int m = 0; m < OPT; ++m) {
-        const int o = tid + m * kThreads;
-        acc[m] = fmaf(xs[e][o / DK], ys[e][o % DK], acc[m]);
-      }
+      for (int r = 0; r < R; ++r) xr[r] = xs[e][x0 + r];
+#pragma unroll
+      for (int c = 0; c < C; ++c) yc[c] = ys[e][j0 + c];
+#pragma unroll
+      for (int r = 0; r < R; ++r)
+#pragma unroll
+        for (int c = 0; c < C; ++c) acc[r][c] = fmaf(xr[r], yc[c], acc[r][c]);
     }
   }
   float* Ab = A_part + (size_t)it.slot * (DK * DK);
   float* Bb = B_part + (size_t)it.slot * (DV * DK);
 #pragma unroll
-  for (int m = 0; m < OPT; ++m) {
-    const int o = tid + m * kThreads;
-    const int x = o / DK, j = o % DK;
-    if (x < DK)
-      Ab[x * DK + j] = acc[m];
-    else
-      Bb[(x - DK) * DK + j] = acc[m];
+  for (int r = 0; r < R; ++r) {
+    const int x = x0 + r;
+    float* dst = x < DK ? Ab + (size_t)x * DK + j0 : Bb + (size_t)(x - DK) * DK + j0;
+#pragma unroll
+    for (int c = 0; c < C; c += 4)
+      *reinterpret_cast<float4*>(dst + c) = make_float4(acc[r][c], acc[r][c + 1], acc[r][c + 2],
+                                                        acc[r][c + 3]);
   }
 }
 
