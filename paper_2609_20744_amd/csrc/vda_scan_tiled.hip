@@ -147,8 +147,11 @@ struct TiledScanArgs {
 // last frame (reverse).  The additive term comes after the product here, so
 // step j adds J of the previous chunk (loaded one step late) to the product
 // before it stores and splits the state; the last step's product is unused.
+// At most 256 registers per lane (two waves per SIMD), so two workgroups
+// share a compute unit when there are more chains' row blocks than compute
+// units (e.g. 24 heads: 384 workgroups) instead of running in two rounds.
 template <int DK, bool DECAY, bool CHUNKED>
-__global__ __launch_bounds__(kThreads)
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2)))
 void scan_tiled_kernel(TiledScanArgs a) {
   static_assert(!(CHUNKED && DECAY), "chunk maps already hold the decay");
   const int F = a.F, DV = a.DV, C = a.C;
