@@ -13,8 +13,10 @@
 // loads straight from HBM, two groups in flight per wave), O^T = S~ Q^T is
 // accumulated in fp32 by v_mfma_f32_16x16x32_bf16, and the RMSNorm over the
 // d_v outputs of a token is a lane-local sum plus two cross-lane exchanges.
-// The normalised, gated values are rounded to bf16 and stored 16 bytes per
-// lane (a cross-lane swap first gathers 8 consecutive channels in a lane).
+// The normalised, gated values are rounded to bf16 into a per-wave LDS tile
+// of the group's 16 token rows, from which each 16-byte-per-lane streaming
+// store writes consecutive whole token rows (one contiguous run of up to
+// 1 KB).
 #include "vda_common.h"
 #include "vda_launch.h"
 
