@@ -90,7 +90,7 @@ def instance_of(w):
     return {"frame_stats": f"stats_bf16_kernel<{dk},{dv}>",
             "frame_inverse": f"inverse_kernel<{dk},true>",
             "state_scan": f"scan_tiled_kernel<{dk},false,false>",
-            "readout": f"readout_bf16_kernel<{dk},{dv},false>",
+            "readout": f"readout_bf16_kernel<{dk},{dv},false,false>",
             "prep_qnorm": f"prep_qnorm_kernel<{dk}>"}
 
 

@@ -158,8 +158,8 @@ typedef enum {
 
 /*
  * Options of vda_forward_ex.  A NULL pointer to this struct, or all fields at
- * their defaults (rule 0, NULL pointers, chunk 1, radius 0, offset 0), give
- * exactly vda_forward.
+ * their defaults (rule 0, NULL pointers, chunk 1, radius 0, offset 0,
+ * out_heads 0), give exactly vda_forward.
  *  - rule: a vda_rule.
  *  - alpha: NULL (alpha = 1) or a DEVICE pointer to [H][F][d_k] fp32 channel
  *    decays in [0, 1] (16-byte aligned), one per frame and key channel:
@@ -181,6 +181,16 @@ typedef enum {
  *    channel, computed upstream and applied after RMSNorm,
  *    out[t][u][c] = G^L[t][u][c] * RMSNorm(S~_t q[t][u])[c].  It replaces
  *    the per-head gate, whose pointer may then be NULL.
+ *  - out_heads: the layout of out.  0: frame-major per head, [H][F][N][d_v]
+ *    (as vda_forward).  out_heads > 0: token-major, the layout of the
+ *    attention output that the model's output projection reads (the final
+ *    layout conversion of the epilogue, Sec. 4): the H head problems are
+ *    H / out_heads clips of out_heads heads each, and out is
+ *    [H / out_heads][F][N][out_heads * d_v], head problem b * out_heads + h
+ *    writing channels h * d_v .. h * d_v + d_v - 1 of its clip's rows.  The
+ *    inputs and gate_tokens keep their per-head layouts.  VDA_ERR_SIZE if
+ *    out_heads < 0, if it does not divide H, or if (N + 64) * out_heads * d_v
+ *    elements of one frame exceed 2^31 bytes.
  */
 typedef struct vda_options {
   int rule;
@@ -190,6 +200,7 @@ typedef struct vda_options {
   int window_radius;
   int window_offset;
   const void* gate_tokens;
+  int out_heads;
 } vda_options;
 
 /*

@@ -284,10 +284,11 @@ int check_options(const vda_options* o, vda_options* out) {
   d.window_radius = 0;
   d.window_offset = 0;
   d.gate_tokens = nullptr;
+  d.out_heads = 0;
   if (o) d = *o;
   if (d.rule != VDA_RULE_JOINT && d.rule != VDA_RULE_FROZEN_SCALED) return VDA_ERR_UNSUPPORTED;
   if (d.window_chunk < 1 || d.window_radius < 0 || d.window_offset < 0 ||
-      d.window_offset >= d.window_chunk)
+      d.window_offset >= d.window_chunk || d.out_heads < 0)
     return VDA_ERR_SIZE;
   if (!aligned(d.alpha, 16) || !aligned(d.text_state, 16) || !aligned(d.gate_tokens, 16))
     return VDA_ERR_ALIGN;
@@ -331,6 +332,12 @@ int check_forward(bool is_f32, const void* q, const void* k, const void* v, cons
     return VDA_ERR_ALIGN;
   // The window arithmetic stays within 32 bits.
   if ((long long)F + 2LL * (o.window_radius + 1) * o.window_chunk > 0x3fffffffLL) return VDA_ERR_SIZE;
+  // A token-major output holds whole clips of out_heads heads, and one
+  // frame's rows of it stay within 32-bit byte offsets.
+  if (o.out_heads > 0 &&
+      (H % o.out_heads != 0 ||
+       (long long)(N + 64) * o.out_heads * d_v * (is_f32 ? 4 : 2) > 0x7fffffffLL))
+    return VDA_ERR_SIZE;
   const size_t es = is_f32 ? 4 : 2;
   const size_t tok = (size_t)H * F * N;
   const Range ro = range_of(out, tok * d_v * es);
@@ -383,7 +390,7 @@ void plan_forward(bool is_f32, const void* q, const void* k, const void* v, cons
   C.t_pad = pad_any && o.text_state ? round_up((size_t)H * pv * pk * 4, 256) : 0;
   C.t_tmp = pad_any && o.text_state ? round_up((size_t)H * d_v * pk * 4, 256) : 0;
   C.g_pad = o.gate_tokens && pv != d_v ? round_up(tok * pv * es, 256) : 0;
-  C.ws_bytes = round_up(C.w.total, 256) + 2 * C.qk_pad + 2 * C.v_pad + C.a_pad + C.t_pad +
+  C.ws_bytes = round_up(C.w.total, 256) + 2 * C.qk_pad + C.v_pad + C.a_pad + C.t_pad +
                C.t_tmp + C.g_pad + C.c_ws;
 }
 
@@ -402,7 +409,7 @@ hipError_t launch_forward(const ForwardCall& C, char* base, hipStream_t stream) 
   const void* qx = C.q;
   const void* kx = C.k;
   const void* vx = C.v;
-  void* ox = C.out;
+
   const float* alpha_x = o.alpha;
   const float* ts_x = o.text_state;
 
@@ -420,9 +427,8 @@ hipError_t launch_forward(const ForwardCall& C, char* base, hipStream_t stream) 
     void* vp = pad_base + 2 * C.qk_pad;
     e = vda::launch_pad_rows(C.v, vp, (long long)tok, (int)(d_v * es), (int)(pv * es), stream);
     vx = vp;
-    ox = pad_base + 2 * C.qk_pad + C.v_pad;
   }
-  char* opt_base = pad_base + 2 * C.qk_pad + 2 * C.v_pad;
+  char* opt_base = pad_base + 2 * C.qk_pad + C.v_pad;
   void* chunk_work = opt_base + C.a_pad + C.t_pad + C.t_tmp + C.g_pad;
   const void* gt_x = o.gate_tokens;
   if (C.g_pad && e == hipSuccess) {  // output gates [tok][d_v] -> [tok][32], zero channels added
@@ -480,11 +486,12 @@ hipError_t launch_forward(const ForwardCall& C, char* base, hipStream_t stream) 
   go.radius = o.window_radius;
   go.offset = o.window_offset;
   go.gate_tokens = gt_x;
+  go.out_heads = o.out_heads > 0 ? o.out_heads : 1;
+  // The readout writes the true d_v channels of each head straight into out
+  // (a padded head's zero channels are not stored).
   if (e == hipSuccess)
-    e = vda::launch_readout(C.is_f32, qx, S_fwd, S_rev, C.gate, F, N, H, pk, pv, d_v, go, ox,
+    e = vda::launch_readout(C.is_f32, qx, S_fwd, S_rev, C.gate, F, N, H, pk, pv, d_v, go, C.out,
                             stream);
-  if (e == hipSuccess && ox != C.out)
-    e = vda::launch_unpad_rows(ox, C.out, (long long)tok, (int)(pv * es), (int)(d_v * es), stream);
   return e;
 }
 

@@ -107,11 +107,17 @@ struct GatherOptions {
   // [H][F][N][d_v] output gate G^L per token and channel (the storage type
   // of q and out), or null: the per-head gate applies.
   const void* gate_tokens = nullptr;
+  // Output layout: head problems per clip of a token-major output
+  // [H / out_heads][F][N][out_heads * d_v_norm] (head problem b * out_heads
+  // + h writes channels h * d_v_norm ..); 1 is frame-major per head,
+  // [H][F][N][d_v_norm].
+  int out_heads = 1;
 };
 
 // Steps a5-a7, Eq. A.4 / 1a / 1c: gather, readout, RMSNorm and gate.
-// d_v_norm: the number of channels RMSNorm averages over (d_v, or fewer
-// when the trailing value channels are zero padding).
+// d_v_norm: the true number of value channels, which RMSNorm averages over
+// and out holds per head (d_v, or fewer when the trailing value channels of
+// the padded heads are zero padding: only the first d_v_norm are written).
 hipError_t launch_readout(bool is_f32, const void* q, const float* S_fwd, const float* S_rev,
                           const float* gate, int F, int N, int H, int d_k, int d_v,
                           int d_v_norm, const GatherOptions& g, void* out, hipStream_t stream);
@@ -122,11 +128,9 @@ hipError_t launch_readout(bool is_f32, const void* q, const float* S_fwd, const 
 hipError_t launch_text_state(const float* B, const float* Inv, int H, int pk, int pv, int d_k,
                              int d_v, float scale, float* S, hipStream_t stream);
 
-// Row-wise channel padding (zero fill) and its inverse, in 16-byte pieces.
+// Row-wise channel padding (zero fill), in 16-byte pieces.
 hipError_t launch_pad_rows(const void* src, void* dst, long long rows, int src_bytes,
                            int dst_bytes, hipStream_t stream);
-hipError_t launch_unpad_rows(const void* src, void* dst, long long rows, int src_bytes,
-                             int dst_bytes, hipStream_t stream);
 
 // Token count of each statistics split (a multiple of the 64-token tile).
 inline int stats_tokens_per_split(int N, int splits) {

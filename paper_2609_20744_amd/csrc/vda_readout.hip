@@ -16,7 +16,9 @@
 // The normalised, gated values are rounded to bf16 into a per-wave LDS tile
 // of the group's 16 token rows, from which each 16-byte-per-lane streaming
 // store writes consecutive whole token rows (one contiguous run of up to
-// 1 KB).
+// 1 KB when the output is frame-major per head; with the token-major output
+// of the epilogue's layout conversion, a head's rows sit out_heads * d_v
+// apart and each is one run of d_v values).
 #include "vda_common.h"
 #include "vda_launch.h"
 
@@ -56,12 +58,14 @@ __device__ __forceinline__ void bridge_decay(const float* alpha, int h, int F, i
   }
 }
 
-template <int DK, int DV, bool TOKGATE>
+// GENOUT: the token-major output or a padded narrow head (row stride and
+// stored channels at run time); otherwise frame-major rows of DV channels.
+template <int DK, int DV, bool TOKGATE, bool GENOUT>
 __global__ __launch_bounds__(kThreads, 2)
 void readout_bf16_kernel(const uint16_t* __restrict__ Q, const float* __restrict__ S_fwd,
                          const float* __restrict__ S_rev, const float* __restrict__ gate,
                          int F, int N, int chunks, int tokens_per_chunk, unsigned nwg,
-                         float inv_norm, const float* __restrict__ alpha, int wchunk,
+                         int dvo, int oh, const float* __restrict__ alpha, int wchunk,
                          int wradius, int woffset, const uint16_t* __restrict__ gtok,
                          uint16_t* __restrict__ out) {
   constexpr int SLD = DK + 8;  // bf16 row stride of S~ in LDS
@@ -119,7 +123,13 @@ void readout_bf16_kernel(const uint16_t* __restrict__ Q, const float* __restrict
       sop[mb][kb] = *reinterpret_cast<const bf16x8*>(&st[(mb * 16 + li) * SLD + kb * 32 + lg * 8]);
 
   const uint16_t* qbase = Q + (size_t)fh * N * DK;
-  uint16_t* obase = out + (size_t)fh * N * DV;
+  // This frame's output rows: dvo channels at row stride oh * dvo, from
+  // head h % oh of clip h / oh (frame-major per head when oh = 1).
+  const unsigned ohu = GENOUT ? (unsigned)oh : 1u, hp = fh / F, fr = fh % F;
+  const int dvw = GENOUT ? dvo : DV;
+  const uint32_t ors = ohu * (uint32_t)dvw;
+  uint16_t* obase = out + (((size_t)(hp / ohu) * F + fr) * N * ohu + hp % ohu) * dvw;
+  const float inv_norm = 1.0f / (float)dvw;
 
   // The frame's tokens go in 64-token super-groups, dealt out to its
   // `chunks` workgroups in turn (super-group c, c + chunks, ...), so the
@@ -130,7 +140,9 @@ void readout_bf16_kernel(const uint16_t* __restrict__ Q, const float* __restrict
   // Rows past the frame are clamped onto its last row (always valid
   // memory); their outputs are dropped by the range-checked stores, so
   // loads and stores need no branches.
-  constexpr int kQ = TOKGATE ? 1 : 2;  // the gated variant keeps its gate loads in the budget
+  // The gated and the general-output variants keep their extra registers in
+  // the budget with one group in flight.
+  constexpr int kQ = TOKGATE || GENOUT ? 1 : 2;
   const int S = 64 * chunks;
   uint4 qr[kQ][KB];
   auto load_q = [&](int nq, uint4 (&qv)[KB]) {
@@ -144,7 +156,8 @@ void readout_bf16_kernel(const uint16_t* __restrict__ Q, const float* __restrict
   // the frame read as zero).
   const __amdgpu_buffer_rsrc_t grsrc =
       make_rsrc(TOKGATE ? gtok + (size_t)fh * N * DV : Q, TOKGATE ? (uint32_t)N * DV * 2u : 0u);
-  const __amdgpu_buffer_rsrc_t orsrc = make_rsrc(obase, (uint32_t)N * DV * 2u);
+  const __amdgpu_buffer_rsrc_t orsrc =
+      make_rsrc(obase, ((uint32_t)(N - 1) * ors + (uint32_t)dvw) * 2u);
 
   const int n_first = chunk * 64 + wave * 16;
   if (n_first >= N) return;
@@ -213,7 +226,9 @@ void readout_bf16_kernel(const uint16_t* __restrict__ Q, const float* __restrict
       for (int r0 = 0; r0 < 16; r0 += RPI) {
         const int tok = r0 + lane / CPR, ch = lane % CPR;
         const u32x4 v = *reinterpret_cast<const u32x4*>(&tile[tok * OLD + ch * 8]);
-        store_b128_stream(orsrc, ((uint32_t)(ng + tok) * DV + ch * 8) * 2u, v);
+        // Channels past dvo (zero padding of a narrow head) are not stored.
+        store_b128_stream(orsrc, !GENOUT || ch * 8 < dvw ? ((uint32_t)(ng + tok) * ors + ch * 8) * 2u
+                                                        : kOutOfRange, v);
       }
     }
   }
@@ -225,7 +240,7 @@ template <int DK, int DV, bool TOKGATE>
 __global__ __launch_bounds__(kThreads)
 void readout_f32_kernel(const float* __restrict__ Q, const float* __restrict__ S_fwd,
                         const float* __restrict__ S_rev, const float* __restrict__ gate,
-                        int F, int N, int chunks, int tokens_per_chunk, float inv_norm,
+                        int F, int N, int chunks, int tokens_per_chunk, int dvo, int oh,
                         const float* __restrict__ alpha, int wchunk, int wradius, int woffset,
                         const float* __restrict__ gtok, float* __restrict__ out) {
   constexpr int SLD = DK + 1;
@@ -239,6 +254,10 @@ void readout_f32_kernel(const float* __restrict__ Q, const float* __restrict__ S
   const int n_end = min(N, n_begin + tokens_per_chunk);
   const float g = TOKGATE ? 1.0f : gate[fh / F];
   const int tid = threadIdx.x;
+  const float inv_norm = 1.0f / (float)dvo;
+  // Output rows as in readout_bf16_kernel.
+  const size_t ors = (size_t)oh * dvo;
+  float* obase = out + (((size_t)(fh / F / oh) * F + fh % F) * N * oh + (fh / F) % oh) * dvo;
 
   // Gather (Eq. A.4), as in readout_bf16_kernel.
   const int h = (int)(fh / F), f = (int)(fh % F);
@@ -279,8 +298,9 @@ void readout_f32_kernel(const float* __restrict__ Q, const float* __restrict__ S
     if (n < n_end) {
 #pragma unroll
       for (int m = 0; m < VPT; ++m) {
-        const size_t idx = ((size_t)fh * N + n) * DV + part + 16 * m;
-        out[idx] = TOKGATE ? o[m] * scale * gtok[idx] : o[m] * scale;
+        const int c = part + 16 * m;
+        const size_t idx = ((size_t)fh * N + n) * DV + c;
+        if (c < dvo) obase[(size_t)n * ors + c] = TOKGATE ? o[m] * scale * gtok[idx] : o[m] * scale;
       }
     }
   }
@@ -299,28 +319,35 @@ template <int DK, int DV>
 hipError_t launch_readout_t(bool is_f32, const void* q, const float* S_fwd, const float* S_rev,
                             const float* gate, int F, int N, int H, int d_v_norm,
                             const GatherOptions& go, void* out, hipStream_t stream) {
-  const float inv_norm = 1.0f / (float)d_v_norm;
   const long long fh_count = (long long)H * F;
   const int chunks = readout_chunks(fh_count, N);
   int tpc = (N + chunks - 1) / chunks;
   tpc = ((tpc + 63) / 64) * 64;
   const dim3 grid((unsigned)(fh_count * chunks));
-#define VDA_READOUT_LAUNCH(TG)                                                                     \
+  const bool genout = go.out_heads > 1 || d_v_norm != DV;
+#define VDA_READOUT_LAUNCH(TG, GO)                                                                 \
   if (is_f32)                                                                                      \
     hipLaunchKernelGGL((readout_f32_kernel<DK, DV, TG>), grid, dim3(kThreads), 0, stream,          \
                        static_cast<const float*>(q), S_fwd, S_rev, gate, F, N, chunks, tpc,       \
-                       inv_norm, go.alpha, go.chunk, go.radius, go.offset,                         \
+                       d_v_norm, go.out_heads, go.alpha, go.chunk, go.radius, go.offset,           \
                        static_cast<const float*>(go.gate_tokens), static_cast<float*>(out));      \
   else                                                                                             \
-    hipLaunchKernelGGL((readout_bf16_kernel<DK, DV, TG>), grid, dim3(kThreads), 0, stream,         \
+    hipLaunchKernelGGL((readout_bf16_kernel<DK, DV, TG, GO>), grid, dim3(kThreads), 0, stream,     \
                        static_cast<const uint16_t*>(q), S_fwd, S_rev, gate, F, N, chunks, tpc,    \
-                       (unsigned)(fh_count * chunks), inv_norm, go.alpha, go.chunk, go.radius,     \
+                       (unsigned)(fh_count * chunks), d_v_norm, go.out_heads, go.alpha, go.chunk,  \
+                       go.radius,                                                                  \
                        go.offset, static_cast<const uint16_t*>(go.gate_tokens),                    \
                        static_cast<uint16_t*>(out));
   if (go.gate_tokens != nullptr) {
-    VDA_READOUT_LAUNCH(true)
+    if (genout) {
+      VDA_READOUT_LAUNCH(true, true)
+    } else {
+      VDA_READOUT_LAUNCH(true, false)
+    }
+  } else if (genout) {
+    VDA_READOUT_LAUNCH(false, true)
   } else {
-    VDA_READOUT_LAUNCH(false)
+    VDA_READOUT_LAUNCH(false, false)
   }
 #undef VDA_READOUT_LAUNCH
   return hipGetLastError();

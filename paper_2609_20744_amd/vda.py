@@ -41,7 +41,7 @@ class VdaOptions(ctypes.Structure):
     _fields_ = [("rule", ctypes.c_int), ("alpha", ctypes.c_void_p),
                 ("text_state", ctypes.c_void_p), ("window_chunk", ctypes.c_int),
                 ("window_radius", ctypes.c_int), ("window_offset", ctypes.c_int),
-                ("gate_tokens", ctypes.c_void_p)]
+                ("gate_tokens", ctypes.c_void_p), ("out_heads", ctypes.c_int)]
 
 
 RULES = {"joint": 0, "frozen": 1}
@@ -158,7 +158,7 @@ def _shape(q, k, v, beta, gate=None):
 
 
 def forward(q, k, v, beta, gate, out=None, stream=None, alpha=None, text_state=None,
-            window=None, rule="joint", gate_tokens=None):
+            window=None, rule="joint", gate_tokens=None, out_heads=None):
     """VDA forward (vda_forward for bf16 tensors, vda_forward_f32 for fp32).
 
     With any of the full-operator options it calls vda_forward_ex(_f32):
@@ -167,7 +167,9 @@ def forward(q, k, v, beta, gate, out=None, stream=None, alpha=None, text_state=N
     (Eq. 5) or 'frozen' (Eq. 3c with 1/sqrt(U) key scaling), and
     gate_tokens [..., F, N, d_v] (q's dtype), the output gate G^L of Eq. 1c
     per token and channel, which replaces the per-head gate (gate may then
-    be None)."""
+    be None).  out_heads (> 0) selects the token-major output
+    [H / out_heads, F, N, out_heads * d_v] of clips of out_heads heads, H the
+    number of head problems (the product of the leading dimensions)."""
     torch = _torch()
     dt = q.dtype
     if dt not in (torch.bfloat16, torch.float32):
@@ -181,14 +183,18 @@ def forward(q, k, v, beta, gate, out=None, stream=None, alpha=None, text_state=N
     if gate is not None or gate_tokens is None:
         _require(gate, "gate", torch.float32, dev)
     lead, F, N, H, d_k, d_v = _shape(q, k, v, beta, gate)
+    oh = int(out_heads or 0)
+    if oh < 0 or (oh and H % oh):
+        raise ValueError(f"out_heads {out_heads} must divide the {H} head problems")
+    oshape = (H // oh, F, N, oh * d_v) if oh else lead + (F, N, d_v)
     if out is None:
-        out = torch.empty(lead + (F, N, d_v), dtype=dt, device=dev)
+        out = torch.empty(oshape, dtype=dt, device=dev)
     else:
         _require(out, "out", dt, dev)
-        if tuple(out.shape) != lead + (F, N, d_v):
-            raise ValueError(f"out shape {tuple(out.shape)} must be {lead + (F, N, d_v)}")
+        if tuple(out.shape) != oshape:
+            raise ValueError(f"out shape {tuple(out.shape)} must be {oshape}")
     if alpha is None and text_state is None and window is None and rule == "joint" and \
-            gate_tokens is None:
+            gate_tokens is None and not oh:
         fn = lib.vda_forward if dt == torch.bfloat16 else lib.vda_forward_f32
         with torch.cuda.device(dev):
             st = fn(q.data_ptr(), k.data_ptr(), v.data_ptr(), beta.data_ptr(), gate.data_ptr(),
@@ -215,7 +221,7 @@ def forward(q, k, v, beta, gate, out=None, stream=None, alpha=None, text_state=N
     opts = VdaOptions(RULES[rule], alpha.data_ptr() if alpha is not None else None,
                       text_state.data_ptr() if text_state is not None else None,
                       chunk, radius, offset,
-                      gate_tokens.data_ptr() if gate_tokens is not None else None)
+                      gate_tokens.data_ptr() if gate_tokens is not None else None, oh)
     fn = lib.vda_forward_ex if dt == torch.bfloat16 else lib.vda_forward_ex_f32
     with torch.cuda.device(dev):
         st = fn(q.data_ptr(), k.data_ptr(), v.data_ptr(), beta.data_ptr(),

@@ -194,6 +194,13 @@ def test_forward_ex_validation():
                             ctypes.byref(opts()), 6 * big, None) == 1
     assert L.vda_forward_ex(big, 2 * big, 3 * big, 4 * big, None, 4, 64, 2, 64, 64, None,
                             6 * big, None) == 1
+    # token-major output: out_heads >= 0, dividing H, one frame's rows within
+    # 32-bit byte offsets
+    assert ex(vda.VdaOptions(0, None, None, 1, 0, 0, None, -1)) == 2
+    assert ex(vda.VdaOptions(0, None, None, 1, 0, 0, None, 3)) == 2
+    assert L.vda_forward_ex(big, 2 * big, 3 * big, 4 * big, 5 * big, 1, 1 << 21, 4, 128, 128,
+                            ctypes.byref(vda.VdaOptions(0, None, None, 1, 0, 0, None, 4)),
+                            8 * big, None) == 2
 
 
 def test_text_state_validation():

@@ -312,3 +312,51 @@ def test_full_operator_paper_shard_full_size(V, rule):
         worst = max(worst, err)
         assert err <= tol_for(w), (h, err)
     _log(f"  rel max-norm error over the sampled outputs {worst:.3e}")
+
+
+def _token_major(y, clips, heads):
+    """Frame-major per head [clips*heads, F, N, d_v] rearranged to the
+    token-major [clips, F, N, heads*d_v] (a layout change only)."""
+    _, F, N, dv = y.shape
+    return y.reshape(clips, heads, F, N, dv).permute(0, 2, 3, 1, 4).reshape(clips, F, N, heads * dv)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("dk,dv", [(64, 64), (128, 128), (32, 16), (16, 64)])
+def test_token_major_output(V, dtype, dk, dv):
+    """The epilogue's final layout conversion (vda_options.out_heads): for
+    every divisor of the six head problems, with and without the options,
+    the token-major output is the frame-major one rearranged, bit for bit
+    (the same kernels write it, only to other addresses); once also against
+    the oracle's output rearranged."""
+    import torch
+    _log(f"token-major output dtype={dtype} dk={dk} dv={dv}")
+    w = I.custom("ex_tm", 2, 3, 7, 150, dk, dv, dtype, seed=dk + 3 * dv)
+    x = I.make_inputs(w)
+    d = device_inputs(w, x)
+    alpha, S_T, G = I.make_decay(w), I.make_text_state(w), I.make_token_gates(w)
+    variants = [
+        dict(),
+        dict(alpha=to_device(alpha, "f32"), text_state=to_device(S_T, "f32"), window=PAPER_WINDOW),
+        dict(gate_tokens=to_device(G, w.dtype), window=(3, 1, 0)),
+    ]
+    bits = torch.int16 if dtype == "bf16" else torch.int32
+    H = w.heads
+    for opts in variants:
+        gate = None if "gate_tokens" in opts else d["gate"]
+        ref = V.forward(d["q"], d["k"], d["v"], d["beta"], gate, **opts)
+        for oh in (1, 2, 3, 6):
+            y = V.forward(d["q"], d["k"], d["v"], d["beta"], gate, out_heads=oh, **opts)
+            torch.cuda.synchronize()
+            assert tuple(y.shape) == (H // oh, w.F, w.N, oh * dv)
+            assert torch.equal(y.view(bits), _token_major(ref, H // oh, oh).contiguous().view(bits)), \
+                (sorted(opts), oh)
+    y = V.forward(d["q"], d["k"], d["v"], d["beta"], d["gate"], out_heads=3,
+                  alpha=to_device(alpha, "f32"), text_state=to_device(S_T, "f32"),
+                  window=PAPER_WINDOW)
+    torch.cuda.synchronize()
+    exp = _oracle(w, x, alpha, S_T, PAPER_WINDOW)
+    exp_tm = exp.reshape(2, 3, w.F, w.N, dv).transpose(0, 2, 3, 1, 4).reshape(2, w.F, w.N, 3 * dv)
+    err = rel_max_err(from_device(y), exp_tm)
+    _log(f"  against the oracle: rel err {err:.2e}")
+    assert err <= tol_for(w), err
