@@ -747,6 +747,26 @@ def main() -> int:
         full[name] = {"ms_per_step": ms_ex, "tokens_per_s": w.tokens / (ms_ex / 1e3)}
         print(f"[bench] vda_forward_ex ({name}): {ms_ex:.4f} ms/step", file=sys.stderr,
               flush=True)
+    # The core operator with the epilogue's token-major output
+    # ([clips][F][N][heads * d_v], vda_options.out_heads), the layout the
+    # model's output projection reads.
+    out_tm = torch.empty((w.B, F, N, w.H * dv), dtype=out.dtype, device=out.device)
+    def fwd_tm():
+        vda.forward(q, k, v, beta, gate, out=out_tm, out_heads=w.H)
+    for _ in range(max(2, args.warmup)):
+        fwd_tm()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(K):
+        fwd_tm()
+    e1.record()
+    torch.cuda.synchronize()
+    ms_tm = e0.elapsed_time(e1) / K
+    full["token_major_output"] = {"ms_per_step": ms_tm, "tokens_per_s": w.tokens / (ms_tm / 1e3)}
+    print(f"[bench] vda_forward_ex (token-major output): {ms_tm:.4f} ms/step", file=sys.stderr,
+          flush=True)
+    del out_tm
     # The prompt state itself (vda_text_state): a 512-token prompt per head of
     # the workload, one frame from zero, joint rule.
     pw = I.custom("prompt", 1, w.heads, 1, 512, w.d_k, w.d_v, w.dtype, seed=w.seed + 77)
