@@ -192,11 +192,29 @@ def pmc_summary(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, copy_gib, 
             "write_factor": f_write, "kernels": kernels}
 
 
+def _time_calls(torch, fn, K, warm=3):
+    """Average ms of K back-to-back calls of fn on the current stream."""
+    for _ in range(warm):
+        fn()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(K):
+        fn()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / K
+
+
 def prep_bench(vda, torch, w, K):
     """Time vda_prep on the workload's shape (B clips, F frames, H heads,
     latent grid, d_k / d_v channels) from seeded synthetic projections.  Its
     algorithmic bytes are the three bf16 inputs and outputs (filters are
-    negligible)."""
+    negligible).  Also timed: vda_prep of K and V only, and the two ways from
+    the projections to the token-major attention output -- vda_prep of all
+    three then vda_forward_ex (out_heads = H), and vda_prep of K and V then
+    vda_forward_ex on the raw query (q_heads = out_heads = H), whose readout
+    applies the query's L2 map."""
     import numpy as np
     from paper_2609_20744_amd import inputs as I
     if w.dtype != "bf16" or w.grid is None or w.d_k not in (64, 128) or w.d_v not in (64, 128):
@@ -204,24 +222,41 @@ def prep_bench(vda, torch, w, K):
     x = I.make_prep_inputs(w.B, w.F, w.grid, w.H, w.d_k, w.d_v, seed=w.seed)
     bf = lambda a: torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).cuda()
     f32 = lambda a: torch.from_numpy(a).cuda()
-    args = (bf(x["q"]), bf(x["k"]), bf(x["v"]), w.grid, f32(x["wk_spatial"]),
-            f32(x["wk_temporal"]), f32(x["wv_spatial"]), f32(x["wv_temporal"]), w.H)
-    outs = vda.prep(*args)
-    for _ in range(3):
-        vda.prep(*args, outs=outs)
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for _ in range(K):
-        vda.prep(*args, outs=outs)
-    e1.record()
-    torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1) / K
+    qp = bf(x["q"])
+    rest = (bf(x["k"]), bf(x["v"]), w.grid, f32(x["wk_spatial"]), f32(x["wk_temporal"]),
+            f32(x["wv_spatial"]), f32(x["wv_temporal"]), w.H)
+    outs = vda.prep(qp, *rest)
+    ms = _time_calls(torch, lambda: vda.prep(qp, *rest, outs=outs), K)
+    kv_outs = (None,) + tuple(outs[1:])
+    ms_kv = _time_calls(torch, lambda: vda.prep(None, *rest, outs=kv_outs), K)
     tok = w.B * w.F * w.N
     nbytes = 2 * tok * w.H * 2 * (2 * w.d_k + w.d_v)
-    print(f"[bench] vda_prep: {ms:.4f} ms", file=sys.stderr, flush=True)
+    print(f"[bench] vda_prep: {ms:.4f} ms; K and V only: {ms_kv:.4f} ms", file=sys.stderr,
+          flush=True)
+    # the pipelines, with the workload's beta and per-head gate shapes
+    g = torch.Generator(device="cuda").manual_seed(w.seed)
+    HB = w.B * w.H
+    beta = torch.sigmoid(torch.randn((HB, w.F, w.N), generator=g, device="cuda"))
+    gate = torch.sigmoid(torch.randn((HB,), generator=g, device="cuda"))
+    y = torch.empty((w.B, w.F, w.N, w.H * w.d_v), dtype=torch.bfloat16, device="cuda")
+
+    def two_step():
+        vda.prep(qp, *rest, outs=outs)
+        vda.forward(outs[0], outs[1], outs[2], beta, gate, out=y, out_heads=w.H)
+
+    def raw_query():
+        vda.prep(None, *rest, outs=kv_outs)
+        vda.forward(qp, outs[1], outs[2], beta, gate, out=y, out_heads=w.H, q_heads=w.H)
+
+    ms_two = _time_calls(torch, two_step, K)
+    ms_raw = _time_calls(torch, raw_query, K)
+    print(f"[bench] prep + forward: {ms_two:.4f} ms; K/V prep + raw-query forward: "
+          f"{ms_raw:.4f} ms", file=sys.stderr, flush=True)
     return {"ms": ms, "tokens_per_s": tok / (ms / 1e3), "hbm_gbs_alg": nbytes / (ms / 1e3) / 1e9,
-            "frac_hbm_peak": nbytes / (ms / 1e3) / 1e9 / PEAK_HBM_GBS, "bytes_alg": nbytes}
+            "frac_hbm_peak": nbytes / (ms / 1e3) / 1e9 / PEAK_HBM_GBS, "bytes_alg": nbytes,
+            "kv_only_ms": ms_kv,
+            "pipeline_token_major": {"prep_then_forward_ms": ms_two,
+                                     "kv_prep_then_raw_query_forward_ms": ms_raw}}
 
 
 def scan_paths(vda, torch, H, F, dk, dv, chunk, offset, K):

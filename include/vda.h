@@ -159,7 +159,7 @@ typedef enum {
 /*
  * Options of vda_forward_ex.  A NULL pointer to this struct, or all fields at
  * their defaults (rule 0, NULL pointers, chunk 1, radius 0, offset 0,
- * out_heads 0), give exactly vda_forward.
+ * out_heads 0, q_heads 0), give exactly vda_forward.
  *  - rule: a vda_rule.
  *  - alpha: NULL (alpha = 1) or a DEVICE pointer to [H][F][d_k] fp32 channel
  *    decays in [0, 1] (16-byte aligned), one per frame and key channel:
@@ -191,6 +191,24 @@ typedef enum {
  *    inputs and gate_tokens keep their per-head layouts.  VDA_ERR_SIZE if
  *    out_heads < 0, if it does not divide H, or if (N + 64) * out_heads * d_v
  *    elements of one frame exceed 2^31 bytes.
+ *  - q_heads: the form of q.  0: q is the feature-mapped query phi(q) in the
+ *    frame-major per-head layout [H][F][N][d_k] (as vda_forward).  q_heads
+ *    > 0: q is the raw query projection in its token-major layout
+ *    [H / q_heads][F][N][q_heads * d_k] (head problem b * q_heads + h reads
+ *    channels h * d_k .. h * d_k + d_k - 1 of its clip's rows), and the
+ *    readout applies the query's L2 feature map itself (Sec. 2.3: each token
+ *    of each head divided by sqrt(sum of its squared channels + 1e-6), the
+ *    map vda_prep applies).  RMSNorm is invariant to a positive per-token
+ *    scale up to its epsilon, so the readout folds the division into the
+ *    norm: with o = S~_t q the raw product and n = |q|^2 + 1e-6,
+ *    RMSNorm(o / sqrt(n)) = o / sqrt(mean(o^2) + eps * n) times the norm
+ *    weight, which is what is computed (no normalised copy of q is rounded
+ *    to the storage type).  k and v keep the per-head layout (vda_prep
+ *    writes it; its query output can then be skipped).  VDA_ERR_SIZE if
+ *    q_heads < 0, if it does not divide H, or if (N + 64) * q_heads * d_k
+ *    elements of one frame exceed 2^31 bytes; VDA_ERR_UNSUPPORTED if d_k is
+ *    not one of the kernels' key widths (32, 64, 128; a narrower key is
+ *    zero-padded, which needs the per-head query layout).
  */
 typedef struct vda_options {
   int rule;
@@ -201,6 +219,7 @@ typedef struct vda_options {
   int window_offset;
   const void* gate_tokens;
   int out_heads;
+  int q_heads;
 } vda_options;
 
 /*
@@ -259,6 +278,10 @@ int vda_forward_ex_f32(const float* q, const float* k, const float* v,
  *    wv_temporal [H*d_v][5]: fp32 DEVICE pointers, one filter per channel.
  *  - q_out, k_out [B*H][F][grid_h*grid_w][d_k], v_out [..][d_v]: bf16 DEVICE
  *    pointers, the frame-major per-head layout of vda_forward (index b*H+h).
+ *  - q and q_out may both be NULL: the query map is then not computed here
+ *    (vda_forward_ex with q_heads = H reads the raw token-major query and
+ *    applies the L2 map in its readout); one of the two NULL alone is
+ *    VDA_ERR_NULL.
  * The filters accumulate in fp32; results are rounded to bf16 once.
  * d_k, d_v in {64, 128}; B, F, grid_h, grid_w, H >= 1.  Tensors 16-byte
  * aligned, filters 4-byte aligned; no output may overlap an input or

@@ -285,10 +285,11 @@ int check_options(const vda_options* o, vda_options* out) {
   d.window_offset = 0;
   d.gate_tokens = nullptr;
   d.out_heads = 0;
+  d.q_heads = 0;
   if (o) d = *o;
   if (d.rule != VDA_RULE_JOINT && d.rule != VDA_RULE_FROZEN_SCALED) return VDA_ERR_UNSUPPORTED;
   if (d.window_chunk < 1 || d.window_radius < 0 || d.window_offset < 0 ||
-      d.window_offset >= d.window_chunk || d.out_heads < 0)
+      d.window_offset >= d.window_chunk || d.out_heads < 0 || d.q_heads < 0)
     return VDA_ERR_SIZE;
   if (!aligned(d.alpha, 16) || !aligned(d.text_state, 16) || !aligned(d.gate_tokens, 16))
     return VDA_ERR_ALIGN;
@@ -338,6 +339,14 @@ int check_forward(bool is_f32, const void* q, const void* k, const void* v, cons
       (H % o.out_heads != 0 ||
        (long long)(N + 64) * o.out_heads * d_v * (is_f32 ? 4 : 2) > 0x7fffffffLL))
     return VDA_ERR_SIZE;
+  // A raw token-major query: whole clips, 32-bit row offsets, and the
+  // kernels' own key widths (no padded copy of it is made).
+  if (o.q_heads > 0) {
+    if (H % o.q_heads != 0 ||
+        (long long)(N + 64) * o.q_heads * d_k * (is_f32 ? 4 : 2) > 0x7fffffffLL)
+      return VDA_ERR_SIZE;
+    if (padded_dim(d_k) != d_k) return VDA_ERR_UNSUPPORTED;
+  }
   const size_t es = is_f32 ? 4 : 2;
   const size_t tok = (size_t)H * F * N;
   const Range ro = range_of(out, tok * d_v * es);
@@ -383,7 +392,7 @@ void plan_forward(bool is_f32, const void* q, const void* k, const void* v, cons
                                                             o.window_offset),
                                 256)
                      : 0;
-  C.qk_pad = pk != d_k ? round_up(tok * pk * es, 256) : 0;
+  C.qk_pad = pk != d_k ? round_up(tok * pk * es, 256) : 0;  // (never with a raw query)
   C.v_pad = pv != d_v ? round_up(tok * pv * es, 256) : 0;
   const bool pad_any = pk != d_k || pv != d_v;
   C.a_pad = pk != d_k && o.alpha ? round_up((size_t)H * F * pk * 4, 256) : 0;
@@ -487,6 +496,8 @@ hipError_t launch_forward(const ForwardCall& C, char* base, hipStream_t stream) 
   go.offset = o.window_offset;
   go.gate_tokens = gt_x;
   go.out_heads = o.out_heads > 0 ? o.out_heads : 1;
+  go.q_heads = o.q_heads > 0 ? o.q_heads : 1;
+  go.q_l2 = o.q_heads > 0;
   // The readout writes the true d_v channels of each head straight into out
   // (a padded head's zero channels are not stored).
   if (e == hipSuccess)
@@ -890,8 +901,10 @@ int vda_prep(const void* q, const void* k, const void* v, const float* wk_spatia
              const float* wk_temporal, const float* wv_spatial, const float* wv_temporal, int B,
              int F, int grid_h, int grid_w, int H, int d_k, int d_v, void* q_out, void* k_out,
              void* v_out, hipStream_t stream) {
-  if (!q || !k || !v || !wk_spatial || !wk_temporal || !wv_spatial || !wv_temporal || !q_out ||
-      !k_out || !v_out)
+  // q and q_out may both be NULL: the queries are then left to a forward
+  // call that normalises raw queries itself (vda_options.q_heads).
+  if (!k || !v || !wk_spatial || !wk_temporal || !wv_spatial || !wv_temporal || !k_out ||
+      !v_out || !q != !q_out)
     return VDA_ERR_NULL;
   if (B < 1 || F < 1 || grid_h < 1 || grid_w < 1 || H < 1) return VDA_ERR_SIZE;
   if ((d_k != 64 && d_k != 128) || (d_v != 64 && d_v != 128)) return VDA_ERR_UNSUPPORTED;
@@ -908,12 +921,12 @@ int vda_prep(const void* q, const void* k, const void* v, const float* wk_spatia
       !aligned(wk_temporal, 4) || !aligned(wv_spatial, 4) || !aligned(wv_temporal, 4))
     return VDA_ERR_ALIGN;
   const size_t tk = (size_t)B * F * N * H * d_k * 2, tv = (size_t)B * F * N * H * d_v * 2;
-  const Range in[] = {range_of(q, tk), range_of(k, tk), range_of(v, tv),
+  const Range in[] = {range_of(q, q ? tk : 0), range_of(k, tk), range_of(v, tv),
                       range_of(wk_spatial, (size_t)H * d_k * 25 * 4),
                       range_of(wk_temporal, (size_t)H * d_k * 5 * 4),
                       range_of(wv_spatial, (size_t)H * d_v * 25 * 4),
                       range_of(wv_temporal, (size_t)H * d_v * 5 * 4)};
-  const Range outs[] = {range_of(q_out, tk), range_of(k_out, tk), range_of(v_out, tv)};
+  const Range outs[] = {range_of(q_out, q_out ? tk : 0), range_of(k_out, tk), range_of(v_out, tv)};
   for (const Range& o : outs)
     for (const Range& i : in)
       if (overlaps(o, i)) return VDA_ERR_OVERLAP;

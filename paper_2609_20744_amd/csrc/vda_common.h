@@ -10,6 +10,10 @@ namespace vda {
 // not state a value.
 constexpr float kRmsEps = 1e-6f;
 
+// L2-normalisation epsilon of the feature map (Sec. 2.3), x / sqrt(|x|^2 +
+// eps); the paper states none.
+constexpr float kL2Eps = 1e-6f;
+
 // Workgroup size of every kernel: four 64-wide wavefronts, one per SIMD.
 constexpr int kThreads = 256;
 

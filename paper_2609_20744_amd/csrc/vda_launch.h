@@ -112,6 +112,12 @@ struct GatherOptions {
   // + h writes channels h * d_v_norm ..); 1 is frame-major per head,
   // [H][F][N][d_v_norm].
   int out_heads = 1;
+  // Query layout, likewise: q_heads > 1 reads q token-major,
+  // [H / q_heads][F][N][q_heads * d_k]; 1 is frame-major per head.
+  int q_heads = 1;
+  // Whether q is the raw projection: the readout then applies the feature
+  // map's L2 normalisation to each token's query (Sec. 2.3) itself.
+  bool q_l2 = false;
 };
 
 // Steps a5-a7, Eq. A.4 / 1a / 1c: gather, readout, RMSNorm and gate.

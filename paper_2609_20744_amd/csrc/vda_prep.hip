@@ -37,7 +37,6 @@
 namespace vda {
 namespace {
 
-constexpr float kL2Eps = 1e-6f;  // the paper states none
 constexpr int kConvThreads = 512;                    // eight waves, one output row each
 constexpr int kPTY = 8, kPTX = 8;                    // output tile (rows = waves)
 constexpr int kPHY = kPTY + 4, kPHX = kPTX + 4;      // with the 2-token halo
@@ -381,13 +380,12 @@ hipError_t launch_prep(const void* q, const void* k, const void* v, const float*
                        int gw, int H, int d_k, int d_v, void* q_out, void* k_out, void* v_out,
                        hipStream_t stream) {
   const int N = gh * gw;
-  hipError_t e;
-  if (d_k == 128)
+  hipError_t e = hipSuccess;
+  if (d_k != 128 && d_k != 64) return hipErrorInvalidValue;
+  if (q && d_k == 128)
     e = launch_qnorm_t<128>(q, q_out, B, F, N, H, stream);
-  else if (d_k == 64)
+  else if (q)
     e = launch_qnorm_t<64>(q, q_out, B, F, N, H, stream);
-  else
-    return hipErrorInvalidValue;
   if (e != hipSuccess) return e;
   PrepConvArgs a{};
   a.F = F;

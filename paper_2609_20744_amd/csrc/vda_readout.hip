@@ -58,15 +58,17 @@ __device__ __forceinline__ void bridge_decay(const float* alpha, int h, int F, i
   }
 }
 
-// GENOUT: the token-major output or a padded narrow head (row stride and
-// stored channels at run time); otherwise frame-major rows of DV channels.
+// GENOUT: the general layouts (the token-major output, a padded narrow
+// head: row stride and stored channels at run time; a token-major raw query,
+// qh heads per clip, L2-normalised here when ql2); otherwise frame-major rows
+// of DK and DV channels.
 template <int DK, int DV, bool TOKGATE, bool GENOUT>
 __global__ __launch_bounds__(kThreads, 2)
 void readout_bf16_kernel(const uint16_t* __restrict__ Q, const float* __restrict__ S_fwd,
                          const float* __restrict__ S_rev, const float* __restrict__ gate,
                          int F, int N, int chunks, int tokens_per_chunk, unsigned nwg,
-                         int dvo, int oh, const float* __restrict__ alpha, int wchunk,
-                         int wradius, int woffset, const uint16_t* __restrict__ gtok,
+                         int dvo, int oh, int qh, int ql2, const float* __restrict__ alpha,
+                         int wchunk, int wradius, int woffset, const uint16_t* __restrict__ gtok,
                          uint16_t* __restrict__ out) {
   constexpr int SLD = DK + 8;  // bf16 row stride of S~ in LDS
   constexpr int MB = DV / 16;  // 16-row blocks of S~ (output channels)
@@ -122,10 +124,13 @@ void readout_bf16_kernel(const uint16_t* __restrict__ Q, const float* __restrict
     for (int kb = 0; kb < KB; ++kb)
       sop[mb][kb] = *reinterpret_cast<const bf16x8*>(&st[(mb * 16 + li) * SLD + kb * 32 + lg * 8]);
 
-  const uint16_t* qbase = Q + (size_t)fh * N * DK;
-  // This frame's output rows: dvo channels at row stride oh * dvo, from
-  // head h % oh of clip h / oh (frame-major per head when oh = 1).
-  const unsigned ohu = GENOUT ? (unsigned)oh : 1u, hp = fh / F, fr = fh % F;
+  // This frame's query rows: DK channels at row stride qh * DK, from head
+  // h % qh of clip h / qh (frame-major per head when qh = 1).
+  const unsigned qhu = GENOUT ? (unsigned)qh : 1u, hp = fh / F, fr = fh % F;
+  const uint32_t qrs = qhu * (uint32_t)DK;
+  const uint16_t* qbase = Q + (((size_t)(hp / qhu) * F + fr) * N * qhu + hp % qhu) * DK;
+  // This frame's output rows: dvo channels at row stride oh * dvo, likewise.
+  const unsigned ohu = GENOUT ? (unsigned)oh : 1u;
   const int dvw = GENOUT ? dvo : DV;
   const uint32_t ors = ohu * (uint32_t)dvw;
   uint16_t* obase = out + (((size_t)(hp / ohu) * F + fr) * N * ohu + hp % ohu) * dvw;
@@ -149,7 +154,7 @@ void readout_bf16_kernel(const uint16_t* __restrict__ Q, const float* __restrict
     const int row = min(nq + li, N - 1);
 #pragma unroll
     for (int kb = 0; kb < KB; ++kb)
-      qv[kb] = *reinterpret_cast<const uint4*>(qbase + (size_t)row * DK + kb * 32 + lg * 8);
+      qv[kb] = *reinterpret_cast<const uint4*>(qbase + (size_t)row * qrs + kb * 32 + lg * 8);
   };
   // TOKGATE: a group's output gate, four channels per lane and row block in
   // the accumulators' layout, loaded after the group's products (rows past
@@ -184,6 +189,28 @@ void readout_bf16_kernel(const uint16_t* __restrict__ Q, const float* __restrict
         for (int mb = 0; mb < MB; ++mb)
           acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sop[mb][kb], qop, acc[mb], 0, 0, 0);
       }
+      // A raw query: |q|^2 of the lane's token from the operand registers
+      // (the token's DK channels are spread over lanes li + 16 lg), so that
+      // the L2-normalised query's output is this one divided by
+      // sqrt(|q|^2 + eps), which the RMSNorm below takes in.
+      float qn2 = 1.0f;
+      if constexpr (GENOUT) {
+        if (ql2) {
+          float s = 0.f;
+#pragma unroll
+          for (int kb = 0; kb < KB; ++kb) {
+            const uint32_t w4[4] = {qr[d][kb].x, qr[d][kb].y, qr[d][kb].z, qr[d][kb].w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              s = fmaf(bf16_lo(w4[e]), bf16_lo(w4[e]), s);
+              s = fmaf(bf16_hi(w4[e]), bf16_hi(w4[e]), s);
+            }
+          }
+          s += __shfl_xor(s, 16);
+          s += __shfl_xor(s, 32);
+          qn2 = s + kL2Eps;
+        }
+      }
       load_q(ng + S * kQ, qr[d]);
       u32x2 gnow[MB];  // this group's gate, in flight during the norm's reduction
       if constexpr (TOKGATE) {
@@ -201,7 +228,9 @@ void readout_bf16_kernel(const uint16_t* __restrict__ Q, const float* __restrict
         for (int i = 0; i < 4; ++i) ss = fmaf(acc[mb][i], acc[mb][i], ss);
       ss += __shfl_xor(ss, 16);
       ss += __shfl_xor(ss, 32);
-      const float scale = g / sqrtf(ss * inv_norm + kRmsEps);
+      // With q / n (n^2 = qn2) in place of q: g (o / n) / sqrt(mean((o / n)^2)
+      // + eps) = g o / sqrt(mean(o^2) + eps n^2).
+      const float scale = g / sqrtf(ss * inv_norm + kRmsEps * qn2);
       // Stores of whole token rows: the group's outputs (16 tokens x DV,
       // bf16) go through this wave's LDS tile, then each store instruction
       // writes 64 / (DV / 8) consecutive token rows, one contiguous run of
@@ -240,9 +269,9 @@ template <int DK, int DV, bool TOKGATE>
 __global__ __launch_bounds__(kThreads)
 void readout_f32_kernel(const float* __restrict__ Q, const float* __restrict__ S_fwd,
                         const float* __restrict__ S_rev, const float* __restrict__ gate,
-                        int F, int N, int chunks, int tokens_per_chunk, int dvo, int oh,
-                        const float* __restrict__ alpha, int wchunk, int wradius, int woffset,
-                        const float* __restrict__ gtok, float* __restrict__ out) {
+                        int F, int N, int chunks, int tokens_per_chunk, int dvo, int oh, int qh,
+                        int ql2, const float* __restrict__ alpha, int wchunk, int wradius,
+                        int woffset, const float* __restrict__ gtok, float* __restrict__ out) {
   constexpr int SLD = DK + 1;
   constexpr int VPT = DV / 16;  // output channels per thread
   __shared__ float st[DV * SLD];
@@ -255,7 +284,9 @@ void readout_f32_kernel(const float* __restrict__ Q, const float* __restrict__ S
   const float g = TOKGATE ? 1.0f : gate[fh / F];
   const int tid = threadIdx.x;
   const float inv_norm = 1.0f / (float)dvo;
-  // Output rows as in readout_bf16_kernel.
+  // Query and output rows as in readout_bf16_kernel.
+  const size_t qrs = (size_t)qh * DK;
+  const float* qbase = Q + (((size_t)(fh / F / qh) * F + fh % F) * N * qh + (fh / F) % qh) * DK;
   const size_t ors = (size_t)oh * dvo;
   float* obase = out + (((size_t)(fh / F / oh) * F + fh % F) * N * oh + (fh / F) % oh) * dvo;
 
@@ -277,7 +308,7 @@ void readout_f32_kernel(const float* __restrict__ Q, const float* __restrict__ S
     for (int idx = tid; idx < 16 * DK; idx += kThreads) {
       const int e = idx / DK, c = idx % DK;
       const int n = n0 + e;
-      qs[e][c] = n < n_end ? Q[((size_t)fh * N + n) * DK + c] : 0.f;
+      qs[e][c] = n < n_end ? qbase[(size_t)n * qrs + c] : 0.f;
     }
     lds_barrier();
     float o[VPT];
@@ -293,7 +324,16 @@ void readout_f32_kernel(const float* __restrict__ Q, const float* __restrict__ S
     for (int m = 0; m < VPT; ++m) ss = fmaf(o[m], o[m], ss);
 #pragma unroll
     for (int off = 1; off < 16; off <<= 1) ss += __shfl_xor(ss, off);
-    const float scale = g / sqrtf(ss * inv_norm + kRmsEps);
+    // A raw query, as in readout_bf16_kernel: |q|^2 over the token's row.
+    float qn2 = 1.0f;
+    if (ql2) {
+      float s = 0.f;
+      for (int c = part; c < DK; c += 16) s = fmaf(qs[tok][c], qs[tok][c], s);
+#pragma unroll
+      for (int off = 1; off < 16; off <<= 1) s += __shfl_xor(s, off);
+      qn2 = s + kL2Eps;
+    }
+    const float scale = g / sqrtf(ss * inv_norm + kRmsEps * qn2);
     const int n = n0 + tok;
     if (n < n_end) {
 #pragma unroll
@@ -324,17 +364,20 @@ hipError_t launch_readout_t(bool is_f32, const void* q, const float* S_fwd, cons
   int tpc = (N + chunks - 1) / chunks;
   tpc = ((tpc + 63) / 64) * 64;
   const dim3 grid((unsigned)(fh_count * chunks));
-  const bool genout = go.out_heads > 1 || d_v_norm != DV;
+  const bool genout = go.out_heads > 1 || d_v_norm != DV || go.q_heads > 1 || go.q_l2;
+  const int ql2 = go.q_l2 ? 1 : 0;
 #define VDA_READOUT_LAUNCH(TG, GO)                                                                 \
   if (is_f32)                                                                                      \
     hipLaunchKernelGGL((readout_f32_kernel<DK, DV, TG>), grid, dim3(kThreads), 0, stream,          \
                        static_cast<const float*>(q), S_fwd, S_rev, gate, F, N, chunks, tpc,       \
-                       d_v_norm, go.out_heads, go.alpha, go.chunk, go.radius, go.offset,           \
+                       d_v_norm, go.out_heads, go.q_heads, ql2, go.alpha, go.chunk, go.radius,     \
+                       go.offset,                                                                  \
                        static_cast<const float*>(go.gate_tokens), static_cast<float*>(out));      \
   else                                                                                             \
     hipLaunchKernelGGL((readout_bf16_kernel<DK, DV, TG, GO>), grid, dim3(kThreads), 0, stream,     \
                        static_cast<const uint16_t*>(q), S_fwd, S_rev, gate, F, N, chunks, tpc,    \
-                       (unsigned)(fh_count * chunks), d_v_norm, go.out_heads, go.alpha, go.chunk,  \
+                       (unsigned)(fh_count * chunks), d_v_norm, go.out_heads, go.q_heads, ql2,     \
+                       go.alpha, go.chunk,                                                         \
                        go.radius,                                                                  \
                        go.offset, static_cast<const uint16_t*>(go.gate_tokens),                    \
                        static_cast<uint16_t*>(out));

@@ -41,7 +41,8 @@ class VdaOptions(ctypes.Structure):
     _fields_ = [("rule", ctypes.c_int), ("alpha", ctypes.c_void_p),
                 ("text_state", ctypes.c_void_p), ("window_chunk", ctypes.c_int),
                 ("window_radius", ctypes.c_int), ("window_offset", ctypes.c_int),
-                ("gate_tokens", ctypes.c_void_p), ("out_heads", ctypes.c_int)]
+                ("gate_tokens", ctypes.c_void_p), ("out_heads", ctypes.c_int),
+                ("q_heads", ctypes.c_int)]
 
 
 RULES = {"joint": 0, "frozen": 1}
@@ -139,17 +140,23 @@ def _require(t, name, dtype, device):
         raise ValueError(f"{name} must be contiguous")
 
 
-def _shape(q, k, v, beta, gate=None):
-    if q.dim() < 3:
-        raise ValueError("q must be [..., F, N, d_k]")
-    lead = tuple(q.shape[:-3])
-    F, N, d_k = q.shape[-3:]
+def _shape(q, k, v, beta, gate=None, q_heads=0):
+    if k.dim() < 3:
+        raise ValueError("k must be [..., F, N, d_k]")
+    lead = tuple(k.shape[:-3])
+    F, N, d_k = k.shape[-3:]
     d_v = v.shape[-1]
     H = math.prod(lead) if lead else 1
-    if tuple(k.shape) != tuple(q.shape):
+    if q_heads:
+        if H % q_heads:
+            raise ValueError(f"q_heads {q_heads} must divide the {H} head problems")
+        qshape = (H // q_heads, F, N, q_heads * d_k)
+        if tuple(q.shape) != qshape:
+            raise ValueError(f"raw q shape {tuple(q.shape)} must be {qshape}")
+    elif tuple(k.shape) != tuple(q.shape):
         raise ValueError(f"k shape {tuple(k.shape)} != q shape {tuple(q.shape)}")
     if tuple(v.shape) != lead + (F, N, d_v):
-        raise ValueError(f"v shape {tuple(v.shape)} does not match q")
+        raise ValueError(f"v shape {tuple(v.shape)} does not match k")
     if tuple(beta.shape) != lead + (F, N):
         raise ValueError(f"beta shape {tuple(beta.shape)} must be {lead + (F, N)}")
     if gate is not None and gate.numel() != H:
@@ -158,7 +165,7 @@ def _shape(q, k, v, beta, gate=None):
 
 
 def forward(q, k, v, beta, gate, out=None, stream=None, alpha=None, text_state=None,
-            window=None, rule="joint", gate_tokens=None, out_heads=None):
+            window=None, rule="joint", gate_tokens=None, out_heads=None, q_heads=None):
     """VDA forward (vda_forward for bf16 tensors, vda_forward_f32 for fp32).
 
     With any of the full-operator options it calls vda_forward_ex(_f32):
@@ -169,7 +176,10 @@ def forward(q, k, v, beta, gate, out=None, stream=None, alpha=None, text_state=N
     per token and channel, which replaces the per-head gate (gate may then
     be None).  out_heads (> 0) selects the token-major output
     [H / out_heads, F, N, out_heads * d_v] of clips of out_heads heads, H the
-    number of head problems (the product of the leading dimensions)."""
+    number of head problems (the product of the leading dimensions).
+    q_heads (> 0) passes the raw token-major query [H / q_heads, F, N,
+    q_heads * d_k] (as vda_prep's input) and leaves its L2 map to the
+    readout; k, v and the other arguments keep their per-head layouts."""
     torch = _torch()
     dt = q.dtype
     if dt not in (torch.bfloat16, torch.float32):
@@ -182,7 +192,10 @@ def forward(q, k, v, beta, gate, out=None, stream=None, alpha=None, text_state=N
     _require(beta, "beta", torch.float32, dev)
     if gate is not None or gate_tokens is None:
         _require(gate, "gate", torch.float32, dev)
-    lead, F, N, H, d_k, d_v = _shape(q, k, v, beta, gate)
+    qh = int(q_heads or 0)
+    if qh < 0:
+        raise ValueError(f"q_heads {q_heads} must be positive")
+    lead, F, N, H, d_k, d_v = _shape(q, k, v, beta, gate, qh)
     oh = int(out_heads or 0)
     if oh < 0 or (oh and H % oh):
         raise ValueError(f"out_heads {out_heads} must divide the {H} head problems")
@@ -194,7 +207,7 @@ def forward(q, k, v, beta, gate, out=None, stream=None, alpha=None, text_state=N
         if tuple(out.shape) != oshape:
             raise ValueError(f"out shape {tuple(out.shape)} must be {oshape}")
     if alpha is None and text_state is None and window is None and rule == "joint" and \
-            gate_tokens is None and not oh:
+            gate_tokens is None and not oh and not qh:
         fn = lib.vda_forward if dt == torch.bfloat16 else lib.vda_forward_f32
         with torch.cuda.device(dev):
             st = fn(q.data_ptr(), k.data_ptr(), v.data_ptr(), beta.data_ptr(), gate.data_ptr(),
@@ -221,7 +234,7 @@ def forward(q, k, v, beta, gate, out=None, stream=None, alpha=None, text_state=N
     opts = VdaOptions(RULES[rule], alpha.data_ptr() if alpha is not None else None,
                       text_state.data_ptr() if text_state is not None else None,
                       chunk, radius, offset,
-                      gate_tokens.data_ptr() if gate_tokens is not None else None, oh)
+                      gate_tokens.data_ptr() if gate_tokens is not None else None, oh, qh)
     fn = lib.vda_forward_ex if dt == torch.bfloat16 else lib.vda_forward_ex_f32
     with torch.cuda.device(dev):
         st = fn(q.data_ptr(), k.data_ptr(), v.data_ptr(), beta.data_ptr(),
@@ -481,31 +494,38 @@ def prep(q, k, v, grid, wk_spatial, wk_temporal, wv_spatial, wv_temporal, H, out
     """VDA-Prep (vda_prep): q, k [B, F, N, H*d_k], v [B, F, N, H*d_v] bf16
     projections with N = grid[0] * grid[1]; filters fp32 wk_spatial
     [H*d_k, 25] (or [H*d_k, 5, 5]), wk_temporal [H*d_k, 5], likewise for v.
-    Returns (q', k', v') [B*H, F, N, d] bf16 (or fills `outs`)."""
+    Returns (q', k', v') [B*H, F, N, d] bf16 (or fills `outs`).  With q None
+    the query map is skipped (forward with q_heads = H applies it to the raw
+    query) and q' is None."""
     torch = _torch()
-    dev = q.device
+    dev = k.device
     for t, n in ((q, "q"), (k, "k"), (v, "v")):
-        _require(t, n, torch.bfloat16, dev)
+        if t is not None or n != "q":
+            _require(t, n, torch.bfloat16, dev)
     for t, n in ((wk_spatial, "wk_spatial"), (wk_temporal, "wk_temporal"),
                  (wv_spatial, "wv_spatial"), (wv_temporal, "wv_temporal")):
         _require(t, n, torch.float32, dev)
-    B, F, N, Ck = q.shape
+    B, F, N, Ck = k.shape
     Cv = v.shape[-1]
     gh, gw = grid
-    if gh * gw != N or k.shape != q.shape or v.shape[:3] != q.shape[:3]:
+    if gh * gw != N or (q is not None and q.shape != k.shape) or v.shape[:3] != k.shape[:3]:
         raise ValueError("q, k, v must be [B, F, grid_h*grid_w, H*d]")
     if Ck % H or Cv % H:
         raise ValueError("channels must split into H heads")
     d_k, d_v = Ck // H, Cv // H
     if outs is None:
-        outs = (torch.empty((B * H, F, N, d_k), dtype=torch.bfloat16, device=dev),
+        outs = (torch.empty((B * H, F, N, d_k), dtype=torch.bfloat16, device=dev)
+                if q is not None else None,
                 torch.empty((B * H, F, N, d_k), dtype=torch.bfloat16, device=dev),
                 torch.empty((B * H, F, N, d_v), dtype=torch.bfloat16, device=dev))
+    elif (outs[0] is None) != (q is None):
+        raise ValueError("q and its output must both be given or both be None")
     with torch.cuda.device(dev):
-        st = lib.vda_prep(q.data_ptr(), k.data_ptr(), v.data_ptr(), wk_spatial.data_ptr(),
-                          wk_temporal.data_ptr(), wv_spatial.data_ptr(), wv_temporal.data_ptr(),
-                          B, F, gh, gw, H, d_k, d_v, outs[0].data_ptr(), outs[1].data_ptr(),
-                          outs[2].data_ptr(), _stream_ptr(dev, stream))
+        st = lib.vda_prep(q.data_ptr() if q is not None else None, k.data_ptr(), v.data_ptr(),
+                          wk_spatial.data_ptr(), wk_temporal.data_ptr(), wv_spatial.data_ptr(),
+                          wv_temporal.data_ptr(), B, F, gh, gw, H, d_k, d_v,
+                          outs[0].data_ptr() if outs[0] is not None else None,
+                          outs[1].data_ptr(), outs[2].data_ptr(), _stream_ptr(dev, stream))
     _check(st, "vda_prep")
     return outs
 

@@ -132,6 +132,14 @@ def test_stage_validation():
     w = [9 * big, 9 * big + 4096, 9 * big + 8192, 9 * big + 12288]
     outs = [4 * big, 5 * big, 6 * big]
     assert pr(None, 2 * big, 3 * big, *w, 1, 4, 6, 8, 2, 128, 128, *outs, None) == 1
+    # q and q_out NULL together skip the query map (the size check is then
+    # the first to fail); either alone is a NULL error
+    assert pr(big, 2 * big, 3 * big, *w, 1, 4, 6, 8, 2, 128, 128, None, 5 * big, 6 * big,
+              None) == 1
+    assert pr(None, 2 * big, 3 * big, *w, 1, 0, 6, 8, 2, 128, 128, None, 5 * big, 6 * big,
+              None) == 2
+    assert pr(None, 2 * big, 3 * big, *w, 1, 4, 6, 8, 2, 128, 128, None, 5 * big + 8, 6 * big,
+              None) == 4
     assert pr(big, 2 * big, 3 * big, *w, 1, 0, 6, 8, 2, 128, 128, *outs, None) == 2
     assert pr(big, 2 * big, 3 * big, *w, 1, 4, 6, 8, 2, 96, 128, *outs, None) == 3
     assert pr(big, 2 * big, 3 * big, *w, 1, 4, 6, 8, 2, 128, 32, *outs, None) == 3
@@ -201,6 +209,17 @@ def test_forward_ex_validation():
     assert L.vda_forward_ex(big, 2 * big, 3 * big, 4 * big, 5 * big, 1, 1 << 21, 4, 128, 128,
                             ctypes.byref(vda.VdaOptions(0, None, None, 1, 0, 0, None, 4)),
                             8 * big, None) == 2
+    # raw token-major query: q_heads >= 0, dividing H, a kernel key width
+    # (no padded 16-channel key), one frame's rows within 32-bit offsets
+    assert ex(vda.VdaOptions(0, None, None, 1, 0, 0, None, 0, -1)) == 2
+    assert ex(vda.VdaOptions(0, None, None, 1, 0, 0, None, 0, 3)) == 2
+    assert ex(vda.VdaOptions(0, None, None, 1, 0, 0, None, 0, 2), d_k=16) == 3
+    assert L.vda_forward_ex(big, 2 * big, 3 * big, 4 * big, 5 * big, 1, 1 << 21, 4, 128, 128,
+                            ctypes.byref(vda.VdaOptions(0, None, None, 1, 0, 0, None, 0, 4)),
+                            8 * big, None) == 2
+    assert L.vda_forward_ex_f32(big, 2 * big, 3 * big, 4 * big, 5 * big, 1, 1 << 20, 4, 128, 128,
+                                ctypes.byref(vda.VdaOptions(0, None, None, 1, 0, 0, None, 0, 4)),
+                                8 * big, None) == 2
 
 
 def test_text_state_validation():

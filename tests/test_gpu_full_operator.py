@@ -360,3 +360,70 @@ def test_token_major_output(V, dtype, dk, dv):
     err = rel_max_err(from_device(y), exp_tm)
     _log(f"  against the oracle: rel err {err:.2e}")
     assert err <= tol_for(w), err
+
+
+def _raw_queries(w, seed):
+    """Raw query projections per head [H, F, N, d_k] in storage form: normal
+    directions with per-token scales spread over e^-3 .. e^3, and a few
+    all-zero tokens (whose L2 map is zero, and so is their output)."""
+    rng = np.random.default_rng([seed, 77])
+    q = rng.standard_normal((w.heads, w.F, w.N, w.d_k))
+    q *= np.exp(rng.uniform(-3.0, 3.0, (w.heads, w.F, w.N, 1)))
+    q[:, 0, :3] = 0.0
+    q[:, -1, -2:] = 0.0
+    q32 = q.astype(np.float32)
+    return I.f32_to_bf16_bits(q32) if w.dtype == "bf16" else q32
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("dk,dv", [(64, 64), (128, 128), (32, 16), (128, 64)])
+def test_raw_query(V, dtype, dk, dv):
+    """vda_options.q_heads: the raw token-major query with the L2 map folded
+    into the readout's RMSNorm, against the oracle's forward on the
+    L2-normalised query (Sec. 2.3), with and without the options, for
+    several query and output clip sizes."""
+    import torch
+    _log(f"raw query dtype={dtype} dk={dk} dv={dv}")
+    w = I.custom("ex_rq", 2, 3, 7, 150, dk, dv, dtype, seed=5 * dk + dv)
+    x = I.make_inputs(w)
+    d = device_inputs(w, x)
+    qraw = _raw_queries(w, w.seed)
+    alpha, S_T, G = I.make_decay(w), I.make_text_state(w), I.make_token_gates(w)
+    H = w.heads
+    variants = [
+        ("core", {}, {}),
+        ("all", dict(alpha=to_device(alpha, "f32"), text_state=to_device(S_T, "f32"),
+                     window=PAPER_WINDOW), dict(alpha=alpha, S_T=S_T, window=PAPER_WINDOW)),
+        ("token_gate", dict(gate_tokens=to_device(G, w.dtype), window=(3, 1, 0)),
+         dict(G=G, window=(3, 1, 0))),
+    ]
+    xo = oracle_inputs(w, x)
+    q_l2 = O.l2_normalise(I.as_float64(qraw, w.dtype))
+    for name, opts, oopts in variants:
+        exp = O.vda_forward_ex(q_l2, xo["k"], xo["v"], xo["beta"], xo["gate"],
+                               None if "alpha" not in oopts else alpha.astype(np.float64),
+                               None if "S_T" not in oopts else S_T.astype(np.float64),
+                               *(oopts.get("window") or (1, 0, 0)), "joint",
+                               gate_tokens=None if "G" not in oopts else
+                               I.as_float64(G, w.dtype))
+        # zero queries read out zero
+        assert np.all(exp[:, 0, :3] == 0.0)
+        gate = None if "gate_tokens" in opts else d["gate"]
+        for qh, oh in ((1, None), (3, None), (3, 3), (6, 2)):
+            qdev = to_device(_token_major_np(qraw, H // qh, qh), w.dtype)
+            y = V.forward(qdev, d["k"], d["v"], d["beta"], gate, q_heads=qh, out_heads=oh, **opts)
+            torch.cuda.synchronize()
+            got = from_device(y)
+            ref = exp if oh is None else _token_major_np(exp, H // oh, oh)
+            err = rel_max_err(got, ref)
+            _log(f"  {name} q_heads={qh} out_heads={oh}: rel err {err:.2e}")
+            assert err <= tol_for(w), (name, qh, oh, err)
+            if oh is None:
+                assert np.all(got[:, 0, :3] == 0.0) and np.all(got[:, -1, -2:] == 0.0)
+
+
+def _token_major_np(y, clips, heads):
+    """numpy version of _token_major."""
+    _, F, N, d = y.shape
+    return np.ascontiguousarray(
+        y.reshape(clips, heads, F, N, d).transpose(0, 2, 3, 1, 4).reshape(clips, F, N, heads * d))

@@ -123,3 +123,56 @@ def test_prep_feeds_forward(V):
     err = rel_max_err(from_device(y), ref)
     _log(f"  rel err {err:.2e}")
     assert err <= 2e-2, err
+
+
+def test_prep_without_query(V):
+    """With q and q_out NULL the query map is skipped and the key and value
+    outputs are those of the full call, bit for bit."""
+    import torch
+    B, F, grid, H = 2, 5, (7, 9), 3
+    _log("prep without the query")
+    x = I.make_prep_inputs(B, F, grid, H, 128, 64, seed=21)
+    args = (_dev_bf16(x["k"]), _dev_bf16(x["v"]), grid, _dev_f32(x["wk_spatial"]),
+            _dev_f32(x["wk_temporal"]), _dev_f32(x["wv_spatial"]), _dev_f32(x["wv_temporal"]), H)
+    full = V.prep(_dev_bf16(x["q"]), *args)
+    q0, k0, v0 = V.prep(None, *args)
+    torch.cuda.synchronize()
+    assert q0 is None
+    assert torch.equal(k0.view(torch.int16), full[1].view(torch.int16))
+    assert torch.equal(v0.view(torch.int16), full[2].view(torch.int16))
+
+
+@pytest.mark.parametrize("d", [64, 128])
+def test_raw_query_pipeline(V, d):
+    """The fused pipeline: vda_prep maps only K and V, and vda_forward_ex
+    reads the raw token-major query (q_heads = H) and writes the token-major
+    output (out_heads = H), the layouts of the projections on both sides;
+    against the oracle's feature map and forward (the forward's bf16 bar),
+    with and without the full-operator options."""
+    import torch
+    B, F, grid, H = 2, 6, (6, 8), 2
+    _log(f"raw-query pipeline d={d}")
+    x = I.make_prep_inputs(B, F, grid, H, d, d, seed=13 + d)
+    N = grid[0] * grid[1]
+    _, k, v = V.prep(None, _dev_bf16(x["k"]), _dev_bf16(x["v"]), grid, _dev_f32(x["wk_spatial"]),
+                     _dev_f32(x["wk_temporal"]), _dev_f32(x["wv_spatial"]),
+                     _dev_f32(x["wv_temporal"]), H)
+    rng = np.random.default_rng(7)
+    beta = (1.0 / (1.0 + np.exp(-rng.standard_normal((B * H, F, N))))).astype(np.float32)
+    gate = (1.0 / (1.0 + np.exp(-rng.standard_normal(B * H)))).astype(np.float32)
+    alpha = (0.6 + 0.4 * rng.random((B * H, F, d))).astype(np.float32)
+    qo, ko, vo = _oracle(x, grid, H)
+    for name, opts, window in (("core", {}, (1, 0, 0)),
+                               ("decay+window", dict(alpha=_dev_f32(alpha), window=(5, 1, 1)),
+                                (5, 1, 1))):
+        y = V.forward(_dev_bf16(x["q"]), k, v, _dev_f32(beta), _dev_f32(gate), q_heads=H,
+                      out_heads=H, **opts)
+        torch.cuda.synchronize()
+        assert tuple(y.shape) == (B, F, N, H * d)
+        ref = O.vda_forward_ex(qo, ko, vo, beta.astype(np.float64), gate.astype(np.float64),
+                               alpha.astype(np.float64) if opts else None, None, *window,
+                               "joint")
+        ref = ref.reshape(B, H, F, N, d).transpose(0, 2, 3, 1, 4).reshape(B, F, N, H * d)
+        err = rel_max_err(from_device(y), ref)
+        _log(f"  {name}: rel err {err:.2e}")
+        assert err <= 2e-2, (name, err)
