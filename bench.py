@@ -801,6 +801,15 @@ def main() -> int:
     full["token_major_output"] = {"ms_per_step": ms_tm, "tokens_per_s": w.tokens / (ms_tm / 1e3)}
     print(f"[bench] vda_forward_ex (token-major output): {ms_tm:.4f} ms/step", file=sys.stderr,
           flush=True)
+    # ... and reading the raw token-major query (vda_options.q_heads), whose
+    # L2 map the readout applies; the timing reads q's buffer in that layout.
+    q_tm = q.view(w.B, F, N, w.H * dk)
+    ms_rq = _time_calls(torch, lambda: vda.forward(q_tm, k, v, beta, gate, out=out_tm,
+                                                   out_heads=w.H, q_heads=w.H),
+                        K, max(2, args.warmup))
+    full["raw_query_token_major"] = {"ms_per_step": ms_rq, "tokens_per_s": w.tokens / (ms_rq / 1e3)}
+    print(f"[bench] vda_forward_ex (raw token-major query and output): {ms_rq:.4f} ms/step",
+          file=sys.stderr, flush=True)
     del out_tm
     # The prompt state itself (vda_text_state): a 512-token prompt per head of
     # the workload, one frame from zero, joint rule.

@@ -393,7 +393,7 @@ def test_raw_query(V, dtype, dk, dv):
     variants = [
         ("core", {}, {}),
         ("all", dict(alpha=to_device(alpha, "f32"), text_state=to_device(S_T, "f32"),
-                     window=PAPER_WINDOW), dict(alpha=alpha, S_T=S_T, window=PAPER_WINDOW)),
+                     window=(3, 0, 1)), dict(alpha=alpha, S_T=S_T, window=(3, 0, 1))),
         ("token_gate", dict(gate_tokens=to_device(G, w.dtype), window=(3, 1, 0)),
          dict(G=G, window=(3, 1, 0))),
     ]

@@ -162,9 +162,11 @@ def test_raw_query_pipeline(V, d):
     gate = (1.0 / (1.0 + np.exp(-rng.standard_normal(B * H)))).astype(np.float32)
     alpha = (0.6 + 0.4 * rng.random((B * H, F, d))).astype(np.float32)
     qo, ko, vo = _oracle(x, grid, H)
+    # (a window must leave frames outside it: one covering the clip reads
+    # only the zero initial state)
     for name, opts, window in (("core", {}, (1, 0, 0)),
-                               ("decay+window", dict(alpha=_dev_f32(alpha), window=(5, 1, 1)),
-                                (5, 1, 1))):
+                               ("decay+window", dict(alpha=_dev_f32(alpha), window=(2, 0, 0)),
+                                (2, 0, 0))):
         y = V.forward(_dev_bf16(x["q"]), k, v, _dev_f32(beta), _dev_f32(gate), q_heads=H,
                       out_heads=H, **opts)
         torch.cuda.synchronize()
@@ -173,6 +175,7 @@ def test_raw_query_pipeline(V, d):
                                alpha.astype(np.float64) if opts else None, None, *window,
                                "joint")
         ref = ref.reshape(B, H, F, N, d).transpose(0, 2, 3, 1, 4).reshape(B, F, N, H * d)
+        assert np.abs(ref).max() > 0.1
         err = rel_max_err(from_device(y), ref)
         _log(f"  {name}: rel err {err:.2e}")
         assert err <= 2e-2, (name, err)
