@@ -117,12 +117,19 @@ void readout_bf16_kernel(const uint16_t* __restrict__ Q, const float* __restrict
   }
   lds_barrier();
 
-  bf16x8 sop[MB][KB];
+  // S~ as MFMA A-operands: held in registers on the frame-major path; the
+  // general-layout variant reads them from LDS at each group instead, which
+  // leaves it the registers for two query groups in flight.
+  constexpr bool kSopRegs = !GENOUT;
+  bf16x8 sop[kSopRegs ? MB : 1][kSopRegs ? KB : 1];
+  if constexpr (kSopRegs) {
 #pragma unroll
-  for (int mb = 0; mb < MB; ++mb)
+    for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-    for (int kb = 0; kb < KB; ++kb)
-      sop[mb][kb] = *reinterpret_cast<const bf16x8*>(&st[(mb * 16 + li) * SLD + kb * 32 + lg * 8]);
+      for (int kb = 0; kb < KB; ++kb)
+        sop[mb][kb] = *reinterpret_cast<const bf16x8*>(&st[(mb * 16 + li) * SLD + kb * 32 + lg * 8]);
+  }
+  const uint16_t* sop_lds = &st[li * SLD + lg * 8];
 
   // This frame's query rows: DK channels at row stride qh * DK, from head
   // h % qh of clip h / qh (frame-major per head when qh = 1).
@@ -145,9 +152,9 @@ void readout_bf16_kernel(const uint16_t* __restrict__ Q, const float* __restrict
   // Rows past the frame are clamped onto its last row (always valid
   // memory); their outputs are dropped by the range-checked stores, so
   // loads and stores need no branches.
-  // The gated and the general-output variants keep their extra registers in
-  // the budget with one group in flight.
-  constexpr int kQ = TOKGATE || GENOUT ? 1 : 2;
+  // The gated variant keeps its extra registers in the budget with one
+  // group in flight.
+  constexpr int kQ = TOKGATE ? 1 : 2;
   const int S = 64 * chunks;
   uint4 qr[kQ][KB];
   auto load_q = [&](int nq, uint4 (&qv)[KB]) {
@@ -182,12 +189,22 @@ void readout_bf16_kernel(const uint16_t* __restrict__ Q, const float* __restrict
       floatx4 acc[MB];
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb) acc[mb] = floatx4{0.f, 0.f, 0.f, 0.f};
+      // (An opaque zero offset keeps the compiler from hoisting the LDS
+      // operand reads out of the loop into registers.)
+      int zero_off = 0;
+      if constexpr (!kSopRegs) asm volatile("v_mov_b32 %0, 0" : "=v"(zero_off));
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb) {
         const bf16x8 qop = __builtin_bit_cast(bf16x8, qr[d][kb]);
 #pragma unroll
-        for (int mb = 0; mb < MB; ++mb)
-          acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sop[mb][kb], qop, acc[mb], 0, 0, 0);
+        for (int mb = 0; mb < MB; ++mb) {
+          bf16x8 aop;
+          if constexpr (kSopRegs)
+            aop = sop[mb][kb];
+          else
+            aop = *reinterpret_cast<const bf16x8*>(sop_lds + zero_off + mb * 16 * SLD + kb * 32);
+          acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aop, qop, acc[mb], 0, 0, 0);
+        }
       }
       // A raw query: |q|^2 of the lane's token from the operand registers
       // (the token's DK channels are spread over lanes li + 16 lg), so that
