@@ -117,10 +117,10 @@ void readout_bf16_kernel(const uint16_t* __restrict__ Q, const float* __restrict
   }
   lds_barrier();
 
-  // S~ as MFMA A-operands: held in registers on the frame-major path; the
-  // general-layout variant reads them from LDS at each group instead, which
-  // leaves it the registers for two query groups in flight.
-  constexpr bool kSopRegs = !GENOUT;
+  // S~ as MFMA A-operands: held in registers on the plain frame-major path;
+  // the gated and general-layout variants read them from LDS at each group
+  // instead, which leaves them the registers for two query groups in flight.
+  constexpr bool kSopRegs = !GENOUT && !TOKGATE;
   bf16x8 sop[kSopRegs ? MB : 1][kSopRegs ? KB : 1];
   if constexpr (kSopRegs) {
 #pragma unroll
@@ -152,9 +152,7 @@ void readout_bf16_kernel(const uint16_t* __restrict__ Q, const float* __restrict
   // Rows past the frame are clamped onto its last row (always valid
   // memory); their outputs are dropped by the range-checked stores, so
   // loads and stores need no branches.
-  // The gated variant keeps its extra registers in the budget with one
-  // group in flight.
-  constexpr int kQ = TOKGATE ? 1 : 2;
+  constexpr int kQ = 2;
   const int S = 64 * chunks;
   uint4 qr[kQ][KB];
   auto load_q = [&](int nq, uint4 (&qv)[KB]) {
