@@ -461,7 +461,7 @@ hipError_t launch_forward(const ForwardCall& C, char* base, hipStream_t stream) 
   }
   if (e == hipSuccess)
     e = vda::launch_frame_stats(C.is_f32, kx, vx, C.beta, F, N, H, pk, pv, C.plan, A_part, B_part,
-                                stream);
+                                stream, /*lower_only=*/!C.frozen);
   // With bf16 storage the joint rule's inverse is written as split-bf16
   // operand tiles for the state scan.
   if (e == hipSuccess && !C.frozen)

@@ -30,7 +30,8 @@
 // With several matrices' workgroups per SIMD, one wave's serial pivot work
 // also hides behind another matrix's products.
 // Both A_t and its inverse are symmetric, so the column segments of the
-// accumulator layout are loaded and stored as contiguous row segments of the
+// accumulator layout are loaded (for the blocks on and below the diagonal,
+// the only ones read) and stored as contiguous row segments of the
 // transposed block (the result is the transpose of the computed inverse,
 // which equals it up to rounding).
 // The token-split partials of A_t are summed in split order while loading
@@ -187,28 +188,34 @@ __device__ __forceinline__ void invert_rows(const float* A_part, int splits, siz
   const int lg = lane >> 4;
 
   // acc[q][j]: block (i, j) with i = WV + W q.  Its accumulator holds the
-  // column segment M[16i + 4lg .. +3][16j + li]; A_t is symmetric, so it is
-  // read as the contiguous row segment M[16j + li][16i + 4lg .. +3] with
-  // 16-byte loads (and the result is written back the same way).
+  // column segment M[16i + 4lg .. +3][16j + li].  Only the blocks of A_t on
+  // and below the diagonal are read (the statistics may leave the others
+  // unwritten): for j >= i, A_t is symmetric, so the segment is read as the
+  // contiguous row segment M[16j + li][16i + 4lg .. +3] of block (j, i) with
+  // one 16-byte load (and the result is written back the same way); for
+  // j < i, straight from block (i, j) as four scalars.
   // All blocks of this wave's rows of one partial are loaded in one memory
   // round trip: the first partial straight into the accumulators, each
   // further token range of a split frame into a staging set that is then
   // added in range order (one round trip per partial).
+  auto load_block = [&](const float* m, int i, int j) -> floatx4 {
+    if (j >= i)
+      return *reinterpret_cast<const floatx4*>(m + (size_t)(16 * j + li) * DK + 16 * i + 4 * lg);
+    const float* p = m + (size_t)(16 * i + 4 * lg) * DK + 16 * j + li;
+    return floatx4{p[0], p[DK], p[2 * DK], p[3 * DK]};
+  };
   floatx4 acc[RPW][NB];
-  const float* a0 = A_part + base + (size_t)li * DK + 4 * lg;
+  const float* a0 = A_part + base;
 #pragma unroll
   for (int q = 0; q < RPW; ++q)
 #pragma unroll
-    for (int j = 0; j < NB; ++j)
-      acc[q][j] = *reinterpret_cast<const floatx4*>(a0 + (16 * j) * DK + 16 * (WV + W * q));
+    for (int j = 0; j < NB; ++j) acc[q][j] = load_block(a0, WV + W * q, j);
   for (int s = 1; s < splits; ++s) {
     floatx4 x[RPW][NB];
 #pragma unroll
     for (int q = 0; q < RPW; ++q)
 #pragma unroll
-      for (int j = 0; j < NB; ++j)
-        x[q][j] = *reinterpret_cast<const floatx4*>(a0 + s * part_stride + (16 * j) * DK +
-                                                    16 * (WV + W * q));
+      for (int j = 0; j < NB; ++j) x[q][j] = load_block(a0 + s * part_stride, WV + W * q, j);
 #pragma unroll
     for (int q = 0; q < RPW; ++q)
 #pragma unroll

@@ -25,14 +25,18 @@ inline long long stats_workgroups(long long count, SplitPlan plan) {
 // Statistics workgroups one compute unit holds at once (occupancy query).
 int stats_blocks_per_cu(bool is_f32, int d_k, int d_v);
 
-// Step a1, Eq. 3b: partial frame statistics per token range.
+// Step a1, Eq. 3b: partial frame statistics per token range.  lower_only
+// (bf16 storage): A_t's blocks above the diagonal are left unwritten, for a
+// caller whose only reader of A_t is launch_frame_inverse.
 hipError_t launch_frame_stats(bool is_f32, const void* k, const void* v, const float* beta,
                               int F, int N, int H, int d_k, int d_v, SplitPlan plan,
-                              float* A_part, float* B_part, hipStream_t stream);
+                              float* A_part, float* B_part, hipStream_t stream,
+                              bool lower_only = false);
 
 // Step a2, Eq. 5: Inv = (I + sum of A partials)^{-1} (fp32 matrices, or
 // split-bf16 operand tiles when `tiled`); also folds the B partials of every
-// split frame into its first partial.
+// split frame into its first partial.  It reads only A_t's blocks on and
+// below the diagonal.
 hipError_t launch_frame_inverse(const float* A_part, float* B_part, SplitPlan plan,
                                 long long count, int d_k, int d_v, bool tiled, float* Inv,
                                 hipStream_t stream);

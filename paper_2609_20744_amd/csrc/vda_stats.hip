@@ -3,7 +3,11 @@
 //
 // One workgroup per frame (and token range).  A_t is symmetric, so only its
 // blocks on or above the diagonal are accumulated (16 x 16 blocks (i, j),
-// i <= j) and each off-diagonal block is also written transposed.  The four
+// i <= j); each is written transposed to block (j, i), on or below the
+// diagonal (the diagonal blocks as their own transposes), and the blocks
+// above the diagonal as they are.  When the inverse is A_t's only reader
+// (lower_only), those above the diagonal are not stored: the inverse reads
+// only the blocks on and below it.  The four
 // waves split the work by output columns (channels of beta*k): with 8 column
 // blocks, wave w owns columns w and 7 - w, which carry (w + 1) + (8 - w)
 // upper-triangle blocks of A_t and 2 * d_v / 16 blocks of B_t: the same count
@@ -148,7 +152,7 @@ struct StatsFrame {
 
   // The whole token loop and the output stores of wave W.
   template <int W>
-  __device__ void run(int n_begin, int n_end, float* Ab, float* Bb) const {
+  __device__ void run(int n_begin, int n_end, float* Ab, float* Bb, bool lower_only) const {
     using P = WavePlan<DK / 16, DV / 16, W>;
     constexpr int NC = P::ncols;
     floatx4 accA[NC][DK / 16];  // [column c][row block i], i <= col(c)
@@ -216,11 +220,15 @@ struct StatsFrame {
 #pragma unroll
         for (int i = 0; i <= P::imax; ++i) {
           if (i <= P::col(c)) {
+            // Block (j, i), on or below the diagonal, as the transpose of the
+            // accumulated block (i, j); the diagonal blocks too, so that the
+            // blocks the inverse reads are the same in both modes.
+            *reinterpret_cast<floatx4*>(&Ab[(j * 16 + li) * DK + i * 16 + lg * 4]) = accA[c][i];
+            if (!lower_only && i < P::col(c)) {
 #pragma unroll
-            for (int e = 0; e < 4; ++e)
-              Ab[(i * 16 + lg * 4 + e) * DK + j * 16 + li] = accA[c][i][e];
-            if (i < P::col(c))
-              *reinterpret_cast<floatx4*>(&Ab[(j * 16 + li) * DK + i * 16 + lg * 4]) = accA[c][i];
+              for (int e = 0; e < 4; ++e)
+                Ab[(i * 16 + lg * 4 + e) * DK + j * 16 + li] = accA[c][i][e];
+            }
           }
         }
       }
@@ -238,7 +246,7 @@ __global__ __launch_bounds__(kThreads, 2)
 void stats_bf16_kernel(const uint16_t* __restrict__ K, const uint16_t* __restrict__ V,
                        const float* __restrict__ beta, int N, int tokens_per_split,
                        unsigned tail, int splits, unsigned fh_count,
-                       float* __restrict__ A_part, float* __restrict__ B_part) {
+                       float* __restrict__ A_part, float* __restrict__ B_part, int lower_only) {
   using S = StatsFrame<DK, DV>;
   __shared__ __align__(16) uint16_t kt[kStatsTile * S::LDK];
   __shared__ __align__(16) uint16_t yt[kStatsTile * S::LDK];
@@ -275,10 +283,10 @@ void stats_bf16_kernel(const uint16_t* __restrict__ K, const uint16_t* __restric
   float* Bb = B_part + (size_t)slot * (DV * DK);
   // Every branch runs the same number of barriers.
   switch (wave) {
-    case 0: s.template run<0>(n_begin, n_end, Ab, Bb); break;
-    case 1: s.template run<1>(n_begin, n_end, Ab, Bb); break;
-    case 2: s.template run<2>(n_begin, n_end, Ab, Bb); break;
-    default: s.template run<3>(n_begin, n_end, Ab, Bb); break;
+    case 0: s.template run<0>(n_begin, n_end, Ab, Bb, lower_only != 0); break;
+    case 1: s.template run<1>(n_begin, n_end, Ab, Bb, lower_only != 0); break;
+    case 2: s.template run<2>(n_begin, n_end, Ab, Bb, lower_only != 0); break;
+    default: s.template run<3>(n_begin, n_end, Ab, Bb, lower_only != 0); break;
   }
 }
 
@@ -380,7 +388,7 @@ int blocks_per_cu_t(bool is_f32) {
 template <int DK, int DV>
 hipError_t launch_stats_t(bool is_f32, const void* k, const void* v, const float* beta,
                           int F, int N, int H, SplitPlan plan, float* A_part, float* B_part,
-                          hipStream_t stream) {
+                          bool lower_only, hipStream_t stream) {
   const unsigned fh_count = (unsigned)H * (unsigned)F;
   const int splits = plan.splits > 1 && plan.tail > 0 ? plan.splits : 1;
   const unsigned tail = splits > 1 ? (unsigned)plan.tail : 0u;
@@ -393,7 +401,7 @@ hipError_t launch_stats_t(bool is_f32, const void* k, const void* v, const float
   } else {
     hipLaunchKernelGGL((stats_bf16_kernel<DK, DV>), grid, dim3(kThreads), 0, stream,
                        static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v), beta, N,
-                       tps, tail, splits, fh_count, A_part, B_part);
+                       tps, tail, splits, fh_count, A_part, B_part, (int)lower_only);
   }
   return hipGetLastError();
 }
@@ -412,11 +420,12 @@ int stats_blocks_per_cu(bool is_f32, int d_k, int d_v) {
 
 hipError_t launch_frame_stats(bool is_f32, const void* k, const void* v, const float* beta,
                               int F, int N, int H, int d_k, int d_v, SplitPlan plan,
-                              float* A_part, float* B_part, hipStream_t stream) {
+                              float* A_part, float* B_part, hipStream_t stream,
+                              bool lower_only) {
 #define VDA_STATS_CASE(DKV, DVV)                                                       \
   if (d_k == DKV && d_v == DVV)                                                        \
     return launch_stats_t<DKV, DVV>(is_f32, k, v, beta, F, N, H, plan, A_part, B_part, \
-                                    stream);
+                                    lower_only, stream);
   VDA_STATS_CASE(32, 32) VDA_STATS_CASE(32, 64) VDA_STATS_CASE(32, 128)
   VDA_STATS_CASE(64, 32) VDA_STATS_CASE(64, 64) VDA_STATS_CASE(64, 128)
   VDA_STATS_CASE(128, 32) VDA_STATS_CASE(128, 64) VDA_STATS_CASE(128, 128)
