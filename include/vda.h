@@ -394,7 +394,9 @@ int vda_frame_stats(const void* k, const void* v, const float* beta,
  * partials)^{-1} for i < count, under the split plan (tail_frames, splits)
  * that produced the partials, in fp32 by blocked Gauss-Jordan elimination
  * without pivoting (I + A is symmetric positive definite with eigenvalues
- * >= 1 when beta >= 0).  Inv is [count][d_k][d_k].  Inv may alias A_part
+ * >= 1 when beta >= 0).  A_t is symmetric, and only its 16 x 16 blocks on
+ * and below the diagonal are read (the others are taken as their transposes;
+ * vda_frame_stats writes the whole matrix).  Inv is [count][d_k][d_k].  Inv may alias A_part
  * (in place onto the first count matrices); it must not overlap any other
  * partial.  When splits > 1 the call also folds the partials of B in place
  * (B_part[i] = sum of frame i's B partials; B_part as in vda_frame_stats;
