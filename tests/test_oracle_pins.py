@@ -817,6 +817,26 @@ def pin_prep_filters_commute():
     np.testing.assert_allclose(O.depthwise_conv3(x, ws, wt), two_pass, rtol=1e-12, atol=1e-12)
 
 
+def pin_query_l2_folds_into_rmsnorm():
+    """Section 2.3 with Eq. 1c: the readout is linear in the query and RMSNorm
+    is scale-invariant up to its epsilon, so with the raw query q and
+    n = |q|^2 + eps_l2, RMSNorm(S (q / sqrt(n))) = S q / sqrt(mean((S q)^2) +
+    eps_rms n) times the gate: the form in which a readout of the raw query
+    applies the L2 map.  Checked on scales from 1e-3 to 1e3 and a zero query
+    (whose output is zero either way)."""
+    rng = _rng(45)
+    S = rng.standard_normal((6, 5))
+    q = rng.standard_normal((9, 5)) * np.exp(rng.uniform(-7.0, 7.0, (9, 1)))
+    q[4] = 0.0
+    eps_rms = O.RMS_EPS
+    y = O.rmsnorm_gate(O.readout(S, O.l2_normalise(q)), 0.7, eps=eps_rms)
+    o = q @ S.T
+    n = np.sum(q * q, axis=-1, keepdims=True) + O.L2_EPS
+    folded = 0.7 * o / np.sqrt(np.mean(o * o, axis=-1, keepdims=True) + eps_rms * n)
+    np.testing.assert_allclose(y, folded, rtol=1e-12, atol=1e-15)
+    assert np.all(y[4] == 0.0)
+
+
 PINS = [f for name, f in sorted(globals().items()) if name.startswith("pin_")]
 
 
