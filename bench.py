@@ -635,6 +635,9 @@ def main() -> int:
                          "time and throughput, and the oracle at one and at all BLAS threads")
     ap.add_argument("--no-extras", action="store_true",
                     help="time only the headline and the per-kernel launches")
+    ap.add_argument("--prep-only", action="store_true",
+                    help="instead of the headline line, time only VDA-Prep and the two ways from "
+                         "the projections to the token-major output on the workload's shape")
     args = ap.parse_args()
     if args.pmc_summary:
         print(json.dumps(pmc_summary(*args.pmc_summary, args.copy_gib, args.workload), indent=1))
@@ -676,6 +679,10 @@ def main() -> int:
         all_workloads(vda, torch, args.steps, args.warmup, args.settle, args.cpu_budget)
         return 0
     w = I.WORKLOADS[args.workload]
+    if args.prep_only:
+        print(json.dumps({"workload": w.name, "prep": prep_bench(vda, torch, w, args.steps)}),
+              flush=True)
+        return 0
     print(f"[bench] generating {w.name} inputs", file=sys.stderr, flush=True)
     x = I.make_inputs(w)
     sets = device_sets(torch, w, x, input_copies(w))

@@ -181,6 +181,7 @@ void prep_conv_kernel(PrepConvArgs a) {
   // Output tokens of this wave: grid row y0 + wave, columns x0 .. x0 + 7.
   const int oy = y0 + wave;
   uint16_t* obase = a.out + ((size_t)(b * H + h) * F) * N * D;
+  const __amdgpu_buffer_rsrc_t orsrc = make_rsrc(obase, (uint32_t)((size_t)F * N * D * 2));
   // Running sums of the pending output frames: output frame o lives in
   // slot o % 5.  Slots start at zero (outputs 0 and 1 take their first
   // terms by accumulation); the slot of output f + 2 is set, not added to,
@@ -263,11 +264,16 @@ void prep_conv_kernel(PrepConvArgs a) {
 #pragma unroll
         for (int x = 0; x < kPTX; ++x) {
           if (x0 + x < gw) {
-            uint16_t* dst = obase + ((size_t)o * N + oy * gw + x0 + x) * D + lane * CPL;
+            // Streamed stores (sc0 | nt | sc1): the features are read by the
+            // next kernels, not kept dirty in the caches for them to evict.
+            const uint32_t off = (uint32_t)((((size_t)o * N + oy * gw + x0 + x) * D + lane * CPL) * 2);
             if constexpr (CPL == 2)
-              *reinterpret_cast<uint32_t*>(dst) = pack_bf16x2(y[x][0] * scale[x], y[x][1] * scale[x]);
+              __builtin_amdgcn_raw_buffer_store_b32(pack_bf16x2(y[x][0] * scale[x], y[x][1] * scale[x]),
+                                                    orsrc, (int)off, 0, 1 | 2 | 16);
             else
-              *dst = (uint16_t)(pack_bf16x2(y[x][0] * scale[x], 0.f) & 0xffffu);
+              __builtin_amdgcn_raw_buffer_store_b16(
+                  (uint16_t)(pack_bf16x2(y[x][0] * scale[x], 0.f) & 0xffffu), orsrc, (int)off, 0,
+                  1 | 2 | 16);
           }
         }
       }
@@ -339,12 +345,15 @@ void prep_qnorm_kernel(const uint16_t* __restrict__ in, uint16_t* __restrict__ o
 #pragma unroll
   for (int m = LPT / 2; m >= 1; m >>= 1) ss += __shfl_xor(ss, m);
   const float sc = rsqrtf(ss + kL2Eps);
-  if (ok) {
-    const long long b = bf / F, f = bf % F;
-    uint16_t* dst = out + (((size_t)(b * H + h) * F + f) * N + n) * D + j * 8;
-    *reinterpret_cast<uint4*>(dst) = make_uint4(pack_bf16x2(x[0] * sc, x[1] * sc), pack_bf16x2(x[2] * sc, x[3] * sc),
-                                                pack_bf16x2(x[4] * sc, x[5] * sc), pack_bf16x2(x[6] * sc, x[7] * sc));
-  }
+  // This wave's TPW output rows, streamed (sc0 | nt | sc1) like the
+  // convolutions' outputs; rows past the frame fall outside the range.
+  const long long b = bf / F, f = bf % F;
+  const uint16_t* wbase = out + (((size_t)(b * H + h) * F + f) * N + (size_t)nb * TPW) * D;
+  const __amdgpu_buffer_rsrc_t orsrc =
+      make_rsrc(wbase, (uint32_t)((min(N - nb * TPW, TPW)) * D * 2));
+  const u32x4 packed = {pack_bf16x2(x[0] * sc, x[1] * sc), pack_bf16x2(x[2] * sc, x[3] * sc),
+                        pack_bf16x2(x[4] * sc, x[5] * sc), pack_bf16x2(x[6] * sc, x[7] * sc)};
+  store_b128_stream(orsrc, ok ? (uint32_t)((t * D + j * 8) * 2) : kOutOfRange, packed);
 }
 
 template <int D, bool NORM>
